@@ -1,0 +1,201 @@
+/*
+ * hetegen.h - C ABI of the MI355X heterogeneous-parallel Linear (HeteGen,
+ * arXiv 2403.01164) for batch-1..8 decoding.
+ *
+ * A linear module y = x W^T + b with its weight W [N, K] in pinned host memory
+ * is split by output feature: the leading rows [0, n_gpu) are computed on the
+ * GPU (resident in HBM, or streamed host-to-device in chunks), the trailing rows
+ * [n_gpu, N) on host cores, and both parts land in one device output
+ * (Sec. 3.1 "Parallelism Strategy", Fig. 3a, Eq. 2: heterogeneous tensor
+ * parallelism partitions the weight; Sec. 4.2, Fig. 5a: activation to the CPU,
+ * CPU compute concurrent with weight transfer, CPU outputs back to the GPU).
+ *
+ * Conventions used by every call:
+ *  - alpha is the CPU fraction of the output features:
+ *        n_cpu = min(N, floor(alpha * N + 0.5)),  n_gpu = N - n_cpu.
+ *    The paper's alpha (Sec. 3.2) is the GPU fraction, i.e. 1 - alpha here.
+ *  - Matrices are row-major.  W has N rows of K elements (nn.Linear layout).
+ *    x is [B, K], y is [B, N]; row strides are given in elements.
+ *  - Element types: HETEGEN_F16 (IEEE binary16), HETEGEN_BF16, HETEGEN_F32.
+ *    Weights, activations and biases of one call share one 16-bit type;
+ *    accumulation is binary32.
+ *  - Streams are hipStream_t values passed as void*; NULL is the null stream.
+ *  - Every call returns a status and never throws or aborts across the ABI.
+ *    On failure hetegen_last_error() describes the error; outputs are undefined.
+ *  - A context is not thread-safe: one in-flight call per context.
+ */
+#ifndef HETEGEN_H
+#define HETEGEN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HETEGEN_API __attribute__((visibility("default")))
+
+typedef enum {
+  HETEGEN_OK = 0,
+  HETEGEN_ERR_INVALID_ARG = 1, /* null pointer, bad size, alpha outside [0,1] or not finite */
+  HETEGEN_ERR_NOT_PINNED = 2,  /* a host weight buffer is not page-locked host memory */
+  HETEGEN_ERR_UNSUPPORTED = 3, /* K % 8 != 0, B outside [1, 8], misaligned pointer, dtype mix */
+  HETEGEN_ERR_OOM = 4,         /* device or pinned host allocation failed */
+  HETEGEN_ERR_HIP = 5          /* a HIP runtime call failed (code in the message) */
+} hetegen_status;
+
+typedef enum { HETEGEN_F16 = 0, HETEGEN_BF16 = 1, HETEGEN_F32 = 2 } hetegen_dtype;
+
+typedef struct hetegen_ctx hetegen_ctx;
+typedef struct hetegen_model hetegen_model;
+
+typedef struct {
+  int device;         /* HIP device ordinal */
+  int cpu_threads;    /* host threads for the CPU share; <= 0: the OpenMP default */
+  size_t chunk_bytes; /* weight bytes per streamed chunk; 0: 32 MiB */
+  int ring_depth;     /* device staging slots for streamed chunks, in [2, 64]; 0: 8 */
+} hetegen_config;
+
+/* Create a context on cfg->device: a copy stream, the staging ring
+ * (ring_depth x chunk_bytes of HBM), pinned hand-off buffers and events.
+ * cfg may be NULL (device 0, defaults).  *out receives the context. */
+HETEGEN_API hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out);
+
+/* Wait for the context's work and free everything it owns.  NULL is a no-op. */
+HETEGEN_API hetegen_status hetegen_destroy(hetegen_ctx* ctx);
+
+/* Message of the last failing call on ctx ("" if none).  With ctx == NULL, the
+ * message of the last failing hetegen_create on this thread.  The string stays
+ * valid until the next call on ctx. */
+HETEGEN_API const char* hetegen_last_error(const hetegen_ctx* ctx);
+
+/* Page-locked host memory for weights: *p receives `bytes` bytes that the CPU
+ * share reads directly and the copy engines read over PCIe (not write-combined).
+ * Free with hetegen_host_free.  OOM if the allocation fails. */
+HETEGEN_API hetegen_status hetegen_host_alloc(hetegen_ctx* ctx, size_t bytes, void** p);
+HETEGEN_API hetegen_status hetegen_host_free(hetegen_ctx* ctx, void* p);
+
+/* One heterogeneous linear module (Sec. 3.1, Eq. 2; Sec. 4.2, Fig. 5a):
+ *
+ *   y[b, j] = sum_k x[b, k] * W[j, k] + bias[j],   b < B, j < N,
+ *
+ * rows j < n_gpu on the GPU, rows j >= n_gpu on host threads (see alpha above).
+ *   x_dev          device, [B, K] in w_dtype, row stride K, 16-byte aligned.
+ *   W_host         pinned host (hetegen_host_alloc or hipHostMalloc), [N, K] w_dtype.
+ *   W_dev_resident optional device copy of rows [0, n_gpu) (row stride K); when
+ *                  NULL the GPU rows are streamed from W_host through the staging
+ *                  ring in chunks, overlapped with the CPU share.
+ *   bias_host      optional host [N] w_dtype, read for the CPU rows;
+ *   bias_dev       optional device [N] w_dtype, read for the GPU rows.  Pass both
+ *                  or neither (a side with rows needs its pointer).
+ *   y_dev          device [B, N] of y_dtype (w_dtype or HETEGEN_F32), row stride N.
+ * GPU work is enqueued on `stream`.  The call returns after the CPU share is
+ * computed and its upload is enqueued; y is complete in `stream` order.
+ * B in [1, 8], K % 8 == 0, K >= 8, N >= 1.  W_host must be pinned (NOT_PINNED). */
+HETEGEN_API hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K, const void* W_host,
+                              const void* W_dev_resident, int N, hetegen_dtype w_dtype,
+                              const void* bias_host, const void* bias_dev, double alpha, void* y_dev,
+                              hetegen_dtype y_dtype, void* stream);
+
+/* ---- Alpha planner: computation distribution law (Sec. 3.2, Eq. 4-7; Eq. 8-9) ---- */
+
+typedef struct {
+  int N, K;            /* weight shape */
+  hetegen_dtype dtype; /* element type of W */
+  int resident;        /* 1: the whole module stays on the GPU (alpha = 0) */
+} hetegen_shape;
+
+/* Speeds in weight bytes per second (the paper's "parameter size divided by
+ * processing time", Fig. 1 caption). */
+typedef struct {
+  double cpu_Bps;      /* V_CPU: CPU share GEMV */
+  double h2d_Bps;      /* V_COM transfer part: pinned host-to-device copy */
+  double hbm_gemv_Bps; /* V_GPU: GPU GEMV */
+  double pin_Bps;      /* pinning speed for pageable weights; <= 0: weights pre-pinned */
+} hetegen_bw;
+
+#define HETEGEN_PLAN_APPROX 1 /* use Eq. 6/7 (GPU time neglected) instead of Eq. 5 */
+
+/* alpha_out[i] = CPU fraction for shapes[i]:
+ *   resident -> 0, otherwise clamp(1 - alpha_gpu, 0, 1) with
+ *   alpha_gpu = V_GPU V_COM / (V_CPU V_GPU + V_CPU V_COM + V_COM V_GPU)   (Eq. 5)
+ *   or V_COM / (V_COM + V_CPU) with HETEGEN_PLAN_APPROX                    (Eq. 6)
+ *   where V_COM = min(h2d_Bps, pin_Bps) when pin_Bps > 0 (Eq. 8: T_COM = max(T_PIN, T_TRANS)).
+ * bw holds n_bw == n entries (one per shape) or n_bw == 1 (shared).  Speeds must
+ * be finite and > 0.  Pure host arithmetic; no device is touched. */
+HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n, const hetegen_bw* bw, int n_bw,
+                                  int flags, double* alpha_out);
+
+/* Measure V_CPU, V_COM and V_GPU for one shape on this context (the inputs of the
+ * distribution law): the CPU share GEMV over all N rows of W_host (alpha = 1), the
+ * chunked host-to-device copy of W_host through the staging ring, and the GPU
+ * GEMV over the staged chunks; each is the median of `reps` runs in weight bytes
+ * per second.  W_host is pinned [N, K]; batch B.  pin_Bps is set to 0. */
+HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
+                             int B, int reps, hetegen_bw* out);
+
+/* ---- Decode step over a stack of decoder layers (Sec. 4.2: heterogeneous
+ * linears, every other module on the GPU) ----
+ *
+ * Layer l owns four linears in the order qkv [3H, H], out [H, H], fc1 [F, H],
+ * fc2 [H, F]; linear i = 4 l + m.  One step maps x [B, H] to out [B, H]:
+ *   h = LN(x); q = qkv(h); a = q[:, 2H:3H]; x = x + out(a);
+ *   h = LN(x); f = ReLU(fc1(h)); x = x + fc2(f)
+ * with LN a LayerNorm over H without affine terms (eps 1e-5), every
+ * intermediate stored in the model's 16-bit type (round to nearest even) and
+ * a value-only attention (one position, empty KV cache: the result is V). */
+
+/* W_host[i], bias_host[i]: pinned host weights and host biases of linear i
+ * (caller-owned, must outlive the model).  alpha[i]: CPU fraction of linear i.
+ * resident[i] != 0: rows [0, n_gpu) of linear i are copied to HBM at creation;
+ * otherwise they are streamed every step.  max_batch in [1, 8]. */
+HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
+                                    void* const* W_host, void* const* bias_host, const double* alpha,
+                                    const int* resident, int max_batch, hetegen_model** out);
+
+/* Replace the CPU fractions of the non-resident linears (alpha[i] ignored for a
+ * resident linear; its split is fixed at creation). */
+HETEGEN_API hetegen_status hetegen_model_set_alpha(hetegen_model* model, const double* alpha);
+
+/* One decode step: out_dev [B, H] = step(x_dev [B, H]); both device, model dtype,
+ * 16-byte aligned; out_dev may not alias x_dev.  GPU work is enqueued on `stream`;
+ * the call returns after the last CPU share.  When every linear is GPU-only and
+ * resident, the step is captured once into a HIP graph per (B, x_dev, out_dev,
+ * stream) and replayed. */
+HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* model, const void* x_dev,
+                                   void* out_dev, int B, void* stream);
+
+/* Optional trace of every linear's input and output (model dtype), for
+ * teacher-forced checks.  Linear i writes its input [B, K_i] and then its output
+ * [B, N_i] (after the fused ReLU or residual sum), packed in order of i; the
+ * required size for batch B is hetegen_model_trace_bytes().  trace_dev == NULL
+ * turns tracing off.  Tracing disables the graph replay. */
+HETEGEN_API size_t hetegen_model_trace_bytes(const hetegen_model* model, int B);
+HETEGEN_API hetegen_status hetegen_model_set_trace(hetegen_model* model, void* trace_dev, size_t bytes);
+
+HETEGEN_API hetegen_status hetegen_model_destroy(hetegen_ctx* ctx, hetegen_model* model);
+
+/* ---- Per-resource busy times (the Table 2 breakdown) ---- */
+
+typedef struct {
+  double wall_ms;      /* host wall time inside hetegen_linear / hetegen_decode_step */
+  double cpu_ms;       /* host time computing CPU shares */
+  double h2d_ms;       /* copy-stream time moving streamed weight chunks */
+  double gpu_ms;       /* GPU GEMV kernel time (events around each launch) */
+  double h2d_bytes;    /* weight bytes streamed */
+  double gpu_bytes;    /* weight bytes read by GPU GEMV launches */
+  double cpu_bytes;    /* weight bytes read by CPU shares */
+  int64_t gemv_launches;
+} hetegen_profile;
+
+/* on != 0: bracket every chunk copy and GEMV launch with events and synchronise at
+ * the end of each call to accumulate the times (adds overhead; for measurement). */
+HETEGEN_API hetegen_status hetegen_set_profiling(hetegen_ctx* ctx, int on);
+HETEGEN_API hetegen_status hetegen_get_profile(hetegen_ctx* ctx, hetegen_profile* out, int reset);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HETEGEN_H */

@@ -1,0 +1,198 @@
+"""Python binding of the heterogeneous-parallel Linear C ABI (include/hetegen.h).
+
+Argument marshalling only: every step of the path runs in libhetegen.so (gfx950
+kernels and the host runtime).  Pointers are plain integers (device addresses,
+for instance ``tensor.data_ptr()``, or pinned host addresses); streams are
+``hipStream_t`` values as integers (``torch.cuda.current_stream().cuda_stream``).
+Importing fails loudly when the library has not been built.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhetegen.so")
+
+F16, BF16, F32 = 0, 1, 2
+OK, ERR_INVALID_ARG, ERR_NOT_PINNED, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP = range(6)
+PLAN_APPROX = 1
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "NOT_PINNED", 3: "UNSUPPORTED", 4: "OOM", 5: "HIP"}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libhetegen.so is not built: run `python -m paper_2403_01164_amd.build` "
+                      "(or __graft_entry__.build())")
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("device", ctypes.c_int), ("cpu_threads", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
+                ("ring_depth", ctypes.c_int)]
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int), ("K", ctypes.c_int), ("dtype", ctypes.c_int), ("resident", ctypes.c_int)]
+
+
+class Bw(ctypes.Structure):
+    _fields_ = [("cpu_Bps", ctypes.c_double), ("h2d_Bps", ctypes.c_double), ("hbm_gemv_Bps", ctypes.c_double),
+                ("pin_Bps", ctypes.c_double)]
+
+
+class Profile(ctypes.Structure):
+    _fields_ = [("wall_ms", ctypes.c_double), ("cpu_ms", ctypes.c_double), ("h2d_ms", ctypes.c_double),
+                ("gpu_ms", ctypes.c_double), ("h2d_bytes", ctypes.c_double), ("gpu_bytes", ctypes.c_double),
+                ("cpu_bytes", ctypes.c_double), ("gemv_launches", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib = ctypes.CDLL(LIB_PATH)
+_vp, _i, _d, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_size_t
+_SIGS = {
+    "hetegen_create": ([ctypes.POINTER(Config), ctypes.POINTER(_vp)], _i),
+    "hetegen_destroy": ([_vp], _i),
+    "hetegen_last_error": ([_vp], ctypes.c_char_p),
+    "hetegen_host_alloc": ([_vp, _sz, ctypes.POINTER(_vp)], _i),
+    "hetegen_host_free": ([_vp, _vp], _i),
+    "hetegen_linear": ([_vp, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _d, _vp, _i, _vp], _i),
+    "hetegen_layer_plan": ([ctypes.POINTER(Shape), _i, ctypes.POINTER(Bw), _i, _i, ctypes.POINTER(_d)], _i),
+    "hetegen_probe": ([_vp, _vp, _i, _i, _i, _i, _i, ctypes.POINTER(Bw)], _i),
+    "hetegen_model_create": ([_vp, _i, _i, _i, _i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_d),
+                              ctypes.POINTER(_i), _i, ctypes.POINTER(_vp)], _i),
+    "hetegen_model_set_alpha": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_decode_step": ([_vp, _vp, _vp, _vp, _i, _vp], _i),
+    "hetegen_model_trace_bytes": ([_vp, _i], _sz),
+    "hetegen_model_set_trace": ([_vp, _vp, _sz], _i),
+    "hetegen_model_destroy": ([_vp, _vp], _i),
+    "hetegen_set_profiling": ([_vp, _i], _i),
+    "hetegen_get_profile": ([_vp, ctypes.POINTER(Profile), _i], _i),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+EXPORTED = tuple(_SIGS)
+
+
+class HetegenError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), message))
+        self.status = status
+
+
+def _check(rc, ctx=None):
+    if rc != OK:
+        msg = _lib.hetegen_last_error(ctx)
+        raise HetegenError(rc, msg.decode() if msg else "")
+
+
+def hetegen_create(device=0, cpu_threads=0, chunk_bytes=0, ring_depth=0):
+    cfg = Config(device, cpu_threads, chunk_bytes, ring_depth)
+    out = _vp()
+    _check(_lib.hetegen_create(ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def hetegen_destroy(ctx):
+    _check(_lib.hetegen_destroy(ctx))
+
+
+def hetegen_last_error(ctx):
+    m = _lib.hetegen_last_error(ctx)
+    return m.decode() if m else ""
+
+
+def hetegen_host_alloc(ctx, nbytes):
+    p = _vp()
+    _check(_lib.hetegen_host_alloc(ctx, nbytes, ctypes.byref(p)), ctx)
+    return p.value
+
+
+def hetegen_host_free(ctx, ptr):
+    _check(_lib.hetegen_host_free(ctx, ptr), ctx)
+
+
+def hetegen_linear(ctx, x_dev, B, K, W_host, W_dev_resident, N, w_dtype, bias_host, bias_dev, alpha, y_dev,
+                   y_dtype, stream=0):
+    _check(_lib.hetegen_linear(ctx, x_dev, B, K, W_host, W_dev_resident or None, N, w_dtype, bias_host or None,
+                               bias_dev or None, float(alpha), y_dev, y_dtype, stream or None), ctx)
+
+
+def hetegen_linear_status(ctx, *args):
+    """Same arguments as hetegen_linear; returns the raw status instead of raising."""
+    (x_dev, B, K, W_host, W_dev_resident, N, w_dtype, bias_host, bias_dev, alpha, y_dev, y_dtype, stream) = args
+    return _lib.hetegen_linear(ctx, x_dev, B, K, W_host, W_dev_resident or None, N, w_dtype, bias_host or None,
+                               bias_dev or None, float(alpha), y_dev, y_dtype, stream or None)
+
+
+def hetegen_layer_plan(shapes, bws, flags=0):
+    """shapes: list of (N, K, dtype, resident); bws: list of (cpu, h2d, hbm, pin) bytes/s, one or len(shapes)."""
+    n = len(shapes)
+    sh = (Shape * max(n, 1))(*[Shape(*s) for s in shapes])
+    bw = (Bw * len(bws))(*[Bw(*b) for b in bws])
+    out = (_d * max(n, 1))()
+    rc = _lib.hetegen_layer_plan(sh, n, bw, len(bws), flags, out)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_layer_plan")
+    return [out[i] for i in range(n)]
+
+
+def hetegen_probe(ctx, W_host, N, K, dtype, B=1, reps=3):
+    bw = Bw()
+    _check(_lib.hetegen_probe(ctx, W_host, N, K, dtype, B, reps, ctypes.byref(bw)), ctx)
+    return {"cpu_Bps": bw.cpu_Bps, "h2d_Bps": bw.h2d_Bps, "hbm_gemv_Bps": bw.hbm_gemv_Bps, "pin_Bps": bw.pin_Bps}
+
+
+def hetegen_model_create(ctx, L, H, F, dtype, W_host, bias_host, alpha, resident, max_batch=1):
+    n = 4 * L
+    W = (_vp * n)(*W_host)
+    b = (_vp * n)(*bias_host) if bias_host is not None else None
+    a = (_d * n)(*[float(v) for v in alpha])
+    r = (_i * n)(*[int(v) for v in resident])
+    out = _vp()
+    _check(_lib.hetegen_model_create(ctx, L, H, F, dtype, W, b, a, r, max_batch, ctypes.byref(out)), ctx)
+    return out.value
+
+
+def hetegen_model_set_alpha(model, alpha):
+    a = (_d * len(alpha))(*[float(v) for v in alpha])
+    rc = _lib.hetegen_model_set_alpha(model, a)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_model_set_alpha")
+
+
+def hetegen_decode_step(ctx, model, x_dev, out_dev, B, stream=0):
+    _check(_lib.hetegen_decode_step(ctx, model, x_dev, out_dev, B, stream or None), ctx)
+
+
+def hetegen_model_trace_bytes(model, B):
+    return _lib.hetegen_model_trace_bytes(model, B)
+
+
+def hetegen_model_set_trace(model, trace_dev, nbytes):
+    rc = _lib.hetegen_model_set_trace(model, trace_dev or None, nbytes)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_model_set_trace")
+
+
+def hetegen_model_destroy(ctx, model):
+    _check(_lib.hetegen_model_destroy(ctx, model), ctx)
+
+
+def hetegen_set_profiling(ctx, on):
+    _check(_lib.hetegen_set_profiling(ctx, int(bool(on))), ctx)
+
+
+def hetegen_get_profile(ctx, reset=False):
+    p = Profile()
+    _check(_lib.hetegen_get_profile(ctx, ctypes.byref(p), int(bool(reset))), ctx)
+    return p.as_dict()
+
+
+def host_view(ptr, shape, np_dtype):
+    """numpy view of pinned host memory at address ptr (no copy)."""
+    count = int(np.prod(shape))
+    buf = (ctypes.c_char * (count * np.dtype(np_dtype).itemsize)).from_address(ptr)
+    return np.frombuffer(buf, dtype=np_dtype, count=count).reshape(shape)

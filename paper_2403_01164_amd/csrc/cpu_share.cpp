@@ -1,0 +1,221 @@
+// CPU share of the heterogeneous Linear (HeteGen Sec. 3.2: the CPU computes the
+// part of the module whose parameters stay in host memory, concurrently with the
+// transfer and GPU compute of the other part; Sec. 5 runs it on host cores).
+//
+// Each thread takes a contiguous block of output rows (static schedule), so it
+// streams whole weight rows sequentially from DRAM.  A row block of R rows is
+// processed together so that each binary32 x vector loaded from cache is used R
+// times; 16-bit weights are widened to binary32 in registers (vcvtph2ps for fp16,
+// a 16-bit shift for bf16) and accumulated with FMA.  The instruction set is
+// chosen at run time (AVX-512, else AVX2+F16C+FMA, else portable C), so one build
+// runs on any x86-64 host.
+#include "cpu_share.h"
+
+#include <immintrin.h>
+#include <omp.h>
+#include <string.h>
+
+namespace hg {
+namespace {
+
+// ---------------- portable fallback ----------------
+float f16_to_f32(uint16_t h) {
+  uint32_t sign = (uint32_t)(h & 0x8000u) << 16, e = (h >> 10) & 0x1Fu, m = h & 0x3FFu, bits;
+  if (e == 0x1Fu) {
+    bits = sign | 0x7F800000u | (m << 13);
+  } else if (e) {
+    bits = sign | ((e + 112u) << 23) | (m << 13);
+  } else if (!m) {
+    bits = sign;
+  } else {
+    int sh = 0;
+    while (!(m & 0x400u)) { m <<= 1; ++sh; }
+    bits = sign | ((uint32_t)(113 - sh) << 23) | ((m & 0x3FFu) << 13);
+  }
+  float f;
+  memcpy(&f, &bits, 4);
+  return f;
+}
+
+float bf16_to_f32(uint16_t h) {
+  uint32_t bits = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &bits, 4);
+  return f;
+}
+
+inline float wval(const uint16_t* p, int dtype) { return dtype == 1 ? bf16_to_f32(*p) : f16_to_f32(*p); }
+
+void rows_scalar(const float* x, int B, int K, const uint16_t* W, int dtype, const uint16_t* bias, int r0, int ra,
+                 int rb, float* y, int ldy) {
+  for (int r = ra; r < rb; ++r) {
+    const uint16_t* w = W + (int64_t)r * K;
+    for (int b = 0; b < B; ++b) {
+      float acc = 0.f;
+      for (int k = 0; k < K; ++k) acc += x[(int64_t)b * K + k] * wval(w + k, dtype);
+      if (bias) acc += wval(bias + r, dtype);
+      y[(int64_t)b * ldy + (r - r0)] = acc;
+    }
+  }
+}
+
+// ---------------- AVX-512 ----------------
+template <bool BF>
+__attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) inline __m512 load16(const uint16_t* p) {
+  __m256i v = _mm256_loadu_si256((const __m256i*)p);
+  if (BF) return _mm512_castsi512_ps(_mm512_slli_epi32(_mm512_cvtepu16_epi32(v), 16));
+  return _mm512_cvtph_ps(v);
+}
+
+template <bool BF>
+__attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) inline __m512 load8(const uint16_t* p) {
+  __m256i v = _mm256_maskz_loadu_epi16((__mmask16)0xFF, p);
+  if (BF) return _mm512_castsi512_ps(_mm512_slli_epi32(_mm512_cvtepu16_epi32(v), 16));
+  return _mm512_cvtph_ps(v);
+}
+
+template <bool BF, int B, int R>
+__attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) void block512(const float* x, int K, const uint16_t* W,
+                                                                           const uint16_t* bias, int r0, int r,
+                                                                           float* y, int ldy) {
+  __m512 acc[R][B];
+  for (int i = 0; i < R; ++i)
+    for (int b = 0; b < B; ++b) acc[i][b] = _mm512_setzero_ps();
+  const uint16_t* w[R];
+  for (int i = 0; i < R; ++i) w[i] = W + (int64_t)(r + i) * K;
+  int k = 0;
+  for (; k + 16 <= K; k += 16) {
+    __m512 wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = load16<BF>(w[i] + k);
+    for (int b = 0; b < B; ++b) {
+      __m512 xv = _mm512_loadu_ps(x + (int64_t)b * K + k);
+      for (int i = 0; i < R; ++i) acc[i][b] = _mm512_fmadd_ps(wv[i], xv, acc[i][b]);
+    }
+  }
+  if (k < K) {  // K % 8 == 0: one half vector left
+    __m512 wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = load8<BF>(w[i] + k);
+    for (int b = 0; b < B; ++b) {
+      __m512 xv = _mm512_maskz_loadu_ps((__mmask16)0xFF, x + (int64_t)b * K + k);
+      for (int i = 0; i < R; ++i) acc[i][b] = _mm512_fmadd_ps(wv[i], xv, acc[i][b]);
+    }
+  }
+  for (int i = 0; i < R; ++i) {
+    const float bv = bias ? wval(bias + r + i, BF ? 1 : 0) : 0.f;
+    for (int b = 0; b < B; ++b) y[(int64_t)b * ldy + (r + i - r0)] = _mm512_reduce_add_ps(acc[i][b]) + bv;
+  }
+}
+
+// ---------------- AVX2 + F16C + FMA ----------------
+template <bool BF>
+__attribute__((target("avx2,f16c,fma"))) inline __m256 load8_avx2(const uint16_t* p) {
+  __m128i v = _mm_loadu_si128((const __m128i*)p);
+  if (BF) return _mm256_castsi256_ps(_mm256_slli_epi32(_mm256_cvtepu16_epi32(v), 16));
+  return _mm256_cvtph_ps(v);
+}
+
+__attribute__((target("avx2,f16c,fma"))) inline float hsum256(__m256 v) {
+  __m128 s = _mm_add_ps(_mm256_castps256_ps128(v), _mm256_extractf128_ps(v, 1));
+  s = _mm_add_ps(s, _mm_movehl_ps(s, s));
+  s = _mm_add_ss(s, _mm_shuffle_ps(s, s, 1));
+  return _mm_cvtss_f32(s);
+}
+
+template <bool BF, int B, int R>
+__attribute__((target("avx2,f16c,fma"))) void block256(const float* x, int K, const uint16_t* W, const uint16_t* bias,
+                                                       int r0, int r, float* y, int ldy) {
+  __m256 acc[R][B];
+  for (int i = 0; i < R; ++i)
+    for (int b = 0; b < B; ++b) acc[i][b] = _mm256_setzero_ps();
+  const uint16_t* w[R];
+  for (int i = 0; i < R; ++i) w[i] = W + (int64_t)(r + i) * K;
+  for (int k = 0; k < K; k += 8) {
+    __m256 wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = load8_avx2<BF>(w[i] + k);
+    for (int b = 0; b < B; ++b) {
+      __m256 xv = _mm256_loadu_ps(x + (int64_t)b * K + k);
+      for (int i = 0; i < R; ++i) acc[i][b] = _mm256_fmadd_ps(wv[i], xv, acc[i][b]);
+    }
+  }
+  for (int i = 0; i < R; ++i) {
+    const float bv = bias ? wval(bias + r + i, BF ? 1 : 0) : 0.f;
+    for (int b = 0; b < B; ++b) y[(int64_t)b * ldy + (r + i - r0)] = hsum256(acc[i][b]) + bv;
+  }
+}
+
+enum Isa { ISA_SCALAR = 0, ISA_AVX2 = 1, ISA_AVX512 = 2 };
+
+Isa detect() {
+  __builtin_cpu_init();
+  if (__builtin_cpu_supports("avx512f") && __builtin_cpu_supports("avx512bw") && __builtin_cpu_supports("avx512vl"))
+    return ISA_AVX512;
+  if (__builtin_cpu_supports("avx2") && __builtin_cpu_supports("fma") && __builtin_cpu_supports("f16c"))
+    return ISA_AVX2;
+  return ISA_SCALAR;
+}
+
+const Isa g_isa = detect();
+
+typedef void (*BlockFn)(const float*, int, const uint16_t*, const uint16_t*, int, int, float*, int);
+
+// Rows per block: R x B accumulators stay within the vector register file.
+template <bool BF, int B>
+void run_rows(Isa isa, const float* x, int K, const uint16_t* W, const uint16_t* bias, int r0, int ra, int rb, float* y,
+              int ldy) {
+  constexpr int R = B <= 4 ? 4 : 2;
+  BlockFn blk = isa == ISA_AVX512 ? block512<BF, B, R> : block256<BF, B, R>;
+  BlockFn one = isa == ISA_AVX512 ? block512<BF, B, 1> : block256<BF, B, 1>;
+  int r = ra;
+  for (; r + R <= rb; r += R) blk(x, K, W, bias, r0, r, y, ldy);
+  for (; r < rb; ++r) one(x, K, W, bias, r0, r, y, ldy);
+}
+
+template <bool BF>
+void run_rows_b(Isa isa, const float* x, int B, int K, const uint16_t* W, const uint16_t* bias, int r0, int ra, int rb,
+                float* y, int ldy) {
+  switch (B) {
+    case 1: run_rows<BF, 1>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 2: run_rows<BF, 2>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 3: run_rows<BF, 3>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 4: run_rows<BF, 4>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 5: run_rows<BF, 5>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 6: run_rows<BF, 6>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 7: run_rows<BF, 7>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    default: run_rows<BF, 8>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+  }
+}
+
+}  // namespace
+
+const char* cpu_share_isa() {
+  return g_isa == ISA_AVX512 ? "avx512" : g_isa == ISA_AVX2 ? "avx2" : "scalar";
+}
+
+void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const uint16_t* bias, int r0, int r1,
+               float* y, int ldy, int nthreads) {
+  const int n = r1 - r0;
+  if (n <= 0) return;
+  const int nt_max = nthreads > 0 ? nthreads : omp_get_max_threads();
+  // at least 8 rows per thread so short shares are not spread too thin
+  int nt = (n + 7) / 8;
+  if (nt > nt_max) nt = nt_max;
+  if (nt < 1) nt = 1;
+#pragma omp parallel num_threads(nt)
+  {
+    const int t = omp_get_thread_num(), T = omp_get_num_threads();
+    // contiguous row ranges, aligned to 4 rows so blocks stay whole
+    const int blocks = (n + 3) / 4;
+    const int ba = (int)((int64_t)blocks * t / T), bb = (int)((int64_t)blocks * (t + 1) / T);
+    const int ra = r0 + 4 * ba, rb = r0 + (4 * bb < n ? 4 * bb : n);
+    if (ra < rb) {
+      if (g_isa == ISA_SCALAR)
+        rows_scalar(x, B, K, W, dtype, bias, r0, ra, rb, y, ldy);
+      else if (dtype == 1)
+        run_rows_b<true>(g_isa, x, B, K, W, bias, r0, ra, rb, y, ldy);
+      else
+        run_rows_b<false>(g_isa, x, B, K, W, bias, r0, ra, rb, y, ldy);
+    }
+  }
+}
+
+}  // namespace hg

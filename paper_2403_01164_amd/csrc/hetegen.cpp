@@ -1,0 +1,963 @@
+// Host runtime of the heterogeneous-parallel Linear: context, pinned memory,
+// the chunked host-to-device weight pipeline, the CPU/GPU split of one linear,
+// the distribution-law planner and the decode step over a stack of linears.
+//
+// Dataflow of one linear with n_cpu CPU rows and n_gpu GPU rows (HeteGen Sec. 4.2,
+// Fig. 5a, with the weights pinned once at load time so no per-call pinning):
+//   1. the activation goes to the host: a kernel writes it as binary32 straight into
+//      pinned host memory (no copy-engine queue in the way) and an event marks it;
+//   2. the GPU rows are computed on the caller's stream: resident rows by one GEMV
+//      launch, streamed rows chunk by chunk as the copy stream lands them in a ring
+//      of device staging slots (ring slots are recycled through events);
+//   3. the calling thread waits for the activation and computes the CPU rows on the
+//      host cores while 2 proceeds;
+//   4. a kernel reads the CPU rows from pinned memory, finishes them like the GPU
+//      rows (ReLU / residual / rounding) and writes them into the output.
+// Weights for later chunks are copied as soon as a ring slot is free, across
+// linear and layer boundaries (Sec. 3.1: idle time is hidden by prefetching).
+#include <hip/hip_runtime_api.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <chrono>
+#include <deque>
+#include <string>
+#include <vector>
+
+#include "../../include/hetegen.h"
+#include "cpu_share.h"
+#include "kernels.h"
+
+namespace {
+
+using Clock = std::chrono::steady_clock;
+
+double ms_since(Clock::time_point t0) {
+  return std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
+}
+
+thread_local std::string g_create_error;
+
+constexpr size_t kDefaultChunk = 32ull << 20;
+constexpr int kDefaultRing = 8;
+constexpr int kMaxBatch = 8;
+
+}  // namespace
+
+struct hetegen_ctx {
+  int device = 0;
+  int cpu_threads = 0;
+  size_t chunk_bytes = kDefaultChunk;
+  int ring = kDefaultRing;
+  hipStream_t copy_stream = nullptr;
+  hipStream_t capture_stream = nullptr;
+  std::vector<void*> slot;
+  std::vector<hipEvent_t> ev_ready, ev_free;
+  hipEvent_t ev_x = nullptr, ev_y = nullptr;
+  // pinned hand-off buffers (binary32), grown on demand
+  float* x_host = nullptr;
+  size_t x_host_bytes = 0;
+  float* y_host = nullptr;
+  size_t y_host_bytes = 0;
+  bool y_pending = false;  // ev_y recorded after the last read of y_host
+  // streamed-chunk pipeline
+  struct Chunk {
+    const char* src;
+    size_t bytes;
+  };
+  std::deque<Chunk> planned;  // not yet consumed; the first `copied` have copies enqueued
+  int copied = 0;
+  long long seq_head = 0;  // sequence number of planned.front()
+  // profiling
+  bool profiling = false;
+  struct Timed {
+    hipEvent_t a, b;
+    int kind;  // 0 = copy, 1 = gemv
+    double bytes;
+  };
+  std::vector<Timed> timed;
+  std::vector<hipEvent_t> ev_pool;
+  hetegen_profile prof{};
+  std::string err;
+};
+
+struct hetegen_model {
+  struct Lin {
+    int N = 0, K = 0;
+    const void* W_host = nullptr;
+    const void* bias_host = nullptr;
+    double alpha = 0;
+    int resident = 0;
+    int n_gpu = 0, n_cpu = 0;
+    void* W_dev = nullptr;     // rows [0, n_gpu) when resident
+    void* bias_dev = nullptr;  // all N biases
+  };
+  int L = 0, H = 0, F = 0, dtype = 0, max_batch = 1;
+  std::vector<Lin> lin;
+  void* arena = nullptr;  // device memory for resident weights and biases
+  void* act = nullptr;    // device activations: x, qkv, f, ln
+  void *xbuf = nullptr, *qkv = nullptr, *fbuf = nullptr, *lnbuf = nullptr;
+  void* trace = nullptr;
+  size_t trace_bytes = 0;
+  // graph replay of an all-resident, GPU-only step
+  bool graphable = false;
+  hipGraphExec_t gexec = nullptr;
+  int g_B = 0;
+  const void* g_x = nullptr;
+  void* g_out = nullptr;
+};
+
+namespace {
+
+hetegen_status fail(hetegen_ctx* ctx, hetegen_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (ctx) ctx->err = buf;
+  else g_create_error = buf;
+  return code;
+}
+
+#define HIPCHK(ctx, expr)                                                                           \
+  do {                                                                                              \
+    hipError_t e_ = (expr);                                                                         \
+    if (e_ != hipSuccess)                                                                           \
+      return fail((ctx), HETEGEN_ERR_HIP, "%s failed: %s (%d)", #expr, hipGetErrorString(e_), (int)e_); \
+  } while (0)
+
+#define TRY(expr)                        \
+  do {                                   \
+    hetegen_status s_ = (expr);          \
+    if (s_ != HETEGEN_OK) return s_;     \
+  } while (0)
+
+inline size_t elem_size(int dtype) { return dtype == HETEGEN_F32 ? 4 : 2; }
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int split_cpu_rows(int N, double alpha) {
+  double c = floor(alpha * (double)N + 0.5);
+  if (c < 0) c = 0;
+  if (c > N) c = N;
+  return (int)c;
+}
+
+hetegen_status ensure_host(hetegen_ctx* ctx, float** buf, size_t* have, size_t need) {
+  if (*have >= need) return HETEGEN_OK;
+  if (*buf) {
+    hipError_t e = hipHostFree(*buf);
+    *buf = nullptr;
+    *have = 0;
+    if (e != hipSuccess) return fail(ctx, HETEGEN_ERR_HIP, "hipHostFree: %s", hipGetErrorString(e));
+  }
+  size_t bytes = std::max(need, (size_t)1 << 20);
+  // coherent: written by kernels and read by the host (and the reverse) around events
+  if (hipHostMalloc((void**)buf, bytes, hipHostMallocCoherent) != hipSuccess) {
+    (void)hipGetLastError();
+    *buf = nullptr;
+    return fail(ctx, HETEGEN_ERR_OOM, "pinned hand-off buffer of %zu bytes", bytes);
+  }
+  *have = bytes;
+  return HETEGEN_OK;
+}
+
+hetegen_status check_pinned(hetegen_ctx* ctx, const void* p, size_t bytes) {
+  const char* ends[2] = {(const char*)p, (const char*)p + bytes - 1};
+  for (const char* q : ends) {
+    hipPointerAttribute_t a;
+    hipError_t e = hipPointerGetAttributes(&a, q);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(ctx, HETEGEN_ERR_NOT_PINNED, "host weight %p is not page-locked memory", (const void*)q);
+    }
+    if (a.type != hipMemoryTypeHost)
+      return fail(ctx, HETEGEN_ERR_NOT_PINNED, "weight %p is not pinned host memory (type %d)", (const void*)q,
+                  (int)a.type);
+  }
+  return HETEGEN_OK;
+}
+
+// ---- profiling helpers ----
+hipEvent_t pool_event(hetegen_ctx* ctx) {
+  if (!ctx->ev_pool.empty()) {
+    hipEvent_t e = ctx->ev_pool.back();
+    ctx->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  return e;
+}
+
+hetegen_status flush_profile(hetegen_ctx* ctx) {
+  for (auto& t : ctx->timed) {
+    HIPCHK(ctx, hipEventSynchronize(t.b));
+    float ms = 0;
+    HIPCHK(ctx, hipEventElapsedTime(&ms, t.a, t.b));
+    if (t.kind == 0) {
+      ctx->prof.h2d_ms += ms;
+      ctx->prof.h2d_bytes += t.bytes;
+    } else {
+      ctx->prof.gpu_ms += ms;
+      ctx->prof.gpu_bytes += t.bytes;
+      ctx->prof.gemv_launches++;
+    }
+    ctx->ev_pool.push_back(t.a);
+    ctx->ev_pool.push_back(t.b);
+  }
+  ctx->timed.clear();
+  return HETEGEN_OK;
+}
+
+struct TimedScope {
+  hetegen_ctx* ctx;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  int kind;
+  double bytes;
+  TimedScope(hetegen_ctx* c, hipStream_t st, int k, double by) : ctx(c), s(st), kind(k), bytes(by) {
+    if (ctx->profiling) {
+      a = pool_event(ctx);
+      if (a) (void)hipEventRecord(a, s);
+    }
+  }
+  void end() {
+    if (!a) return;
+    hipEvent_t b = pool_event(ctx);
+    if (!b) return;
+    (void)hipEventRecord(b, s);
+    ctx->timed.push_back({a, b, kind, bytes});
+    a = nullptr;
+  }
+};
+
+// ---- streamed-chunk pipeline ----
+hetegen_status pump(hetegen_ctx* ctx) {
+  while (ctx->copied < (int)ctx->planned.size() && ctx->copied < ctx->ring) {
+    const long long seq = ctx->seq_head + ctx->copied;
+    const int s = (int)(seq % ctx->ring);
+    const auto& c = ctx->planned[ctx->copied];
+    HIPCHK(ctx, hipStreamWaitEvent(ctx->copy_stream, ctx->ev_free[s], 0));
+    TimedScope ts(ctx, ctx->copy_stream, 0, (double)c.bytes);
+    HIPCHK(ctx, hipMemcpyAsync(ctx->slot[s], c.src, c.bytes, hipMemcpyHostToDevice, ctx->copy_stream));
+    ts.end();
+    HIPCHK(ctx, hipEventRecord(ctx->ev_ready[s], ctx->copy_stream));
+    ctx->copied++;
+  }
+  return HETEGEN_OK;
+}
+
+int chunk_rows_for(const hetegen_ctx* ctx, int K, int dtype) {
+  size_t row = (size_t)K * elem_size(dtype);
+  size_t r = ctx->chunk_bytes / row;
+  return r < 1 ? 1 : (int)std::min<size_t>(r, (size_t)1 << 30);
+}
+
+void plan_chunks(hetegen_ctx* ctx, const void* W_host, int n_gpu, int K, int dtype) {
+  const size_t row = (size_t)K * elem_size(dtype);
+  const int cr = chunk_rows_for(ctx, K, dtype);
+  for (int r0 = 0; r0 < n_gpu; r0 += cr) {
+    int nr = std::min(cr, n_gpu - r0);
+    ctx->planned.push_back({(const char*)W_host + (size_t)r0 * row, (size_t)nr * row});
+  }
+}
+
+// ---- one linear ----
+struct Job {
+  const void* x;
+  long long ldx;
+  int B, K, N, dtype;
+  const void* W_host;
+  const void* W_dev;  // rows [0, n_gpu) resident, or nullptr (streamed)
+  const void* bias_host;
+  const void* bias_dev;
+  int n_gpu, n_cpu;
+  void* y;
+  long long ldy;
+  int y_f32;
+  int epi;
+  const void* resid;
+  long long ldr;
+  int ln;
+  void* ln_buf;     // device [B, K] for the normalised input when it must be materialised
+  void* trace_in;   // optional copy of the linear's input [B, K]
+  void* trace_out;  // optional copy of the output [B, N]
+};
+
+hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long ldx, int ln, const void* W, int row0,
+                        int rows, hipStream_t st, void* h_out) {
+  hg::GemvParams p{};
+  const size_t ys = j.y_f32 ? 4 : 2;
+  p.x = x;
+  p.ldx = ldx;
+  p.W = W;
+  p.bias = j.bias_dev ? (const char*)j.bias_dev + (size_t)row0 * 2 : nullptr;
+  p.y = (char*)j.y + (size_t)row0 * ys;
+  p.ldy = j.ldy;
+  p.resid = j.resid ? (const char*)j.resid + (size_t)row0 * 2 : nullptr;
+  p.ldr = j.ldr;
+  p.h_out = h_out;
+  p.ldh = j.K;
+  p.rows = rows;
+  p.K = j.K;
+  p.epi = j.epi;
+  p.y_f32 = j.y_f32;
+  p.ln = ln;
+  TimedScope ts(ctx, st, 1, (double)rows * j.K * 2);
+  HIPCHK(ctx, hg::launch_gemv(p, j.dtype, j.B, st, 0));
+  ts.end();
+  return HETEGEN_OK;
+}
+
+hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
+  const size_t s = 2;
+  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr;
+  const void* xin = j.x;
+  long long ldin = j.ldx;
+  // 1. input: materialise LayerNorm(x) unless it is fused into one resident GEMV,
+  //    and hand the input to the host when there are CPU rows.
+  if (j.ln && !fused_ln) {
+    if (j.n_cpu > 0) TRY(ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, (size_t)j.B * j.K * 4));
+    HIPCHK(ctx, hg::launch_layernorm(j.x, j.ldx, j.B, j.K, j.dtype, j.ln_buf, j.K, j.n_cpu > 0 ? ctx->x_host : nullptr,
+                                     st));
+    xin = j.ln_buf;
+    ldin = j.K;
+  } else if (j.n_cpu > 0) {
+    TRY(ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, (size_t)j.B * j.K * 4));
+    HIPCHK(ctx, hg::launch_export_f32(j.x, j.ldx, j.B, j.K, j.dtype, ctx->x_host, st));
+  }
+  if (j.n_cpu > 0) HIPCHK(ctx, hipEventRecord(ctx->ev_x, st));
+  if (j.trace_in && !fused_ln)
+    HIPCHK(ctx, hipMemcpy2DAsync(j.trace_in, (size_t)j.K * s, xin, (size_t)ldin * s, (size_t)j.K * s, j.B,
+                                 hipMemcpyDeviceToDevice, st));
+  // 2. GPU rows
+  if (j.n_gpu > 0) {
+    if (j.W_dev) {
+      TRY(run_gemv(ctx, j, xin, ldin, fused_ln ? 1 : 0, j.W_dev, 0, j.n_gpu, st, fused_ln ? j.trace_in : nullptr));
+    } else {
+      const int cr = chunk_rows_for(ctx, j.K, j.dtype);
+      for (int r0 = 0; r0 < j.n_gpu; r0 += cr) {
+        const int nr = std::min(cr, j.n_gpu - r0);
+        if (ctx->copied < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk pipeline is empty");
+        const int slot = (int)(ctx->seq_head % ctx->ring);
+        if (ctx->planned.front().bytes != (size_t)nr * j.K * s)
+          return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk plan out of step");
+        HIPCHK(ctx, hipStreamWaitEvent(st, ctx->ev_ready[slot], 0));
+        TRY(run_gemv(ctx, j, xin, ldin, 0, ctx->slot[slot], r0, nr, st, nullptr));
+        HIPCHK(ctx, hipEventRecord(ctx->ev_free[slot], st));
+        ctx->planned.pop_front();
+        ctx->copied--;
+        ctx->seq_head++;
+        TRY(pump(ctx));
+      }
+    }
+  }
+  // 3. CPU rows on the calling thread's OpenMP team
+  if (j.n_cpu > 0) {
+    // the previous import kernel may still read y_host
+    if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
+    ctx->y_pending = false;
+    TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)j.B * j.n_cpu * 4));
+    HIPCHK(ctx, hipEventSynchronize(ctx->ev_x));
+    auto t0 = Clock::now();
+    hg::cpu_share(ctx->x_host, j.B, j.K, (const uint16_t*)j.W_host, j.dtype, (const uint16_t*)j.bias_host, j.n_gpu, j.N,
+                  ctx->y_host, j.n_cpu, ctx->cpu_threads);
+    ctx->prof.cpu_ms += ms_since(t0);
+    ctx->prof.cpu_bytes += (double)j.n_cpu * j.K * s;
+    // 4. finish and place the CPU rows
+    const size_t ys = j.y_f32 ? 4 : 2;
+    HIPCHK(ctx, hg::launch_import_rows(ctx->y_host, j.B, j.n_cpu, j.dtype, j.epi, (char*)j.y + (size_t)j.n_gpu * ys,
+                                       j.ldy, j.y_f32, j.resid ? (const char*)j.resid + (size_t)j.n_gpu * 2 : nullptr,
+                                       j.ldr, st));
+    HIPCHK(ctx, hipEventRecord(ctx->ev_y, st));
+    ctx->y_pending = true;
+  }
+  if (j.trace_out)
+    HIPCHK(ctx, hipMemcpy2DAsync(j.trace_out, (size_t)j.N * s, j.y, (size_t)j.ldy * s, (size_t)j.N * s, j.B,
+                                 hipMemcpyDeviceToDevice, st));
+  return HETEGEN_OK;
+}
+
+hetegen_status finish_call(hetegen_ctx* ctx, Clock::time_point t0) {
+  if (ctx->profiling) TRY(flush_profile(ctx));
+  ctx->prof.wall_ms += ms_since(t0);
+  return HETEGEN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
+  if (!out) return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  hetegen_config c{};
+  if (cfg) c = *cfg;
+  if (c.ring_depth == 0) c.ring_depth = kDefaultRing;
+  if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunk;
+  if (c.ring_depth < 2 || c.ring_depth > 64)
+    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "ring_depth %d outside [2, 64]", c.ring_depth);
+  if (c.chunk_bytes < 4096 || (c.chunk_bytes & 15u))
+    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "chunk_bytes %zu must be >= 4096 and a multiple of 16",
+                c.chunk_bytes);
+  int ndev = 0;
+  hipError_t e = hipGetDeviceCount(&ndev);
+  if (e != hipSuccess || ndev <= 0) {
+    (void)hipGetLastError();
+    return fail(nullptr, HETEGEN_ERR_HIP, "no HIP device (%s)", hipGetErrorString(e));
+  }
+  if (c.device < 0 || c.device >= ndev)
+    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "device %d outside [0, %d)", c.device, ndev);
+  hetegen_ctx* ctx = new hetegen_ctx();
+  ctx->device = c.device;
+  ctx->cpu_threads = c.cpu_threads;
+  ctx->chunk_bytes = c.chunk_bytes;
+  ctx->ring = c.ring_depth;
+  auto bail = [&](hetegen_status st) {
+    g_create_error = ctx->err;
+    hetegen_destroy(ctx);
+    return st;
+  };
+  if (hipSetDevice(c.device) != hipSuccess) return bail(fail(ctx, HETEGEN_ERR_HIP, "hipSetDevice(%d)", c.device));
+  if (hipStreamCreateWithFlags(&ctx->copy_stream, hipStreamNonBlocking) != hipSuccess ||
+      hipStreamCreateWithFlags(&ctx->capture_stream, hipStreamNonBlocking) != hipSuccess)
+    return bail(fail(ctx, HETEGEN_ERR_HIP, "stream creation failed"));
+  if (hipEventCreateWithFlags(&ctx->ev_x, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_y, hipEventDisableTiming) != hipSuccess)
+    return bail(fail(ctx, HETEGEN_ERR_HIP, "event creation failed"));
+  ctx->slot.assign(c.ring_depth, nullptr);
+  ctx->ev_ready.assign(c.ring_depth, nullptr);
+  ctx->ev_free.assign(c.ring_depth, nullptr);
+  for (int i = 0; i < c.ring_depth; ++i) {
+    if (hipMalloc(&ctx->slot[i], c.chunk_bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      ctx->slot[i] = nullptr;
+      return bail(fail(ctx, HETEGEN_ERR_OOM, "staging slot of %zu bytes", c.chunk_bytes));
+    }
+    if (hipEventCreateWithFlags(&ctx->ev_ready[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ctx->ev_free[i], hipEventDisableTiming) != hipSuccess)
+      return bail(fail(ctx, HETEGEN_ERR_HIP, "event creation failed"));
+    // every slot starts free
+    if (hipEventRecord(ctx->ev_free[i], ctx->copy_stream) != hipSuccess)
+      return bail(fail(ctx, HETEGEN_ERR_HIP, "hipEventRecord failed"));
+  }
+  *out = ctx;
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_destroy(hetegen_ctx* ctx) {
+  if (!ctx) return HETEGEN_OK;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  for (auto& t : ctx->timed) {
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
+  for (size_t i = 0; i < ctx->slot.size(); ++i) {
+    if (ctx->slot[i]) (void)hipFree(ctx->slot[i]);
+    if (ctx->ev_ready[i]) (void)hipEventDestroy(ctx->ev_ready[i]);
+    if (ctx->ev_free[i]) (void)hipEventDestroy(ctx->ev_free[i]);
+  }
+  if (ctx->ev_x) (void)hipEventDestroy(ctx->ev_x);
+  if (ctx->ev_y) (void)hipEventDestroy(ctx->ev_y);
+  if (ctx->x_host) (void)hipHostFree(ctx->x_host);
+  if (ctx->y_host) (void)hipHostFree(ctx->y_host);
+  if (ctx->copy_stream) (void)hipStreamDestroy(ctx->copy_stream);
+  if (ctx->capture_stream) (void)hipStreamDestroy(ctx->capture_stream);
+  (void)hipGetLastError();
+  delete ctx;
+  return HETEGEN_OK;
+}
+
+const char* hetegen_last_error(const hetegen_ctx* ctx) { return ctx ? ctx->err.c_str() : g_create_error.c_str(); }
+
+hetegen_status hetegen_host_alloc(hetegen_ctx* ctx, size_t bytes, void** p) {
+  if (!ctx || !p || bytes == 0) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_host_alloc: bad arguments");
+  *p = nullptr;
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  if (hipHostMalloc(p, bytes, hipHostMallocDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(ctx, HETEGEN_ERR_OOM, "hipHostMalloc of %zu bytes failed", bytes);
+  }
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_host_free(hetegen_ctx* ctx, void* p) {
+  if (!ctx) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "ctx is NULL");
+  if (!p) return HETEGEN_OK;
+  HIPCHK(ctx, hipHostFree(p));
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K, const void* W_host,
+                              const void* W_dev_resident, int N, hetegen_dtype w_dtype, const void* bias_host,
+                              const void* bias_dev, double alpha, void* y_dev, hetegen_dtype y_dtype, void* stream) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  auto t0 = Clock::now();
+  ctx->err.clear();
+  if (!x_dev || !W_host || !y_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "x_dev, W_host and y_dev are required");
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "alpha %g outside [0, 1]", alpha);
+  if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
+  if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
+  if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+  if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
+    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
+  if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)
+    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "y dtype must be the weight dtype or fp32");
+  if (!aligned16(x_dev) || !aligned16(W_host) || (W_dev_resident && !aligned16(W_dev_resident)))
+    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x, W and the resident copy must be 16-byte aligned");
+  const int n_cpu = split_cpu_rows(N, alpha), n_gpu = N - n_cpu;
+  if ((n_cpu > 0 && !bias_host && bias_dev) || (n_gpu > 0 && !bias_dev && bias_host))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bias: pass bias_host and bias_dev, or neither");
+  TRY(check_pinned(ctx, W_host, (size_t)N * K * 2));
+  const size_t row = (size_t)K * 2;
+  if (!W_dev_resident && n_gpu > 0 && row > ctx->chunk_bytes)
+    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "a weight row (%zu bytes) exceeds chunk_bytes", row);
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  hipStream_t st = (hipStream_t)stream;
+  Job j{};
+  j.x = x_dev;
+  j.ldx = K;
+  j.B = B;
+  j.K = K;
+  j.N = N;
+  j.dtype = w_dtype;
+  j.W_host = W_host;
+  j.W_dev = W_dev_resident;
+  j.bias_host = bias_host;
+  j.bias_dev = bias_dev;
+  j.n_gpu = n_gpu;
+  j.n_cpu = n_cpu;
+  j.y = y_dev;
+  j.ldy = N;
+  j.y_f32 = y_dtype == HETEGEN_F32;
+  j.epi = hg::EPI_NONE;
+  if (!W_dev_resident && n_gpu > 0) {
+    if (!ctx->planned.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+    plan_chunks(ctx, W_host, n_gpu, K, w_dtype);
+    TRY(pump(ctx));
+  }
+  hetegen_status stt = run_linear(ctx, j, st);
+  if (stt != HETEGEN_OK) {
+    ctx->planned.clear();
+    ctx->copied = 0;
+    return stt;
+  }
+  return finish_call(ctx, t0);
+}
+
+// ---- planner (pure host arithmetic) ----
+hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n, const hetegen_bw* bw, int n_bw, int flags,
+                                  double* alpha_out) {
+  if (!shapes || !bw || !alpha_out || n < 0 || !(n_bw == 1 || n_bw == n)) return HETEGEN_ERR_INVALID_ARG;
+  for (int i = 0; i < n; ++i) {
+    const hetegen_bw& b = bw[n_bw == 1 ? 0 : i];
+    if (shapes[i].N < 1 || shapes[i].K < 1) return HETEGEN_ERR_INVALID_ARG;
+    if (shapes[i].resident) {
+      alpha_out[i] = 0.0;
+      continue;
+    }
+    const double vc = b.cpu_Bps, vg = b.hbm_gemv_Bps;
+    double vm = b.h2d_Bps;
+    if (!(vc > 0 && std::isfinite(vc) && vg > 0 && std::isfinite(vg) && vm > 0 && std::isfinite(vm)))
+      return HETEGEN_ERR_INVALID_ARG;
+    if (b.pin_Bps > 0) {
+      if (!std::isfinite(b.pin_Bps)) return HETEGEN_ERR_INVALID_ARG;
+      vm = std::min(vm, b.pin_Bps);  // T_COM = max(T_PIN, T_TRANS)
+    }
+    // CPU fraction = 1 - alpha_gpu; written as the balance of per-byte times so that
+    // large speed ratios do not overflow: (1/Vcom + 1/Vgpu) / (1/Vcpu + 1/Vcom + 1/Vgpu).
+    double c;
+    if (flags & HETEGEN_PLAN_APPROX) c = (1.0 / vm) / (1.0 / vc + 1.0 / vm);
+    else c = (1.0 / vm + 1.0 / vg) / (1.0 / vc + 1.0 / vm + 1.0 / vg);
+    alpha_out[i] = std::min(1.0, std::max(0.0, c));
+  }
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_set_profiling(hetegen_ctx* ctx, int on) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->profiling = on != 0;
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_get_profile(hetegen_ctx* ctx, hetegen_profile* out, int reset) {
+  if (!ctx || !out) return HETEGEN_ERR_INVALID_ARG;
+  TRY(flush_profile(ctx));
+  *out = ctx->prof;
+  if (reset) ctx->prof = hetegen_profile{};
+  return HETEGEN_OK;
+}
+
+}  // extern "C"
+
+// ---- bandwidth probe ----
+extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype, int B,
+                                        int reps, hetegen_bw* out) {
+  if (!ctx || !W_host || !out || N < 1 || K < 8 || K % 8 || B < 1 || B > kMaxBatch || reps < 1 ||
+      (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe: bad arguments");
+  TRY(check_pinned(ctx, W_host, (size_t)N * K * 2));
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  const size_t wbytes = (size_t)N * K * 2;
+  auto median = [](std::vector<double> v) {
+    std::sort(v.begin(), v.end());
+    return v[v.size() / 2];
+  };
+  // V_CPU: the CPU share over all rows
+  if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
+  ctx->y_pending = false;
+  TRY(ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, (size_t)B * K * 4));
+  TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)B * N * 4));
+  memset(ctx->x_host, 0, (size_t)B * K * 4);
+  std::vector<double> tc;
+  for (int r = 0; r < reps; ++r) {
+    auto t0 = Clock::now();
+    hg::cpu_share(ctx->x_host, B, K, (const uint16_t*)W_host, dtype, nullptr, 0, N, ctx->y_host, N, ctx->cpu_threads);
+    tc.push_back(ms_since(t0) * 1e-3);
+  }
+  // V_COM: chunked pinned copies through the ring on the copy stream
+  hipEvent_t a, b;
+  HIPCHK(ctx, hipEventCreate(&a));
+  HIPCHK(ctx, hipEventCreate(&b));
+  const size_t row = (size_t)K * 2;
+  const size_t cbytes = (size_t)chunk_rows_for(ctx, K, dtype) * row;
+  std::vector<double> tm;
+  for (int r = 0; r < reps; ++r) {
+    HIPCHK(ctx, hipEventRecord(a, ctx->copy_stream));
+    int i = 0;
+    for (size_t off = 0; off < wbytes; off += cbytes, ++i) {
+      const size_t nb = std::min(cbytes, wbytes - off);
+      HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], (const char*)W_host + off, nb, hipMemcpyHostToDevice,
+                                 ctx->copy_stream));
+    }
+    HIPCHK(ctx, hipEventRecord(b, ctx->copy_stream));
+    HIPCHK(ctx, hipEventSynchronize(b));
+    float ms = 0;
+    HIPCHK(ctx, hipEventElapsedTime(&ms, a, b));
+    tm.push_back(ms * 1e-3);
+  }
+  // V_GPU: the GEMV over a device copy of W
+  void *Wd = nullptr, *xd = nullptr, *yd = nullptr;
+  hetegen_status st = HETEGEN_OK;
+  std::vector<double> tg;
+  if (hipMalloc(&Wd, wbytes) != hipSuccess || hipMalloc(&xd, (size_t)B * K * 2) != hipSuccess ||
+      hipMalloc(&yd, (size_t)B * N * 4) != hipSuccess) {
+    (void)hipGetLastError();
+    st = fail(ctx, HETEGEN_ERR_OOM, "probe buffers");
+  }
+  if (st == HETEGEN_OK && (hipMemcpy(Wd, W_host, wbytes, hipMemcpyHostToDevice) != hipSuccess ||
+                           hipMemset(xd, 0, (size_t)B * K * 2) != hipSuccess))
+    st = fail(ctx, HETEGEN_ERR_HIP, "probe upload failed");
+  for (int r = 0; st == HETEGEN_OK && r < reps + 1; ++r) {
+    hg::GemvParams p{};
+    p.x = xd;
+    p.ldx = K;
+    p.W = Wd;
+    p.y = yd;
+    p.ldy = N;
+    p.rows = N;
+    p.K = K;
+    p.y_f32 = 1;
+    if (hipEventRecord(a, ctx->capture_stream) != hipSuccess ||
+        hg::launch_gemv(p, dtype, B, ctx->capture_stream, 0) != hipSuccess ||
+        hipEventRecord(b, ctx->capture_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess) {
+      st = fail(ctx, HETEGEN_ERR_HIP, "probe GEMV failed");
+      break;
+    }
+    float ms = 0;
+    (void)hipEventElapsedTime(&ms, a, b);
+    if (r > 0) tg.push_back(ms * 1e-3);
+  }
+  if (Wd) (void)hipFree(Wd);
+  if (xd) (void)hipFree(xd);
+  if (yd) (void)hipFree(yd);
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  (void)hipGetLastError();
+  if (st != HETEGEN_OK) return st;
+  out->cpu_Bps = wbytes / median(tc);
+  out->h2d_Bps = wbytes / median(tm);
+  out->hbm_gemv_Bps = wbytes / median(tg);
+  out->pin_Bps = 0;
+  return HETEGEN_OK;
+}
+
+// ---- decode step over decoder-layer linears ----
+namespace {
+
+void model_free(hetegen_model* m) {
+  if (!m) return;
+  if (m->gexec) (void)hipGraphExecDestroy(m->gexec);
+  if (m->arena) (void)hipFree(m->arena);
+  if (m->act) (void)hipFree(m->act);
+  (void)hipGetLastError();
+  delete m;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
+                            hipStream_t st) {
+  const int H = m->H, F = m->F;
+  // plan every streamed chunk of the step up front so the copy stream can run
+  // ahead across linears and layers, bounded by the ring
+  if (!ctx->planned.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+  for (const auto& l : m->lin)
+    if (!l.W_dev && l.n_gpu > 0) plan_chunks(ctx, l.W_host, l.n_gpu, l.K, m->dtype);
+  TRY(pump(ctx));
+  char* tr = (char*)m->trace;
+  auto take = [&](size_t elems) -> void* {
+    if (!tr) return nullptr;
+    void* p = tr;
+    tr += elems * 2;
+    return p;
+  };
+  for (int l = 0; l < m->L; ++l) {
+    const void* xl = l == 0 ? x_dev : m->xbuf;
+    for (int which = 0; which < 4; ++which) {
+      const auto& lin = m->lin[4 * l + which];
+      Job j{};
+      j.B = B;
+      j.K = lin.K;
+      j.N = lin.N;
+      j.dtype = m->dtype;
+      j.W_host = lin.W_host;
+      j.W_dev = lin.W_dev;
+      j.bias_host = lin.bias_host;
+      j.bias_dev = lin.bias_dev;
+      j.n_gpu = lin.n_gpu;
+      j.n_cpu = lin.n_cpu;
+      j.ln_buf = m->lnbuf;
+      j.y_f32 = 0;
+      switch (which) {
+        case 0:  // qkv = LN(x) Wqkv^T + b
+          j.x = xl; j.ldx = H; j.ln = 1;
+          j.y = m->qkv; j.ldy = 3 * H; j.epi = hg::EPI_NONE;
+          break;
+        case 1:  // x = x + (V Wout^T + b), V = qkv[:, 2H:3H]
+          j.x = (const char*)m->qkv + (size_t)2 * H * 2; j.ldx = 3 * H; j.ln = 0;
+          j.y = m->xbuf; j.ldy = H; j.epi = hg::EPI_RESID; j.resid = xl; j.ldr = H;
+          break;
+        case 2:  // f = ReLU(LN(x) Wfc1^T + b)
+          j.x = m->xbuf; j.ldx = H; j.ln = 1;
+          j.y = m->fbuf; j.ldy = F; j.epi = hg::EPI_RELU;
+          break;
+        default:  // x = x + (f Wfc2^T + b)
+          j.x = m->fbuf; j.ldx = F; j.ln = 0;
+          j.y = l == m->L - 1 ? out_dev : m->xbuf; j.ldy = H; j.epi = hg::EPI_RESID; j.resid = m->xbuf; j.ldr = H;
+          break;
+      }
+      j.trace_in = take((size_t)B * j.K);
+      j.trace_out = take((size_t)B * j.N);
+      TRY(run_linear(ctx, j, st));
+    }
+  }
+  return HETEGEN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype, void* const* W_host,
+                                    void* const* bias_host, const double* alpha, const int* resident, int max_batch,
+                                    hetegen_model** out) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->err.clear();
+  if (!out || !W_host || !alpha || L < 1 || H < 8 || F < 8 || H % 8 || F % 8 || max_batch < 1 ||
+      max_batch > kMaxBatch)
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_create: bad arguments");
+  if (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16)
+    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "model dtype: fp16 or bf16");
+  *out = nullptr;
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  hetegen_model* m = new hetegen_model();
+  m->L = L;
+  m->H = H;
+  m->F = F;
+  m->dtype = dtype;
+  m->max_batch = max_batch;
+  m->lin.resize((size_t)4 * L);
+  size_t dev_bytes = 0;
+  for (int i = 0; i < 4 * L; ++i) {
+    auto& l = m->lin[i];
+    const int which = i % 4;
+    l.N = which == 0 ? 3 * H : which == 2 ? F : H;
+    l.K = which == 3 ? F : H;
+    l.W_host = W_host[i];
+    l.bias_host = bias_host ? bias_host[i] : nullptr;
+    l.alpha = alpha[i];
+    l.resident = resident ? resident[i] != 0 : 0;
+    if (!l.W_host || !(l.alpha >= 0 && l.alpha <= 1) || !aligned16(l.W_host)) {
+      model_free(m);
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "linear %d: weight pointer or alpha invalid", i);
+    }
+    hetegen_status st = check_pinned(ctx, l.W_host, (size_t)l.N * l.K * 2);
+    if (st != HETEGEN_OK) {
+      model_free(m);
+      return st;
+    }
+    if ((size_t)l.K * 2 > ctx->chunk_bytes && !l.resident) {
+      model_free(m);
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "linear %d: a row exceeds chunk_bytes", i);
+    }
+    l.n_cpu = split_cpu_rows(l.N, l.alpha);
+    l.n_gpu = l.N - l.n_cpu;
+    if (l.resident) dev_bytes += align256((size_t)l.n_gpu * l.K * 2);
+    if (l.bias_host) dev_bytes += align256((size_t)l.N * 2);
+  }
+  if (dev_bytes && hipMalloc(&m->arena, dev_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    model_free(m);
+    return fail(ctx, HETEGEN_ERR_OOM, "%zu bytes of HBM for resident weights", dev_bytes);
+  }
+  char* p = (char*)m->arena;
+  for (auto& l : m->lin) {
+    if (l.resident) {
+      l.W_dev = p;
+      if (l.n_gpu > 0 && hipMemcpy(p, l.W_host, (size_t)l.n_gpu * l.K * 2, hipMemcpyHostToDevice) != hipSuccess) {
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_HIP, "resident upload failed");
+      }
+      p += align256((size_t)l.n_gpu * l.K * 2);
+    }
+    if (l.bias_host) {
+      l.bias_dev = p;
+      if (hipMemcpy(p, l.bias_host, (size_t)l.N * 2, hipMemcpyHostToDevice) != hipSuccess) {
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_HIP, "bias upload failed");
+      }
+      p += align256((size_t)l.N * 2);
+    }
+  }
+  const size_t B = max_batch;
+  const size_t xb = align256(B * H * 2), qb = align256(B * 3 * H * 2), fb = align256(B * F * 2),
+               lb = align256(B * std::max(H, F) * 2);
+  if (hipMalloc(&m->act, xb + qb + fb + lb) != hipSuccess) {
+    (void)hipGetLastError();
+    model_free(m);
+    return fail(ctx, HETEGEN_ERR_OOM, "activation buffers");
+  }
+  m->xbuf = m->act;
+  m->qkv = (char*)m->act + xb;
+  m->fbuf = (char*)m->act + xb + qb;
+  m->lnbuf = (char*)m->act + xb + qb + fb;
+  // size the pinned hand-off buffers once, so no step reallocates them
+  if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
+  ctx->y_pending = false;
+  {
+    hetegen_status hs = ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, B * std::max(H, F) * 4);
+    if (hs == HETEGEN_OK) hs = ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, B * std::max(3 * H, F) * 4);
+    if (hs != HETEGEN_OK) {
+      model_free(m);
+      return hs;
+    }
+  }
+  m->graphable = true;
+  for (const auto& l : m->lin)
+    if (l.n_cpu > 0 || !l.W_dev) m->graphable = false;
+  *out = m;
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {
+  if (!m || !alpha) return HETEGEN_ERR_INVALID_ARG;
+  for (size_t i = 0; i < m->lin.size(); ++i)
+    if (!m->lin[i].resident && !(alpha[i] >= 0 && alpha[i] <= 1)) return HETEGEN_ERR_INVALID_ARG;
+  for (size_t i = 0; i < m->lin.size(); ++i) {
+    auto& l = m->lin[i];
+    if (l.resident) continue;
+    l.alpha = alpha[i];
+    l.n_cpu = split_cpu_rows(l.N, l.alpha);
+    l.n_gpu = l.N - l.n_cpu;
+  }
+  return HETEGEN_OK;
+}
+
+size_t hetegen_model_trace_bytes(const hetegen_model* m, int B) {
+  if (!m || B < 1) return 0;
+  size_t e = 0;
+  for (const auto& l : m->lin) e += (size_t)B * (l.K + l.N);
+  return e * 2;
+}
+
+hetegen_status hetegen_model_set_trace(hetegen_model* m, void* trace_dev, size_t bytes) {
+  if (!m) return HETEGEN_ERR_INVALID_ARG;
+  if (trace_dev && !aligned16(trace_dev)) return HETEGEN_ERR_INVALID_ARG;
+  m->trace = trace_dev;
+  m->trace_bytes = trace_dev ? bytes : 0;
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_model_destroy(hetegen_ctx* ctx, hetegen_model* m) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  if (!m) return HETEGEN_OK;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  model_free(m);
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
+                                   void* stream) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  auto t0 = Clock::now();
+  ctx->err.clear();
+  if (!m || !x_dev || !out_dev || x_dev == out_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "decode_step: bad pointers");
+  if (B < 1 || B > m->max_batch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, m->max_batch);
+  if (!aligned16(x_dev) || !aligned16(out_dev)) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
+  if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  hipStream_t st = (hipStream_t)stream;
+  const bool use_graph = m->graphable && !m->trace && !ctx->profiling;
+  if (use_graph) {
+    if (!m->gexec || m->g_B != B || m->g_x != x_dev || m->g_out != out_dev) {
+      if (m->gexec) {
+        HIPCHK(ctx, hipGraphExecDestroy(m->gexec));
+        m->gexec = nullptr;
+      }
+      hipGraph_t g = nullptr;
+      HIPCHK(ctx, hipStreamBeginCapture(ctx->capture_stream, hipStreamCaptureModeThreadLocal));
+      hetegen_status cs = enqueue_step(ctx, m, x_dev, out_dev, B, ctx->capture_stream);
+      hipError_t ce = hipStreamEndCapture(ctx->capture_stream, &g);
+      if (cs != HETEGEN_OK) {
+        if (g) (void)hipGraphDestroy(g);
+        return cs;
+      }
+      if (ce != hipSuccess) return fail(ctx, HETEGEN_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ce));
+      hipError_t ie = hipGraphInstantiate(&m->gexec, g, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(g);
+      if (ie != hipSuccess) {
+        m->gexec = nullptr;
+        return fail(ctx, HETEGEN_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
+      }
+      m->g_B = B;
+      m->g_x = x_dev;
+      m->g_out = out_dev;
+    }
+    HIPCHK(ctx, hipGraphLaunch(m->gexec, st));
+    return finish_call(ctx, t0);
+  }
+  hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, st);
+  if (s != HETEGEN_OK) {
+    ctx->planned.clear();
+    ctx->copied = 0;
+    return s;
+  }
+  return finish_call(ctx, t0);
+}
+
+}  // extern "C"

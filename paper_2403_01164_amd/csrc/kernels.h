@@ -1,0 +1,49 @@
+// Internal launch interface of the gfx950 kernels (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace hg {
+
+enum Epi : int { EPI_NONE = 0, EPI_RELU = 1, EPI_RESID = 2 };
+
+// y[b, r] = epi(sum_k xn[b, k] * W[r, k] + bias[r]) for b < B, r < rows, where xn is
+// x, or LayerNorm(x) rounded to the activation type when ln != 0.
+struct GemvParams {
+  const void* x;       // [B, K] activation type, row stride ldx elements, 16-byte aligned
+  long long ldx;
+  const void* W;       // [rows, K] row-major, 16-byte aligned
+  const void* bias;    // [rows] activation type, or nullptr
+  void* y;             // element (b, r) at y[b * ldy + r]
+  long long ldy;
+  const void* resid;   // EPI_RESID: element (b, r) at resid[b * ldr + r]
+  long long ldr;
+  void* h_out;         // ln != 0 and non-null: block 0 also writes LayerNorm(x) here
+  long long ldh;
+  int rows;
+  int K;
+  int epi;
+  int y_f32;           // 1: y is float32, 0: y is the activation type
+  int ln;
+  int ktile;           // K elements staged in LDS per pass (set by the launcher)
+};
+
+// dtype: 0 = fp16, 1 = bf16.  grid_cap bounds the number of workgroups
+// (0 = default).  Returns the launch status.
+hipError_t launch_gemv(GemvParams p, int dtype, int B, hipStream_t stream, int grid_cap);
+
+// h[b, :] = act(LayerNorm(x[b, :])) for b < B (device), and optionally
+// h_host_f32[b * K + k] = float(h[b, k]) (pinned host memory).
+hipError_t launch_layernorm(const void* x, long long ldx, int B, int K, int dtype, void* h, long long ldh,
+                            float* h_host_f32, hipStream_t stream);
+
+// dst_host_f32[b * K + k] = float(x[b * ldx + k])  (device -> pinned host, in a kernel).
+hipError_t launch_export_f32(const void* x, long long ldx, int B, int K, int dtype, float* dst_host_f32,
+                             hipStream_t stream);
+
+// y[b * ldy + c] = epi(src_host_f32[b * n + c]) for c < n, b < B: the CPU rows' sums
+// (bias included) read from pinned host memory, finished like the GPU rows.
+hipError_t launch_import_rows(const float* src_host_f32, int B, int n, int dtype, int epi, void* y,
+                              long long ldy, int y_f32, const void* resid, long long ldr, hipStream_t stream);
+
+}  // namespace hg
