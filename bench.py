@@ -1,21 +1,30 @@
 """Benchmark: one decode step over OPT-shaped decoder-layer linears on one MI355X.
 
-Default workload: OPT-6.7B shapes, 32 layers x {QKV [12288,4096], out [4096,4096],
-fc1 [16384,4096], fc2 [4096,16384]}, fp16 weights ~N(0, 0.02) generated from a
-seeded counter-based generator into pinned host memory, every linear resident in
-HBM (CPU fraction 0 from the planner), batch 1, fresh x ~N(0, 1) per step, already
-in HBM before the timed region.  A step is hetegen_decode_step: the four GEMVs of
-every layer with LayerNorm, value slice, ReLU and residual fused into them.
+Default workload (the bench line): OPT-6.7B shapes, 32 layers x {QKV [12288,4096],
+out [4096,4096], fc1 [16384,4096], fc2 [4096,16384]}, fp16 weights ~N(0, 0.02)
+generated from a seeded counter-based generator into pinned host memory, every
+linear resident in HBM (CPU fraction 0 from the planner), batch 1, a fresh
+x ~N(0, 1) per step already in HBM before the timed region.  A step is
+hetegen_decode_step: the four GEMVs of every layer with LayerNorm, value slice,
+ReLU and residual fused into them.
+
+Other workloads (--model): opt-13b (layers 0-19 resident, 20-39 streamed from
+pinned host with the planner's CPU fraction), opt-30b (all linears in pinned host
+memory, planner alpha), opt-66b (bf16, all host, --alpha sweep).  For those the
+planner's speeds come from hetegen_probe on the box, and the JSON line adds the
+heterogeneous figures (link and CPU rates, Table-2-style busy fractions).
 
 Prints ONE JSON line.  `value` is the effective weight bandwidth of the whole step
 (weight bytes per step / time per step); `ms_per_step` is the decode latency per
-token.  `roofline` is the GEMV kernel's algorithmic bytes per launch (weights, x, bias,
-y) over its average launch time; every dispatch in the event-timed region (on the
-stream the step runs on) is that kernel, so the average is the region's time over
-its launches.  Peak: 8 TB/s HBM.  `cpu_baseline` times the
-oracle (plain C, sequential fp32) on a bounded sample of the same linears.
+token.  `roofline` (all-resident workloads) is the GEMV kernel's algorithmic bytes
+per launch (weights, x, bias, y) over its average launch time; every dispatch in
+the event-timed region (on the stream the step runs on) is that kernel, so the
+average is the region's time over its launches.  Peak: 8 TB/s HBM.
+`cpu_baseline` times the oracle (plain C, sequential fp32) on a bounded sample of
+the same linears.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -27,11 +36,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-OPT = {  # name: (layers, hidden, ffn, dtype)
-    "opt-6.7b": (32, 4096, 16384, 0),
-    "opt-13b": (40, 5120, 20480, 0),
-    "opt-30b": (48, 7168, 28672, 0),
-    "opt-66b": (64, 9216, 36864, 1),
+OPT = {  # name: (layers, hidden, ffn, dtype, default placement)
+    "opt-6.7b": (32, 4096, 16384, 0, "all"),
+    "opt-13b": (40, 5120, 20480, 0, "half"),
+    "opt-30b": (48, 7168, 28672, 0, "none"),
+    "opt-66b": (64, 9216, 36864, 1, "none"),
 }
 NAMES = ("qkv", "out", "fc1", "fc2")
 
@@ -40,10 +49,13 @@ def shapes(H, F):
     return [(3 * H, H), (H, H), (F, H), (H, F)]
 
 
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
 def counter_traffic(model, dt, B):
     """HBM bytes per GEMV launch from the committed counter summary, if it was taken
     on this workload with the current kernel source; else None."""
-    import hashlib
     name = "gemv_%s_b%d_%s_decode_hbm_counters.md" % ("bf16" if dt == 1 else "f16", B, model.replace("-", ""))
     path = os.path.join(ROOT, "profiles", name)
     src = os.path.join(ROOT, "paper_2403_01164_amd", "csrc", "kernels.hip")
@@ -56,10 +68,6 @@ def counter_traffic(model, dt, B):
     return float(fields["traffic_bytes_per_launch"])
 
 
-def log(msg):
-    print("[bench] " + msg, file=sys.stderr, flush=True)
-
-
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -67,6 +75,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--model", default="opt-6.7b", choices=sorted(OPT))
     ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--placement", choices=("all", "half", "none"), default=None,
+                    help="HBM-resident layers: all, the first half, or none (default per model)")
+    ap.add_argument("--alpha", type=float, default=None,
+                    help="fixed CPU fraction for every streamed linear (default: the planner's)")
+    ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: OpenMP default)")
+    ap.add_argument("--chunk-mb", type=int, default=32)
+    ap.add_argument("--ring", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with one plain 256 MiB device-to-device copy, the reference dispatch for "
@@ -74,7 +89,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the heterogeneous "
-              "linear shards by output rows across GPUs, see the design notes); run with --gpus 1",
+              "linear would shard by output rows across GPUs, see the design notes); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
@@ -84,9 +99,10 @@ def main():
     import paper_2403_01164_amd as hg
 
     torch.cuda.set_device(0)
-    L, H, F, dt = OPT[args.model]
+    L, H, F, dt, placement = OPT[args.model]
+    placement = args.placement or placement
     B = args.batch
-    ctx = hg.hetegen_create(0)
+    ctx = hg.hetegen_create(0, cpu_threads=args.threads, chunk_bytes=args.chunk_mb << 20, ring_depth=args.ring)
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
 
@@ -105,12 +121,30 @@ def main():
     wbytes = sum(n * k * 2 for n, k in shp)
     log("generated %.3f GB of weights in %.1f s" % (wbytes / 1e9, time.time() - t0))
 
-    # ---- planner: every linear resident -> CPU fraction 0 ----
-    alpha = hg.hetegen_layer_plan([(n, k, dt, 1) for n, k in shp], [(1.0, 1.0, 1.0, 0.0)])
-    assert all(a == 0.0 for a in alpha)
+    res_layers = L if placement == "all" else L // 2 if placement == "half" else 0
+    resident = [1 if (i // 4) < res_layers else 0 for i in range(4 * L)]
+    streamed = [i for i in range(4 * L) if not resident[i]]
+
+    # ---- planner: speeds per shape from the probe (streamed linears only) ----
+    bws = [(1.0, 1.0, 1.0, 0.0)] * (4 * L)
+    probe = {}
+    if streamed:
+        last = 4 * (L - 1)
+        for m in range(4):
+            n, k = shp[last + m]
+            t0 = time.time()
+            probe[NAMES[m]] = hg.hetegen_probe(ctx, W[last + m], n, k, dt, B, 3)
+            p = probe[NAMES[m]]
+            log("probe %s [%d,%d]: V_CPU %.1f GB/s, V_COM %.1f GB/s, V_GPU %.0f GB/s (%.1f s)" %
+                (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9, time.time() - t0))
+        bws = [tuple(probe[NAMES[i % 4]][f] for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps", "pin_Bps"))
+               for i in range(4 * L)]
+    alpha = hg.hetegen_layer_plan([(n, k, dt, resident[i]) for i, (n, k) in enumerate(shp)], bws)
+    if args.alpha is not None:
+        alpha = [0.0 if resident[i] else args.alpha for i in range(4 * L)]
     t0 = time.time()
-    model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, [1] * len(shp), max(B, 1))
-    log("uploaded resident weights in %.1f s" % (time.time() - t0))
+    model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, resident, max(B, 1))
+    log("model ready in %.1f s (resident layers %d of %d)" % (time.time() - t0, res_layers, L))
 
     # fresh input per step, resident in HBM before timing
     nstep = args.warmup + args.steps
@@ -138,15 +172,14 @@ def main():
     log("decode step %.4f ms/token, %.1f GB/s effective (wall %.4f ms/step)" %
         (ms_step, gbps, wall * 1e3 / args.steps))
 
-    # ---- dominant kernel: every dispatch of the replayed step is the GEMV kernel
-    # (LayerNorm, value slice, ReLU and residual are fused into it), so its average
-    # launch time is the event-timed region divided by the launches in it.
-    launches_per_step = 4 * L
-    avg_us = ms_step * 1e3 / launches_per_step
-    bytes_per_launch = (wbytes + sum(B * (n + k) * 2 + n * 2 for n, k in shp)) / launches_per_step
-    achieved = bytes_per_launch / (avg_us * 1e-6) / 1e9
-    log("GEMV: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" % (avg_us, bytes_per_launch / 1e6, achieved))
-
+    if placement == "all":
+        desc = "all linears HBM-resident (alpha=0), GEMV-only"
+    elif placement == "half":
+        desc = "layers 0-%d HBM-resident, %d-%d streamed from pinned host" % (res_layers - 1, res_layers, L - 1)
+    else:
+        desc = "all linears in pinned host memory, streamed + CPU share"
+    if placement != "all":
+        desc += ", %s" % ("planner alpha" if args.alpha is None else "alpha=%g" % args.alpha)
     result = {
         "metric": "decode latency ms/token + effective weight GB/s (frac of HBM/PCIe roofline)",
         "value": round(gbps, 2),
@@ -161,17 +194,64 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if dt == 1 else "f16",
         "data": "synthetic: seeded N(0,0.02) weights, N(0,1) activations (no checkpoints)",
-        "config": {"workload": "%s-shaped decode step, %d layers x {qkv,out,fc1,fc2}, all linears HBM-resident "
-                               "(alpha=0), batch %d, GEMV-only" % (args.model.upper(), L, B),
+        "config": {"workload": "%s-shaped decode step, %d layers x {qkv,out,fc1,fc2}, %s, batch %d" %
+                               (args.model.upper(), L, desc, B),
                    "layers": L, "hidden": H, "ffn": F, "batch": B, "weight_bytes_per_step": wbytes,
-                   "alpha": 0.0, "parallelism": "single GPU"},
-        "frac_of_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": counter_traffic(args.model, dt, B),
-                     "kernel": "gemv_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B),
-                     "avg_launch_us": round(avg_us, 3), "bytes_per_launch": round(bytes_per_launch),
-                     "launches_per_step": launches_per_step},
+                   "resident_layers": res_layers, "parallelism": "single GPU"},
     }
+
+    if not streamed:
+        # dominant kernel: every dispatch of the replayed step is the GEMV kernel (LayerNorm,
+        # value slice, ReLU and residual are fused into it), so its average launch time is the
+        # event-timed region divided by the launches in it.
+        launches = 4 * L
+        avg_us = ms_step * 1e3 / launches
+        bytes_per_launch = (wbytes + sum(B * (n + k) * 2 + n * 2 for n, k in shp)) / launches
+        achieved = bytes_per_launch / (avg_us * 1e-6) / 1e9
+        log("GEMV: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" % (avg_us, bytes_per_launch / 1e6, achieved))
+        result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
+        result["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                              "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                              "traffic": counter_traffic(args.model, dt, B),
+                              "kernel": "gemv_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B),
+                              "avg_launch_us": round(avg_us, 3), "bytes_per_launch": round(bytes_per_launch),
+                              "launches_per_step": launches}
+    else:
+        # heterogeneous figures: link and CPU rates, the ideal rate of Eq. 4, busy fractions
+        sb = sum(shp[i][0] * shp[i][1] * 2 for i in streamed)
+        n_cpu = [min(shp[i][0], int(np.floor(alpha[i] * shp[i][0] + 0.5))) for i in range(4 * L)]
+        cpu_b = sum(n_cpu[i] * shp[i][1] * 2 for i in streamed)
+        h2d_b = sb - cpu_b
+        v_cpu = float(np.mean([p["cpu_Bps"] for p in probe.values()]))
+        v_com = float(np.mean([p["h2d_Bps"] for p in probe.values()]))
+        v_gpu = float(np.mean([p["hbm_gemv_Bps"] for p in probe.values()]))
+        v_g = 1.0 / (1.0 / v_com + 1.0 / v_gpu)
+        hbm_b = wbytes - sb
+        ideal_s = sb / (v_cpu + v_g) + hbm_b / v_gpu
+        hg.hetegen_set_profiling(ctx, 1)
+        hg.hetegen_get_profile(ctx, reset=True)
+        nprof = min(2, args.steps)
+        for t in range(nprof):
+            step(args.warmup + t)
+        torch.cuda.synchronize()
+        prof = hg.hetegen_get_profile(ctx, reset=True)
+        hg.hetegen_set_profiling(ctx, 0)
+        wall_ms = prof["wall_ms"]
+        result["hetero"] = {
+            "alpha_cpu_by_linear": {NAMES[m]: round(alpha[streamed[0] + m], 4) for m in range(4)},
+            "probe_GBps": {k: {f: round(v[f] / 1e9, 2) for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps")}
+                           for k, v in probe.items()},
+            "streamed_bytes_per_step": sb, "h2d_bytes_per_step": h2d_b, "cpu_bytes_per_step": cpu_b,
+            "h2d_GBps_over_step": round(h2d_b / (ms_step * 1e-3) / 1e9, 2),
+            "h2d_frac_of_probe_link": round(h2d_b / (ms_step * 1e-3) / v_com, 4),
+            "cpu_GBps_over_step": round(cpu_b / (ms_step * 1e-3) / 1e9, 2),
+            "ideal_ms_per_step": round(ideal_s * 1e3, 3),
+            "frac_of_ideal": round(ideal_s * 1e3 / ms_step, 4),
+            "busy_frac": {"cpu": round(prof["cpu_ms"] / wall_ms, 4), "io": round(prof["h2d_ms"] / wall_ms, 4),
+                          "gpu": round(prof["gpu_ms"] / wall_ms, 4)},
+            "profiled_ms_per_step": round(wall_ms / nprof, 3),
+        }
+        log("hetero: %s" % json.dumps(result["hetero"]))
 
     # ---- CPU baseline: the oracle on a bounded sample of the same linears ----
     if not args.no_cpu_baseline:
@@ -181,8 +261,8 @@ def main():
         done_bytes, t_cpu, n_lin = 0, 0.0, 0
         xb = {k: synth.normal((B, k), dt, 0, 99) for k in (H, F)}
         ybuf = {}
-        i = 0
-        while t_cpu < budget_s and i < len(shp):
+        while t_cpu < budget_s and n_lin < 4 * len(shp):
+            i = n_lin % len(shp)
             n, k = shp[i]
             y = ybuf.setdefault(n, np.empty((B, n), np.float32))
             c0 = time.perf_counter()
@@ -190,11 +270,10 @@ def main():
             t_cpu += time.perf_counter() - c0
             done_bytes += n * k * 2
             n_lin += 1
-            i += 1
         result["cpu_baseline"] = {"value": round(done_bytes / t_cpu / 1e9, 3), "unit": "GB/s", "cores": threads,
                                   "kind": "oracle",
-                                  "sample": "first %d of the %d linears of one step (%.2f GB of weights), "
-                                            "batch %d, %.1f s" % (n_lin, len(shp), done_bytes / 1e9, B, t_cpu),
+                                  "sample": "%d linears in step order (%d per step; %.2f GB of weights), batch %d, "
+                                            "%.1f s" % (n_lin, len(shp), done_bytes / 1e9, B, t_cpu),
                                   "ms_per_token_extrapolated": round(t_cpu / done_bytes * wbytes * 1e3, 1)}
         log("oracle: %.3f GB/s on %d threads" % (done_bytes / t_cpu / 1e9, threads))
 
