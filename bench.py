@@ -82,6 +82,8 @@ def main():
     ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: OpenMP default)")
     ap.add_argument("--chunk-mb", type=int, default=32)
     ap.add_argument("--ring", type=int, default=8)
+    ap.add_argument("--exec", choices=("auto", "persistent", "graph", "eager"), default="auto",
+                    help="execution mode of an all-resident step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with one plain 256 MiB device-to-device copy, the reference dispatch for "
@@ -145,6 +147,9 @@ def main():
     t0 = time.time()
     model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, resident, max(B, 1))
     log("model ready in %.1f s (resident layers %d of %d)" % (time.time() - t0, res_layers, L))
+    if args.exec != "auto" and not streamed:
+        hg.hetegen_model_set_exec(model, {"persistent": hg.EXEC_PERSISTENT, "graph": hg.EXEC_GRAPH,
+                                          "eager": hg.EXEC_EAGER}[args.exec])
 
     # fresh input per step, resident in HBM before timing
     nstep = args.warmup + args.steps
@@ -200,20 +205,25 @@ def main():
                    "resident_layers": res_layers, "parallelism": "single GPU"},
     }
 
+    exec_mode = {1: "persistent", 2: "graph", 3: "eager"}.get(hg.hetegen_model_last_exec(model), "?")
+    result["config"]["exec"] = exec_mode
     if not streamed:
-        # dominant kernel: every dispatch of the replayed step is the GEMV kernel (LayerNorm,
-        # value slice, ReLU and residual are fused into it), so its average launch time is the
-        # event-timed region divided by the launches in it.
-        launches = 4 * L
+        # dominant kernel: every dispatch of the timed region is the GEMV kernel (LayerNorm,
+        # value slice, ReLU and residual are fused into it): one persistent step kernel per
+        # step, or one GEMV launch per linear; its average launch time is the event-timed
+        # region divided by the launches in it.
+        launches = 1 if exec_mode == "persistent" else 4 * L
         avg_us = ms_step * 1e3 / launches
         bytes_per_launch = (wbytes + sum(B * (n + k) * 2 + n * 2 for n, k in shp)) / launches
         achieved = bytes_per_launch / (avg_us * 1e-6) / 1e9
-        log("GEMV: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" % (avg_us, bytes_per_launch / 1e6, achieved))
+        log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
+            (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         result["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                               "frac": round(achieved / HBM_PEAK_GBPS, 4),
                               "traffic": counter_traffic(args.model, dt, B),
-                              "kernel": "gemv_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B),
+                              "kernel": "%s<%s,%d,...>" % ("step_kernel" if exec_mode == "persistent" else
+                                                           "gemv_kernel", "BF16" if dt == 1 else "F16", B),
                               "avg_launch_us": round(avg_us, 3), "bytes_per_launch": round(bytes_per_launch),
                               "launches_per_step": launches}
     else:

@@ -162,9 +162,33 @@ HETEGEN_API hetegen_status hetegen_model_set_alpha(hetegen_model* model, const d
  * 16-byte aligned; out_dev may not alias x_dev.  GPU work is enqueued on `stream`;
  * the call returns after the last CPU share.  When every linear is GPU-only and
  * resident, the step is captured once into a HIP graph per (B, x_dev, out_dev,
- * stream) and replayed. */
+ * stream) and replayed, or run as one persistent kernel, when selected (see HETEGEN_EXEC_*). */
 HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* model, const void* x_dev,
                                    void* out_dev, int B, void* stream);
+
+/* How hetegen_decode_step runs a step whose linears are all GPU-only and resident:
+ *   AUTO        per-linear launches (as EAGER), the fastest mode measured on MI355X
+ *   PERSISTENT  one cooperative launch per step: every workgroup takes the same
+ *               row block of every linear, grid barriers between linears, the
+ *               next linear's weights requested before each barrier
+ *   GRAPH       one GEMV launch per linear, captured once into a HIP graph
+ *   EAGER       one GEMV launch per linear, launched directly
+ * Steps with CPU rows or streamed linears always run eagerly.  All modes give
+ * bit-identical results. */
+#define HETEGEN_EXEC_AUTO 0
+#define HETEGEN_EXEC_PERSISTENT 1
+#define HETEGEN_EXEC_GRAPH 2
+#define HETEGEN_EXEC_EAGER 3
+
+/* Select the execution mode (UNSUPPORTED when a forced mode cannot run this
+ * model).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
+ * persistent mode (0: the default, seconds of waiting); a wait that gives up lets
+ * the step finish with undefined outputs and makes the next hetegen_decode_step
+ * on the model fail with HETEGEN_ERR_HIP.  A small limit exists to test that path. */
+HETEGEN_API hetegen_status hetegen_model_set_exec(hetegen_model* model, int mode, uint32_t barrier_spin_limit);
+
+/* Mode the last hetegen_decode_step on the model used (HETEGEN_EXEC_*), or -1. */
+HETEGEN_API int hetegen_model_last_exec(const hetegen_model* model);
 
 /* Optional trace of every linear's input and output (model dtype), for
  * teacher-forced checks.  Linear i writes its input [B, K_i] and then its output

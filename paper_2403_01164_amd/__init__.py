@@ -11,12 +11,19 @@ import os
 
 import numpy as np
 
+# torch first: it carries its own HIP runtime, whose SONAME (libamdhip64.so.7) then
+# satisfies the library's dependency, so the process holds ONE HIP runtime and
+# torch's device pointers and stream handles are valid in the library's calls.
+# Loading the library first would bring in /opt/rocm's runtime beside torch's.
+import torch  # noqa: F401
+
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhetegen.so")
 
 F16, BF16, F32 = 0, 1, 2
 OK, ERR_INVALID_ARG, ERR_NOT_PINNED, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP = range(6)
 PLAN_APPROX = 1
+EXEC_AUTO, EXEC_PERSISTENT, EXEC_GRAPH, EXEC_EAGER = 0, 1, 2, 3
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "NOT_PINNED", 3: "UNSUPPORTED", 4: "OOM", 5: "HIP"}
 
 if not os.path.exists(LIB_PATH):
@@ -61,6 +68,8 @@ _SIGS = {
     "hetegen_model_create": ([_vp, _i, _i, _i, _i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_d),
                               ctypes.POINTER(_i), _i, ctypes.POINTER(_vp)], _i),
     "hetegen_model_set_alpha": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_model_set_exec": ([_vp, _i, ctypes.c_uint32], _i),
+    "hetegen_model_last_exec": ([_vp], _i),
     "hetegen_decode_step": ([_vp, _vp, _vp, _vp, _i, _vp], _i),
     "hetegen_model_trace_bytes": ([_vp, _i], _sz),
     "hetegen_model_set_trace": ([_vp, _vp, _sz], _i),
@@ -161,6 +170,16 @@ def hetegen_model_set_alpha(model, alpha):
     rc = _lib.hetegen_model_set_alpha(model, a)
     if rc != OK:
         raise HetegenError(rc, "hetegen_model_set_alpha")
+
+
+def hetegen_model_set_exec(model, mode, barrier_spin_limit=0):
+    rc = _lib.hetegen_model_set_exec(model, mode, barrier_spin_limit)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_model_set_exec")
+
+
+def hetegen_model_last_exec(model):
+    return _lib.hetegen_model_last_exec(model)
 
 
 def hetegen_decode_step(ctx, model, x_dev, out_dev, B, stream=0):

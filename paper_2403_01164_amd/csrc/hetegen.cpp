@@ -43,6 +43,9 @@ double ms_since(Clock::time_point t0) {
 thread_local std::string g_create_error;
 
 constexpr size_t kDefaultChunk = 32ull << 20;
+constexpr uint32_t kDefaultSpinLimit = 1u << 22;  // polls of one grid-barrier wait (seconds)
+constexpr int kBarrierGroups = 16;
+constexpr size_t kCounterBytes = 256;
 constexpr int kDefaultRing = 8;
 constexpr int kMaxBatch = 8;
 
@@ -109,6 +112,21 @@ struct hetegen_model {
   int g_B = 0;
   const void* g_x = nullptr;
   void* g_out = nullptr;
+  // persistent step (one cooperative launch per step), per batch size
+  struct StepPlan {
+    bool built = false, ok = false;
+    void* table = nullptr;  // device StepLinear[4L]
+    int grid = 0;
+    size_t lds = 0;
+  };
+  StepPlan plan[kMaxBatch + 1];
+  uint32_t* counters = nullptr;  // device barrier counters
+  int ngroups = 0;
+  int* err_host = nullptr;       // pinned: set by a barrier wait that gave up
+  uint32_t barrier_base = 0;
+  uint32_t spin_limit = 0;       // 0: the kernel's default
+  int exec_mode = HETEGEN_EXEC_AUTO;
+  int last_exec = 0;
 };
 
 namespace {
@@ -700,6 +718,10 @@ namespace {
 void model_free(hetegen_model* m) {
   if (!m) return;
   if (m->gexec) (void)hipGraphExecDestroy(m->gexec);
+  for (auto& pl : m->plan)
+    if (pl.table) (void)hipFree(pl.table);
+  if (m->counters) (void)hipFree(m->counters);
+  if (m->err_host) (void)hipHostFree(m->err_host);
   if (m->arena) (void)hipFree(m->arena);
   if (m->act) (void)hipFree(m->act);
   (void)hipGetLastError();
@@ -764,6 +786,107 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
       TRY(run_linear(ctx, j, st));
     }
   }
+  return HETEGEN_OK;
+}
+
+// Launch plan of the persistent step for batch B: grid of co-resident workgroups
+// (up to 4 per CU), each linear's rows cut into equal contiguous blocks, and the
+// device table of the linears.  Leaves plan.ok false when the step cannot run
+// persistently (x too large for LDS, no cooperative launch, too little occupancy).
+hetegen_status build_plan(hetegen_ctx* ctx, hetegen_model* m, int B) {
+  auto& pl = m->plan[B];
+  pl.built = true;
+  pl.ok = false;
+  if (!m->graphable) return HETEGEN_OK;
+  int ncu = 0, coop = 0;
+  HIPCHK(ctx, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device));
+  HIPCHK(ctx, hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, ctx->device));
+  if (!coop || ncu < 1) return HETEGEN_OK;
+  const int unit = hg::gemv_rows_unit(B) * 4;
+  const int n = (int)m->lin.size();
+  for (int per_cu = 4; per_cu >= 1; --per_cu) {
+    const long long G = (long long)ncu * per_cu;
+    std::vector<int> rpw(n);
+    size_t lds = 0;
+    for (int i = 0; i < n; ++i) {
+      const long long units = (m->lin[i].n_gpu + unit - 1) / unit;
+      rpw[i] = (int)(((units + G - 1) / G) * unit);
+      lds = std::max(lds, hg::gemv_lds_bytes(B, m->lin[i].K, rpw[i]));
+    }
+    if (lds > hg::gemv_lds_limit()) return HETEGEN_OK;
+    if (hg::step_blocks_per_cu(m->dtype, B, lds) < per_cu) continue;
+    std::vector<hg::StepLinear> tab(n);
+    const int H = m->H, F = m->F;
+    for (int l = 0; l < m->L; ++l) {
+      for (int which = 0; which < 4; ++which) {
+        const int i = 4 * l + which;
+        const auto& lin = m->lin[i];
+        hg::StepLinear& d = tab[i];
+        d.W = lin.W_dev;
+        d.bias = lin.bias_dev;
+        d.rows = lin.n_gpu;
+        d.K = lin.K;
+        d.rpw = rpw[i];
+        switch (which) {
+          case 0:
+            d.x = m->xbuf; d.x_in = l == 0; d.ldx = H; d.ln = 1;
+            d.y = m->qkv; d.ldy = 3 * H; d.epi = hg::EPI_NONE;
+            break;
+          case 1:
+            d.x = (const char*)m->qkv + (size_t)2 * H * 2; d.ldx = 3 * H;
+            d.y = m->xbuf; d.ldy = H; d.epi = hg::EPI_RESID; d.resid = m->xbuf; d.resid_in = l == 0; d.ldr = H;
+            break;
+          case 2:
+            d.x = m->xbuf; d.ldx = H; d.ln = 1;
+            d.y = m->fbuf; d.ldy = F; d.epi = hg::EPI_RELU;
+            break;
+          default:
+            d.x = m->fbuf; d.ldx = F;
+            d.y = m->xbuf; d.y_out = l == m->L - 1; d.ldy = H; d.epi = hg::EPI_RESID; d.resid = m->xbuf; d.ldr = H;
+            break;
+        }
+      }
+    }
+    if (hipMalloc(&pl.table, sizeof(hg::StepLinear) * n) != hipSuccess) {
+      (void)hipGetLastError();
+      pl.table = nullptr;
+      return fail(ctx, HETEGEN_ERR_OOM, "persistent step table");
+    }
+    HIPCHK(ctx, hipMemcpy(pl.table, tab.data(), sizeof(hg::StepLinear) * n, hipMemcpyHostToDevice));
+    pl.grid = (int)G;
+    pl.lds = lds;
+    pl.ok = true;
+    return HETEGEN_OK;
+  }
+  return HETEGEN_OK;
+}
+
+// One persistent step; *launched is false when the launch was refused (the caller
+// falls back to another mode).
+hetegen_status run_persistent(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
+                              hipStream_t st, bool* launched) {
+  *launched = false;
+  auto& pl = m->plan[B];
+  if (!pl.built) TRY(build_plan(ctx, m, B));
+  if (!pl.ok) return HETEGEN_OK;
+  hg::StepArgs a{};
+  a.lin = (const hg::StepLinear*)pl.table;
+  a.nlin = (int)m->lin.size();
+  a.x_in = x_dev;
+  a.out = out_dev;
+  a.counters = m->counters;
+  a.barrier_base = m->barrier_base;
+  a.ngroups = m->ngroups;
+  a.err = m->err_host;
+  a.spin_limit = m->spin_limit ? m->spin_limit : kDefaultSpinLimit;
+  hipError_t e = hg::launch_step(a, m->dtype, B, pl.grid, pl.lds, st);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    pl.ok = false;  // do not try again for this batch size
+    return HETEGEN_OK;
+  }
+  m->barrier_base += (uint32_t)a.nlin;
+  *launched = true;
   return HETEGEN_OK;
 }
 
@@ -868,9 +991,34 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
   m->graphable = true;
   for (const auto& l : m->lin)
     if (l.n_cpu > 0 || !l.W_dev) m->graphable = false;
+  if (m->graphable) {
+    m->ngroups = kBarrierGroups;
+    const size_t cb = (size_t)(m->ngroups + 1) * kCounterBytes;
+    if (hipMalloc((void**)&m->counters, cb) != hipSuccess ||
+        hipHostMalloc((void**)&m->err_host, sizeof(int), hipHostMallocCoherent) != hipSuccess) {
+      (void)hipGetLastError();
+      model_free(m);
+      return fail(ctx, HETEGEN_ERR_OOM, "barrier counters");
+    }
+    *m->err_host = 0;
+    if (hipMemset(m->counters, 0, cb) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+      model_free(m);
+      return fail(ctx, HETEGEN_ERR_HIP, "barrier counter initialisation failed");
+    }
+  }
   *out = m;
   return HETEGEN_OK;
 }
+
+hetegen_status hetegen_model_set_exec(hetegen_model* m, int mode, uint32_t barrier_spin_limit) {
+  if (!m || mode < HETEGEN_EXEC_AUTO || mode > HETEGEN_EXEC_EAGER) return HETEGEN_ERR_INVALID_ARG;
+  if ((mode == HETEGEN_EXEC_PERSISTENT || mode == HETEGEN_EXEC_GRAPH) && !m->graphable) return HETEGEN_ERR_UNSUPPORTED;
+  m->exec_mode = mode;
+  m->spin_limit = barrier_spin_limit;
+  return HETEGEN_OK;
+}
+
+int hetegen_model_last_exec(const hetegen_model* m) { return m ? m->last_exec : -1; }
 
 hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {
   if (!m || !alpha) return HETEGEN_ERR_INVALID_ARG;
@@ -920,9 +1068,26 @@ hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* m, const voi
   if (!aligned16(x_dev) || !aligned16(out_dev)) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
   if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
     return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
+  if (m->err_host && *(volatile int*)m->err_host)
+    return fail(ctx, HETEGEN_ERR_HIP, "a grid-barrier wait of an earlier persistent step gave up; that step's "
+                                      "output is undefined");
   HIPCHK(ctx, hipSetDevice(ctx->device));
   hipStream_t st = (hipStream_t)stream;
-  const bool use_graph = m->graphable && !m->trace && !ctx->profiling;
+  // AUTO runs per-linear launches directly: on this device back-to-back GEMV launches
+  // leave no gap, and the grid barrier of the persistent step costs more than a launch
+  const bool fast = m->graphable && !m->trace && !ctx->profiling && m->exec_mode != HETEGEN_EXEC_EAGER &&
+                    m->exec_mode != HETEGEN_EXEC_AUTO;
+  if (fast && m->exec_mode == HETEGEN_EXEC_PERSISTENT) {
+    bool launched = false;
+    TRY(run_persistent(ctx, m, x_dev, out_dev, B, st, &launched));
+    if (launched) {
+      m->last_exec = HETEGEN_EXEC_PERSISTENT;
+      return finish_call(ctx, t0);
+    }
+    if (m->exec_mode == HETEGEN_EXEC_PERSISTENT)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "the persistent step cannot run for batch %d on this device", B);
+  }
+  const bool use_graph = fast;
   if (use_graph) {
     if (!m->gexec || m->g_B != B || m->g_x != x_dev || m->g_out != out_dev) {
       if (m->gexec) {
@@ -949,8 +1114,10 @@ hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* m, const voi
       m->g_out = out_dev;
     }
     HIPCHK(ctx, hipGraphLaunch(m->gexec, st));
+    m->last_exec = HETEGEN_EXEC_GRAPH;
     return finish_call(ctx, t0);
   }
+  m->last_exec = HETEGEN_EXEC_EAGER;
   hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, st);
   if (s != HETEGEN_OK) {
     ctx->planned.clear();

@@ -25,8 +25,53 @@ struct GemvParams {
   int epi;
   int y_f32;           // 1: y is float32, 0: y is the activation type
   int ln;
-  int ktile;           // K elements staged in LDS per pass (set by the launcher)
+  int ktile;           // set by the launcher: K elements staged in LDS per pass (tiled kernel)
+  int rpw;             // set by the launcher: rows per workgroup (contiguous block)
 };
+
+// One linear of the persistent decode step (a device-resident table entry).
+// x_in / resid_in / y_out select the step's input or output pointer instead of
+// the buffer stored here.
+struct StepLinear {
+  const void* W;
+  const void* bias;
+  const void* x;
+  long long ldx;
+  void* y;
+  long long ldy;
+  const void* resid;
+  long long ldr;
+  int rows, K, epi, ln, rpw;
+  int x_in, resid_in, y_out;
+};
+
+struct StepArgs {
+  const StepLinear* lin;  // device table of nlin entries
+  int nlin;
+  const void* x_in;
+  void* out;
+  uint32_t* counters;     // barrier counters: ngroups + 1 words, 256 bytes apart, zeroed at creation
+  uint32_t barrier_base;  // barriers completed by earlier steps on these counters
+  int ngroups;
+  int* err;               // set to 1 (system scope) if a barrier wait gave up
+  uint32_t spin_limit;    // polls before a barrier wait gives up
+};
+
+// Rows handed to one wavefront at a time by the GEMV for batch B; a workgroup's
+// row block is a multiple of 4x this.
+int gemv_rows_unit(int B);
+
+// Dynamic LDS of the main GEMV for batch B, reduction K and rows_per_block rows.
+size_t gemv_lds_bytes(int B, int K, int rows_per_block);
+
+// Largest LDS the main (non-tiled) GEMV and the persistent step accept.
+size_t gemv_lds_limit();
+
+// Co-resident workgroups of the persistent step kernel per CU (0 if unsupported).
+int step_blocks_per_cu(int dtype, int B, size_t lds);
+
+// Cooperative launch of the persistent step (grid must be co-resident).
+hipError_t launch_step(const StepArgs& a, int dtype, int B, int grid, size_t lds, hipStream_t stream);
 
 // dtype: 0 = fp16, 1 = bf16.  grid_cap bounds the number of workgroups
 // (0 = default).  Returns the launch status.

@@ -5,23 +5,27 @@
 // once its weight rows are in device memory).  At batch 1..8 a linear reads each
 // weight element once and does 2B flops on it, i.e. B flop per byte of fp16/bf16
 // weight: far below the ridge point of the vector ALUs, so the kernel is bound by
-// HBM bandwidth and uses no matrix cores.  Design:
-//  * one wavefront (64 lanes) owns R output rows at a time; a lane loads 16 bytes
-//    (8 elements) of each row per step, so one load instruction reads 1 KiB of a
-//    row, fully coalesced; U steps are unrolled so U*R 16-byte loads per lane are
-//    in flight;
-//  * x [B, K] is staged once per workgroup in LDS (in K tiles when it does not fit)
-//    and every lane reads its 8 elements per batch row with ds_read_b128, reused for
-//    the R rows it holds;
-//  * products accumulate in binary32 through v_dot2 (fp16 pairs or bf16 pairs with
-//    binary32 accumulation);
+// HBM bandwidth and uses no matrix cores.  Design of the main kernel:
+//  * a workgroup (4 wavefronts) owns a contiguous block of output rows; a
+//    wavefront takes R rows at a time and walks them in "tasks" of 64*U 16-byte
+//    chunks per row: a lane loads 16 bytes (8 elements) of each row per step, so
+//    one load instruction reads 1 KiB of a row, fully coalesced, and U*R loads per
+//    lane are in flight;
+//  * the loads of the next task are issued before the current task is computed
+//    (two register buffers), so a wavefront never waits on an empty memory pipe,
+//    and the weights of the first task are requested before the prologue;
+//  * weight loads are non-temporal: the weights are read once per step and should
+//    not evict x or the outputs from the caches;
+//  * x [B, K] is staged once per workgroup in LDS (and normalised there when a
+//    LayerNorm is fused) and read with ds_read_b128, reused for the R rows;
+//  * products accumulate in binary32 through v_dot2 (fp16 pairs or bf16 pairs);
 //  * the 64 lane partials of each (row, batch) pair are summed with DPP row
 //    permutations and four readlanes;
-//  * workgroups walk the row groups in a grid-stride loop, so x is staged once per
-//    workgroup rather than once per row group;
-//  * the epilogue adds the bias, applies ReLU or a residual sum and rounds to the
-//    activation type (or stores binary32), so the decode step needs no separate
-//    elementwise kernels; an optional LayerNorm prologue normalises x while staging it.
+//  * bias and residual of the block are staged in LDS in the prologue, outputs are
+//    gathered in LDS and stored per block with contiguous stores; the epilogue adds
+//    the bias, applies ReLU or a residual sum and rounds to the activation type (or
+//    stores binary32), so the decode step needs no elementwise kernels.
+// When x does not fit in LDS (large B*K), a K-tiled variant restages x per tile.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -38,9 +42,23 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Global-memory view of a pointer.  Pointers read from a device-side table are
+// generic to the compiler; generic (flat) loads also count against the LDS
+// counter, so every LDS wait would drain the weight stream.
+template <class T>
+__device__ __forceinline__ const __attribute__((address_space(1))) T* gmem(const T* p) {
+  return (const __attribute__((address_space(1))) T*)p;
+}
+
+// Cached 16-byte global load.
+__device__ __forceinline__ uint4 load_g16(const uint4* p) {
+  u32x4 v = *gmem((const u32x4*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Streaming 16-byte weight load (read once: marked non-temporal).
 __device__ __forceinline__ uint4 load_stream(const uint4* p) {
-  u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+  u32x4 v = __builtin_nontemporal_load(gmem((const u32x4*)p));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
@@ -108,13 +126,14 @@ __device__ __forceinline__ float wave_sum(float v) {
   return (r0 + r1) + (r2 + r3);
 }
 
-// LayerNorm statistics of B rows of x [B, K] for one 256-thread workgroup, two
-// passes (mean, then the mean of squared deviations).  The reduction order is
-// fixed by the thread mapping, so every workgroup of every kernel that calls this
-// gets bit-identical statistics.
-template <class T, int B>
-__device__ __forceinline__ void ln_stats(const uint16_t* __restrict__ x, long long ldx, int K, float* mean,
-                                         float* rstd, float (*red)[8][kWaves]) {
+// LayerNorm statistics of B rows of x (16-byte chunk c of row b read by get(b, c))
+// for one 256-thread workgroup, two passes (mean, then the mean of squared
+// deviations).  Chunk c is always summed by thread c % 256 in increasing c and the
+// partials are combined in a fixed tree, so every workgroup of every kernel that
+// calls this gets bit-identical statistics, whether x is read from global memory
+// or from LDS.
+template <class T, int B, class Get>
+__device__ __forceinline__ void ln_stats(Get get, int K, float* mean, float* rstd, float (*red)[8][kWaves]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n8 = K >> 3;
   float s[B];
@@ -122,9 +141,8 @@ __device__ __forceinline__ void ln_stats(const uint16_t* __restrict__ x, long lo
   for (int b = 0; b < B; ++b) {
     s[b] = 0.f;
     for (int c = tid; c < n8; c += kThreads) {
-      uint4 v = *(const uint4*)(x + b * ldx + (long long)c * 8);
       float f[8];
-      unpack8<T>(v, f);
+      unpack8<T>(get(b, c), f);
       s[b] += ((f[0] + f[1]) + (f[2] + f[3])) + ((f[4] + f[5]) + (f[6] + f[7]));
     }
     s[b] = wave_sum(s[b]);
@@ -137,9 +155,8 @@ __device__ __forceinline__ void ln_stats(const uint16_t* __restrict__ x, long lo
   for (int b = 0; b < B; ++b) {
     s[b] = 0.f;
     for (int c = tid; c < n8; c += kThreads) {
-      uint4 v = *(const uint4*)(x + b * ldx + (long long)c * 8);
       float f[8];
-      unpack8<T>(v, f);
+      unpack8<T>(get(b, c), f);
       float acc = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -171,19 +188,374 @@ __device__ __forceinline__ uint4 normalize8(const uint4& v, float mean, float rs
   return o;
 }
 
-template <class T>
-__device__ __forceinline__ void finish(float v, int epi, int y_f32, void* y, long long yi, const void* resid,
-                                       long long ri) {
-  if (epi == EPI_RELU) v = fmaxf(v, 0.f);
-  else if (epi == EPI_RESID) v = v + T::to_f32(((const uint16_t*)resid)[ri]);
-  if (y_f32) ((float*)y)[yi] = v;
-  else ((uint16_t*)y)[yi] = T::from_f32(v);
+// ReLU or residual sum on a binary32 value (bias already added).
+__device__ __forceinline__ float apply_epi(float v, int epi, float resid) {
+  if (epi == EPI_RELU) return fmaxf(v, 0.f);
+  if (epi == EPI_RESID) return v + resid;
+  return v;
 }
 
-// Stage tile [k0, k0 + kn) of x (optionally normalised) into LDS as [B][ktile].
+template <class T>
+__device__ __forceinline__ void store_y(void* y, long long i, int y_f32, float v) {
+  if (y_f32) ((float*)y)[i] = v;
+  else ((uint16_t*)y)[i] = T::from_f32(v);
+}
+
+// ---------------------------------------------------------------------------
+// Coherent accesses for data produced by other workgroups of the same kernel
+// (the persistent decode step): buffer loads/stores with sc0 sc1, which bypass
+// the non-coherent cache levels, so no L2 writeback/invalidate is needed between
+// linears.  Word 3 of the buffer descriptor is the gfx9 raw-buffer format.
+// ---------------------------------------------------------------------------
+constexpr int kBufWord3 = 0x00020000;
+constexpr int kCoherent = 1 | 16;  // sc0 | sc1
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
+}
+
+// The descriptor base must be wave-uniform (it lives in scalar registers): pass
+// the row base and a per-lane byte offset; `bytes` bounds the row.
+template <bool COH>
+__device__ __forceinline__ uint4 load_act16(const uint16_t* row, uint32_t bytes, uint32_t off) {
+  if (COH) {
+    u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rsrc(row, bytes), (int)off, 0, kCoherent);
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
+  return *(const uint4*)((const char*)row + off);
+}
+
+template <bool COH>
+__device__ __forceinline__ uint16_t load_act1(const uint16_t* row, uint32_t bytes, uint32_t off) {
+  if (COH) return (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(rsrc(row, bytes), (int)off, 0, kCoherent);
+  return *(const uint16_t*)((const char*)row + off);
+}
+
+// y row base (wave-uniform) and element index within the row.
+template <class T, bool COH>
+__device__ __forceinline__ void store_y_c(void* yrow, uint32_t n, uint32_t i, int y_f32, float v) {
+  if (COH) {
+    if (y_f32)
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc(yrow, n * 4), (int)(i * 4), 0,
+                                            kCoherent);
+    else
+      __builtin_amdgcn_raw_buffer_store_b16(T::from_f32(v), rsrc(yrow, n * 2), (int)(i * 2), 0, kCoherent);
+    return;
+  }
+  store_y<T>(yrow, i, y_f32, v);
+}
+
+// ---------------------------------------------------------------------------
+// Main GEMV, one workgroup's block of rows (x fits in LDS).  Dynamic LDS layout:
+//   xs [B][K/8] uint4 | bias [rpw] f32 | resid [B][rpw] f32 | out [B][rpw] f32
+// The first task of every wavefront is requested before `wait()` and the
+// prologue, so its weights stream in while the block waits for its inputs.
+// ---------------------------------------------------------------------------
+template <class T, int B, int R, int U, bool COH_LOAD, bool COH_STORE, class Wait>
+__device__ __forceinline__ void gemv_block(const GemvParams& p, int blk, uint4* smem, float (*red)[8][kWaves],
+                                           Wait wait) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = p.K, k8 = K >> 3, rpw = p.rpw;
+  uint4* xs = smem;
+  float* sb = (float*)(smem + (size_t)B * k8);
+  float* sr = sb + rpw;
+  float* sy = sr + B * rpw;
+  const int row_begin = blk * rpw;
+  const int nrows = max(0, min(rpw, p.rows - row_begin));
+  constexpr int SEG = 64 * U;  // 16-byte chunks per task and row
+  const int nseg = (k8 + SEG - 1) / SEG;
+  const int nrg = (nrows + R - 1) / R;
+  const int my_rg = nrg > wave ? (nrg - wave + kWaves - 1) / kWaves : 0;
+  const int ntask = my_rg * nseg;
+  const uint16_t* W = (const uint16_t*)p.W;
+
+  // task t of this wavefront: row group j = t / nseg (local rows (wave + j*kWaves)*R ..), segment t % nseg
+  auto load = [&](int t, uint4 (&w)[U][R]) {
+    const int j = t / nseg, seg = t - j * nseg;
+    const int lr0 = (wave + j * kWaves) * R;
+    const int c0 = seg * SEG + lane;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int row = row_begin + min(lr0 + r, nrows - 1);
+      const uint4* wr = (const uint4*)(W + (long long)row * K);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        // unconditional load (clamped address): no branch, so the compiler can keep
+        // later tasks' loads in flight; lanes past the row end reread its last
+        // chunk (same cache line, no extra traffic) and skip it in compute()
+        w[u][r] = load_stream(wr + min(c0 + 64 * u, k8 - 1));
+      }
+    }
+  };
+  auto compute = [&](int t, const uint4 (&w)[U][R], float (&acc)[R][B]) {
+    const int j = t / nseg, seg = t - j * nseg;
+    const int c0 = seg * SEG + lane;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + 64 * u;
+      if (c < k8) {
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          const uint4 xv = xs[b * k8 + c];
+#pragma unroll
+          for (int r = 0; r < R; ++r) acc[r][b] = dot8<T>(w[u][r], xv, acc[r][b]);
+        }
+      }
+    }
+    if (seg == nseg - 1) {  // row group complete: reduce and finish into LDS
+      const int lr0 = (wave + j * kWaves) * R;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          const float s = wave_sum(acc[r][b]);
+          acc[r][b] = 0.f;
+          const int lr = lr0 + r;
+          if (lane == 0 && lr < nrows) sy[b * rpw + lr] = apply_epi(s + sb[lr], p.epi, sr[b * rpw + lr]);
+        }
+      }
+    }
+  };
+
+  uint4 wa[U][R], wb[U][R];
+  float acc[R][B];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int b = 0; b < B; ++b) acc[r][b] = 0.f;
+  if (ntask > 0) load(0, wa);
+
+  wait();
+
+  // prologue: x, bias and residual of the block into LDS
+  {
+    const uint16_t* x = (const uint16_t*)p.x;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const uint16_t* xrow = x + b * p.ldx;
+      for (int c = tid; c < k8; c += kThreads) xs[b * k8 + c] = load_act16<COH_LOAD>(xrow, (uint32_t)K * 2, (uint32_t)c * 16);
+    }
+    const uint16_t* bias = (const uint16_t*)p.bias;
+    for (int i = tid; i < nrows; i += kThreads) sb[i] = bias ? T::to_f32(gmem(bias)[row_begin + i]) : 0.f;
+    if (p.epi == EPI_RESID) {
+      const uint16_t* res = (const uint16_t*)p.resid;
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        const uint16_t* rrow = res + b * p.ldr + row_begin;
+        for (int lr = tid; lr < nrows; lr += kThreads)
+          sr[b * rpw + lr] = T::to_f32(load_act1<COH_LOAD>(rrow, (uint32_t)nrows * 2, (uint32_t)lr * 2));
+      }
+    }
+    __syncthreads();
+    if (p.ln) {
+      float mean[B], rstd[B];
+      ln_stats<T, B>([&](int b, int c) { return xs[b * k8 + c]; }, K, mean, rstd, red);
+      const bool write_h = p.h_out != nullptr && blk == 0;
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        for (int c = tid; c < k8; c += kThreads) {  // each thread rewrites only the chunks it summed
+          const uint4 v = normalize8<T>(xs[b * k8 + c], mean[b], rstd[b]);
+          xs[b * k8 + c] = v;
+          if (write_h) *(uint4*)((uint16_t*)p.h_out + b * p.ldh + (long long)c * 8) = v;
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // main loop, two register buffers: loads of task t+1 are in flight while t is
+  // computed.  The loop body issues its loads unconditionally; the last one or two
+  // tasks are peeled.
+  int t = 0;
+  for (; t + 2 < ntask; t += 2) {
+    load(t + 1, wb);
+    compute(t, wa, acc);
+    load(t + 2, wa);
+    compute(t + 1, wb, acc);
+  }
+  if (t + 1 < ntask) {
+    load(t + 1, wb);
+    compute(t, wa, acc);
+    compute(t + 1, wb, acc);
+  } else if (t < ntask) {
+    compute(t, wa, acc);
+  }
+
+  // block outputs: contiguous stores
+  __syncthreads();
+  const size_t ys = p.y_f32 ? 4 : 2;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    void* yrow = (char*)p.y + ((size_t)b * p.ldy + row_begin) * ys;
+    for (int lr = tid; lr < nrows; lr += kThreads)
+      store_y_c<T, COH_STORE>(yrow, (uint32_t)nrows, (uint32_t)lr, p.y_f32, sy[b * rpw + lr]);
+  }
+}
+
+template <class T, int B, int R, int U>
+__global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
+  extern __shared__ uint4 smem[];
+  __shared__ float red[2][8][kWaves];
+  gemv_block<T, B, R, U, false, false>(p, blockIdx.x, smem, red, [] {});
+}
+
+// ---------------------------------------------------------------------------
+// Batch-1 GEMV without a fused LayerNorm: x is read straight from L1/L2 inside
+// the task loop (it is the same 2*K bytes for every wavefront, so it stays
+// cached), which removes the LDS prologue and its barrier; bias and residual are
+// requested with the task's weights and lane 0 stores each finished row.  Each
+// lane accumulates its chunks in the same order as gemv_block, so both kernels
+// give bit-identical results.
+// ---------------------------------------------------------------------------
+template <class T, int U>
+__global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int K = p.K, k8 = K >> 3, rpw = p.rpw;
+  const int row_begin = blockIdx.x * rpw;
+  const int nrows = min(rpw, p.rows - row_begin);  // >= 1: the grid covers rows exactly
+  constexpr int SEG = 64 * U;
+  const int nseg = (k8 + SEG - 1) / SEG;
+  const int my_rg = nrows > wave ? (nrows - wave + kWaves - 1) / kWaves : 0;
+  const int ntask = my_rg * nseg;
+  const uint16_t* W = (const uint16_t*)p.W;
+  const uint4* x = (const uint4*)p.x;
+  const uint16_t* bias = (const uint16_t*)p.bias;
+  const uint16_t* res = p.epi == EPI_RESID ? (const uint16_t*)p.resid : bias;
+  const bool has_bias = bias != nullptr;
+  struct Buf {
+    uint4 w[U], x[U];
+    uint16_t b, r;
+  };
+  auto load = [&](int t, Buf& f) {
+    const int j = t / nseg, seg = t - j * nseg;
+    const int row = row_begin + wave + j * kWaves;
+    const uint4* wr = (const uint4*)(W + (long long)row * K);
+    const int c0 = seg * SEG + lane;
+#pragma unroll
+    for (int u = 0; u < U; ++u) f.w[u] = load_stream(wr + min(c0 + 64 * u, k8 - 1));
+#pragma unroll
+    for (int u = 0; u < U; ++u) f.x[u] = load_g16(x + min(c0 + 64 * u, k8 - 1));
+    // the row's bias and residual travel with every task (no dependent load at the row end)
+    f.b = has_bias ? gmem(bias)[row] : (uint16_t)0;
+    f.r = res ? gmem(res)[row] : (uint16_t)0;
+  };
+  float acc = 0.f;
+  auto compute = [&](int t, const Buf& f) {
+    const int j = t / nseg, seg = t - j * nseg;
+    const int c0 = seg * SEG + lane;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (c0 + 64 * u < k8) acc = dot8<T>(f.w[u], f.x[u], acc);
+    if (seg == nseg - 1) {
+      const float s = wave_sum(acc);
+      acc = 0.f;
+      if (lane == 0) {
+        const int row = row_begin + wave + j * kWaves;
+        const float v = apply_epi(s + (has_bias ? T::to_f32(f.b) : 0.f), p.epi, T::to_f32(f.r));
+        store_y<T>(p.y, row, p.y_f32, v);
+      }
+    }
+  };
+  Buf fa, fb;
+  if (ntask > 0) load(0, fa);
+  int t = 0;
+  for (; t + 2 < ntask; t += 2) {
+    load(t + 1, fb);
+    compute(t, fa);
+    load(t + 2, fa);
+    compute(t + 1, fb);
+  }
+  if (t + 1 < ntask) {
+    load(t + 1, fb);
+    compute(t, fa);
+    compute(t + 1, fb);
+  } else if (t < ntask) {
+    compute(t, fa);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent decode step: one cooperative launch runs every linear of the step,
+// each workgroup taking the same row block of every linear, with a grid barrier
+// between dependent linears.  A workgroup requests the weights of its first
+// task of linear i+1 before it waits at the barrier of linear i, so HBM keeps
+// streaming through the barrier and the next prologue.
+// Barrier: workgroups arrive on one of `ngroups` counters (blockIdx % ngroups);
+// the last arrival of a group bumps the top counter, which the waiting
+// workgroups poll.  Counters only grow (wrap-safe comparisons); barrier n of the
+// model's lifetime completes when the top counter reaches (n + 1) * ngroups.
+// The wait gives up after a bounded number of polls, records the failure in
+// `err` and lets the kernel run to its end, so the grid always drains.
+// ---------------------------------------------------------------------------
+constexpr int kCounterStride = 64;  // uint32 words: one 256-byte line per counter
+
+__device__ __forceinline__ bool reached(uint32_t v, uint32_t target) { return (int32_t)(v - target) >= 0; }
+
+__device__ __forceinline__ void grid_arrive(const StepArgs& a, uint32_t n) {
+  // every thread's output stores have completed (coherent stores: visible device-wide)
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int g = blockIdx.x % a.ngroups;
+    const uint32_t gsize = gridDim.x / a.ngroups + ((uint32_t)g < gridDim.x % a.ngroups ? 1u : 0u);
+    const uint32_t old =
+        __hip_atomic_fetch_add(a.counters + g * kCounterStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old + 1u == (n + 1u) * gsize)
+      __hip_atomic_fetch_add(a.counters + a.ngroups * kCounterStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+__device__ __forceinline__ void grid_wait(const StepArgs& a, uint32_t n) {
+  if (threadIdx.x == 0) {
+    const uint32_t target = (n + 1u) * (uint32_t)a.ngroups;
+    const uint32_t* top = a.counters + a.ngroups * kCounterStride;
+    uint32_t spins = 0;
+    while (!reached(__hip_atomic_load(top, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), target)) {
+      if (++spins > a.spin_limit) {
+        __hip_atomic_store(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  __syncthreads();
+}
+
+template <class T, int B, int R, int U>
+__global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
+  extern __shared__ uint4 smem[];
+  __shared__ float red[2][8][kWaves];
+  for (int i = 0; i < a.nlin; ++i) {
+    const StepLinear& d = a.lin[i];
+    GemvParams p{};
+    p.x = d.x_in ? a.x_in : d.x;
+    p.ldx = d.ldx;
+    p.W = d.W;
+    p.bias = d.bias;
+    p.y = d.y_out ? a.out : d.y;
+    p.ldy = d.ldy;
+    p.resid = d.resid_in ? a.x_in : d.resid;
+    p.ldr = d.ldr;
+    p.rows = d.rows;
+    p.K = d.K;
+    p.epi = d.epi;
+    p.ln = d.ln;
+    p.rpw = d.rpw;
+    const uint32_t n = a.barrier_base + (uint32_t)i;
+    gemv_block<T, B, R, U, true, true>(p, blockIdx.x, smem, red, [&] {
+      if (i > 0) grid_wait(a, n - 1u);
+    });
+    grid_arrive(a, n);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// K-tiled GEMV for x that does not fit in LDS: x is restaged per K tile and row
+// group (grid-stride over row groups).
+// ---------------------------------------------------------------------------
 template <class T, int B>
-__device__ __forceinline__ void stage_x(const GemvParams& p, uint4* xs, int k0, int kn, const float* mean,
-                                        const float* rstd, bool write_h) {
+__device__ __forceinline__ void stage_x_tile(const GemvParams& p, uint4* xs, int k0, int kn, const float* mean,
+                                             const float* rstd, bool write_h) {
   const uint16_t* x = (const uint16_t*)p.x;
   const int n8 = kn >> 3, kt8 = p.ktile >> 3;
 #pragma unroll
@@ -200,7 +572,7 @@ __device__ __forceinline__ void stage_x(const GemvParams& p, uint4* xs, int k0, 
 }
 
 template <class T, int B, int R, int U>
-__global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
+__global__ __launch_bounds__(kThreads) void gemv_tiled_kernel(GemvParams p) {
   extern __shared__ uint4 xs[];
   __shared__ float red[2][8][kWaves];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -209,12 +581,11 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
   float mean[B], rstd[B];
 #pragma unroll
   for (int b = 0; b < B; ++b) { mean[b] = 0.f; rstd[b] = 1.f; }
-  if (p.ln) ln_stats<T, B>((const uint16_t*)p.x, p.ldx, K, mean, rstd, red);
+  const uint16_t* x = (const uint16_t*)p.x;
+  if (p.ln)
+    ln_stats<T, B>([&](int b, int c) { return *(const uint4*)(x + b * p.ldx + (long long)c * 8); }, K, mean, rstd,
+                   red);
   const bool wg_writes_h = p.ln && p.h_out != nullptr && blockIdx.x == 0;
-  if (ntiles == 1) {
-    stage_x<T, B>(p, xs, 0, K, mean, rstd, wg_writes_h);
-    __syncthreads();
-  }
   const int nrg = (p.rows + R - 1) / R;
   const uint16_t* W = (const uint16_t*)p.W;
   const uint16_t* bias = (const uint16_t*)p.bias;
@@ -225,10 +596,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
     const int row0 = rg * R;
     const uint4* wp[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      int row = min(row0 + r, p.rows - 1);
-      wp[r] = (const uint4*)(W + (long long)row * K);
-    }
+    for (int r = 0; r < R; ++r) wp[r] = (const uint4*)(W + (long long)min(row0 + r, p.rows - 1) * K);
     float acc[R][B];
 #pragma unroll
     for (int r = 0; r < R; ++r)
@@ -236,17 +604,14 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
       for (int b = 0; b < B; ++b) acc[r][b] = 0.f;
     for (int t = 0; t < ntiles; ++t) {
       const int k0 = t * ktile, kn = min(ktile, K - k0);
-      if (ntiles > 1) {
-        __syncthreads();
-        stage_x<T, B>(p, xs, k0, kn, mean, rstd, wg_writes_h && first);
-        __syncthreads();
-      }
+      __syncthreads();
+      stage_x_tile<T, B>(p, xs, k0, kn, mean, rstd, wg_writes_h && first);
+      __syncthreads();
       if (valid) {
         const int n8 = kn >> 3, c0 = k0 >> 3;
         int c = lane;
         for (; c + 64 * (U - 1) < n8; c += 64 * U) {
           uint4 w[U][R];
-          uint4 xv[U][B];
 #pragma unroll
           for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -254,13 +619,11 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
 #pragma unroll
           for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int b = 0; b < B; ++b) xv[u][b] = xs[b * kt8 + c + 64 * u];
+            for (int b = 0; b < B; ++b) {
+              const uint4 xv = xs[b * kt8 + c + 64 * u];
 #pragma unroll
-          for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int r = 0; r < R; ++r)
-#pragma unroll
-              for (int b = 0; b < B; ++b) acc[r][b] = dot8<T>(w[u][r], xv[u][b], acc[r][b]);
+              for (int r = 0; r < R; ++r) acc[r][b] = dot8<T>(w[u][r], xv, acc[r][b]);
+            }
         }
         for (; c < n8; c += 64) {
           uint4 w[R];
@@ -268,7 +631,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
           for (int r = 0; r < R; ++r) w[r] = load_stream(wp[r] + c0 + c);
 #pragma unroll
           for (int b = 0; b < B; ++b) {
-            uint4 xv = xs[b * kt8 + c];
+            const uint4 xv = xs[b * kt8 + c];
 #pragma unroll
             for (int r = 0; r < R; ++r) acc[r][b] = dot8<T>(w[r], xv, acc[r][b]);
           }
@@ -284,7 +647,8 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
           const int row = row0 + r;
           if (lane == 0 && row < p.rows) {
             if (bias) s += T::to_f32(bias[row]);
-            finish<T>(s, p.epi, p.y_f32, p.y, b * p.ldy + row, p.resid, b * p.ldr + row);
+            const float rv = p.epi == EPI_RESID ? T::to_f32(((const uint16_t*)p.resid)[b * p.ldr + row]) : 0.f;
+            store_y<T>(p.y, b * p.ldy + row, p.y_f32, apply_epi(s, p.epi, rv));
           }
         }
       }
@@ -299,7 +663,7 @@ __global__ __launch_bounds__(kThreads) void layernorm_kernel(const uint16_t* __r
                                                              float* __restrict__ h_host) {
   __shared__ float red[2][8][kWaves];
   float mean[B], rstd[B];
-  ln_stats<T, B>(x, ldx, K, mean, rstd, red);
+  ln_stats<T, B>([&](int b, int c) { return *(const uint4*)(x + b * ldx + (long long)c * 8); }, K, mean, rstd, red);
   const int n8 = K >> 3;
 #pragma unroll
   for (int b = 0; b < B; ++b) {
@@ -339,11 +703,12 @@ __global__ __launch_bounds__(kThreads) void import_kernel(const float* __restric
   const long long total = (long long)B * n;
   for (long long i = (long long)blockIdx.x * kThreads + threadIdx.x; i < total; i += (long long)gridDim.x * kThreads) {
     const int b = (int)(i / n), c = (int)(i - (long long)b * n);
-    finish<T>(src[i], epi, y_f32, y, b * ldy + c, resid, b * ldr + c);
+    const float rv = epi == EPI_RESID ? T::to_f32(((const uint16_t*)resid)[b * ldr + c]) : 0.f;
+    store_y<T>(y, b * ldy + c, y_f32, apply_epi(src[i], epi, rv));
   }
 }
 
-// Per-batch tiling: rows per wavefront R and unrolled steps U (U*R loads in flight).
+// Per-batch tiling: rows per wavefront R and 16-byte steps per task U (U*R loads in flight).
 template <int B> struct Tile;
 template <> struct Tile<1> { static constexpr int R = 1, U = 8; };
 template <> struct Tile<2> { static constexpr int R = 2, U = 4; };
@@ -354,22 +719,43 @@ template <> struct Tile<6> { static constexpr int R = 4, U = 2; };
 template <> struct Tile<7> { static constexpr int R = 4, U = 2; };
 template <> struct Tile<8> { static constexpr int R = 4, U = 2; };
 
-constexpr int kLdsBudget = 32768;  // bytes of LDS for the x tile per workgroup
+constexpr size_t kLdsMain = 65536 - 1024;  // dynamic LDS of the main kernel (x, bias, residual, outputs)
+constexpr int kTiledLdsBudget = 32768;  // bytes of x per tile in the K-tiled kernel
 constexpr int kDefaultGridCap = 1024;
 
 template <class T, int B>
 hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
   constexpr int R = Tile<B>::R, U = Tile<B>::U;
-  int kt = kLdsBudget / (2 * B);
+  const int cap = grid_cap > 0 ? grid_cap : kDefaultGridCap;
+  if (B == 1 && !p.ln) {
+    constexpr int U1 = 4;
+    const long long units = (p.rows + kWaves - 1) / kWaves;
+    const long long per = (units + cap - 1) / cap;
+    p.rpw = (int)(per * kWaves);
+    const int grid = (int)((p.rows + p.rpw - 1) / p.rpw);
+    hipLaunchKernelGGL((gemv_x1_kernel<T, U1>), dim3(grid), dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+  }
+  // contiguous row blocks of a multiple of R*kWaves rows, at most `cap` blocks
+  const int unit = R * kWaves;
+  const long long units = (p.rows + unit - 1) / unit;
+  const long long per = (units + cap - 1) / cap;
+  const int rpw = (int)(per * unit);
+  const size_t lds = (size_t)B * p.K * 2 + (size_t)(1 + 2 * B) * rpw * 4;  // gemv_lds_bytes
+  if (lds <= kLdsMain) {
+    p.rpw = rpw;
+    p.ktile = p.K;
+    const int grid = (int)((p.rows + rpw - 1) / rpw);
+    hipLaunchKernelGGL((gemv_kernel<T, B, R, U>), dim3(grid), dim3(kThreads), lds, s, p);
+    return hipGetLastError();
+  }
+  int kt = kTiledLdsBudget / (2 * B);
   kt -= kt % 512;
-  if (p.K <= kt) kt = p.K;
   p.ktile = kt;
   const int nrg = (p.rows + R - 1) / R;
   int grid = (nrg + kWaves - 1) / kWaves;
-  const int cap = grid_cap > 0 ? grid_cap : kDefaultGridCap;
   if (grid > cap) grid = cap;
-  const size_t lds = (size_t)B * kt * 2;
-  hipLaunchKernelGGL((gemv_kernel<T, B, R, U>), dim3(grid), dim3(kThreads), lds, s, p);
+  hipLaunchKernelGGL((gemv_tiled_kernel<T, B, R, U>), dim3(grid), dim3(kThreads), (size_t)B * kt * 2, s, p);
   return hipGetLastError();
 }
 
@@ -414,6 +800,21 @@ hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long
   return hipErrorInvalidValue;
 }
 
+template <class T>
+const void* step_fn(int B) {
+  switch (B) {
+    case 1: return (const void*)step_kernel<T, 1, Tile<1>::R, Tile<1>::U>;
+    case 2: return (const void*)step_kernel<T, 2, Tile<2>::R, Tile<2>::U>;
+    case 3: return (const void*)step_kernel<T, 3, Tile<3>::R, Tile<3>::U>;
+    case 4: return (const void*)step_kernel<T, 4, Tile<4>::R, Tile<4>::U>;
+    case 5: return (const void*)step_kernel<T, 5, Tile<5>::R, Tile<5>::U>;
+    case 6: return (const void*)step_kernel<T, 6, Tile<6>::R, Tile<6>::U>;
+    case 7: return (const void*)step_kernel<T, 7, Tile<7>::R, Tile<7>::U>;
+    case 8: return (const void*)step_kernel<T, 8, Tile<8>::R, Tile<8>::U>;
+  }
+  return nullptr;
+}
+
 int small_grid(long long work_items) {
   long long g = (work_items + kThreads - 1) / kThreads;
   if (g < 1) g = 1;
@@ -422,6 +823,37 @@ int small_grid(long long work_items) {
 }
 
 }  // namespace
+
+int gemv_rows_unit(int B) {
+  static const int r[9] = {0, Tile<1>::R, Tile<2>::R, Tile<3>::R, Tile<4>::R,
+                           Tile<5>::R, Tile<6>::R, Tile<7>::R, Tile<8>::R};
+  return (B >= 1 && B <= 8) ? r[B] : 0;
+}
+
+size_t gemv_lds_bytes(int B, int K, int rows_per_block) {
+  return (size_t)B * K * 2 + (size_t)(1 + 2 * B) * rows_per_block * 4;
+}
+
+size_t gemv_lds_limit() { return kLdsMain; }
+
+int step_blocks_per_cu(int dtype, int B, size_t lds) {
+  const void* f = dtype == 1 ? step_fn<BF16>(B) : step_fn<F16>(B);
+  if (!f) return 0;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, kThreads, lds) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return n;
+}
+
+hipError_t launch_step(const StepArgs& a, int dtype, int B, int grid, size_t lds, hipStream_t stream) {
+  const void* f = dtype == 1 ? step_fn<BF16>(B) : step_fn<F16>(B);
+  if (!f) return hipErrorInvalidValue;
+  StepArgs args = a;
+  void* kargs[] = {(void*)&args};
+  return hipLaunchCooperativeKernel(f, dim3(grid), dim3(kThreads), kargs, (unsigned)lds, stream);
+}
 
 hipError_t launch_gemv(GemvParams p, int dtype, int B, hipStream_t stream, int grid_cap) {
   if (p.rows <= 0) return hipSuccess;

@@ -87,3 +87,11 @@ def test_create_rejects_bad_config():
     with pytest.raises(hg.HetegenError) as e:
         hg.hetegen_create(0, chunk_bytes=100)
     assert e.value.status == hg.ERR_INVALID_ARG
+
+
+def test_single_hip_runtime_in_process():
+    # the binding imports torch before the library, so only one libamdhip64 is mapped
+    import torch  # noqa: F401
+    maps = open("/proc/self/maps").read()
+    paths = {l.split()[-1] for l in maps.splitlines() if "libamdhip64" in l}
+    assert len(paths) == 1, paths

@@ -216,3 +216,74 @@ def test_opt13b_shape_one_layer_hetero(ctx):
         assert np.array_equal(out, last)
     finally:
         m.free()
+
+
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+@pytest.mark.parametrize("B", [1, 2, 5, 8])
+def test_exec_modes_bit_identical(ctx, dtype, B):
+    # persistent (one cooperative launch, grid barriers), graph replay and eager
+    # per-linear launches compute every output row the same way
+    L, H, F = 3, 512, 2048
+    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    try:
+        xs = [synth.normal((B, H), dtype, 0, synth.act_id(t)) for t in range(3)]
+        outs = {}
+        for mode in (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT, hg.EXEC_AUTO):
+            hg.hetegen_model_set_exec(m.m, mode)
+            outs[mode] = [m.step(x) for x in xs] + [m.step(xs[0])]
+            want = {hg.EXEC_AUTO: hg.EXEC_EAGER}.get(mode, mode)
+            assert hg.hetegen_model_last_exec(m.m) == want
+        for mode, o in outs.items():
+            for a, b in zip(o, outs[hg.EXEC_EAGER]):
+                assert np.array_equal(a, b), mode
+        # and the persistent result is the teacher-forced-checked eager result
+        _, tr = m.step(xs[1], trace=True)
+        last, _ = m.check_teacher_forced(xs[1], tr)
+        assert np.array_equal(outs[hg.EXEC_PERSISTENT][1], last)
+    finally:
+        m.free()
+
+
+def test_persistent_opt67b_shapes_two_layers(ctx):
+    dtype, L, H, F = synth.F16, 2, 4096, 16384
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
+    try:
+        x = synth.normal((1, H), dtype, 0, synth.act_id(0))
+        hg.hetegen_model_set_exec(m.m, hg.EXEC_EAGER)
+        eager = m.step(x)
+        hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT)
+        for _ in range(3):
+            assert np.array_equal(m.step(x), eager)
+    finally:
+        m.free()
+
+
+def test_barrier_wait_that_gives_up_is_reported(ctx):
+    # a spin limit of one poll makes waits give up (outputs undefined, kernel still
+    # drains); the next step on the model must report the failure
+    dtype, L, H, F = synth.F16, 2, 256, 1024
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
+    try:
+        x = synth.normal((1, H), dtype, 0, synth.act_id(0))
+        hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT, 1)
+        for _ in range(4):
+            m.step(x)
+            try:
+                m.step(x)
+            except hg.HetegenError as e:
+                assert e.status == hg.ERR_HIP and "barrier" in str(e)
+                return
+        pytest.skip("every barrier completed within one poll; the failure path was not reached")
+    finally:
+        m.free()
+
+
+def test_forced_modes_rejected_for_split_models(ctx):
+    m = Model(ctx, 1, 256, 1024, synth.F16, 0.5, 0, max_batch=1)
+    try:
+        with pytest.raises(hg.HetegenError) as e:
+            hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT)
+        assert e.value.status == hg.ERR_UNSUPPORTED
+        hg.hetegen_model_set_exec(m.m, hg.EXEC_EAGER)
+    finally:
+        m.free()
