@@ -161,8 +161,8 @@ HETEGEN_API hetegen_status hetegen_model_set_alpha(hetegen_model* model, const d
 /* One decode step: out_dev [B, H] = step(x_dev [B, H]); both device, model dtype,
  * 16-byte aligned; out_dev may not alias x_dev.  GPU work is enqueued on `stream`;
  * the call returns after the last CPU share.  When every linear is GPU-only and
- * resident, the step is captured once into a HIP graph per (B, x_dev, out_dev,
- * stream) and replayed, or run as one persistent kernel, when selected (see HETEGEN_EXEC_*). */
+ * resident, the step can instead be replayed from a HIP graph captured once per
+ * (B, x_dev, out_dev, stream) or run as one persistent kernel (HETEGEN_EXEC_*). */
 HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* model, const void* x_dev,
                                    void* out_dev, int B, void* stream);
 
