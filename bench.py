@@ -75,10 +75,19 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--model", default="opt-6.7b", choices=sorted(OPT))
     ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=0,
+                    help="run only the first N decoder layers (0: all); reported in config")
     ap.add_argument("--placement", choices=("all", "half", "none"), default=None,
                     help="HBM-resident layers: all, the first half, or none (default per model)")
     ap.add_argument("--alpha", type=float, default=None,
                     help="fixed CPU fraction for every streamed linear (default: the planner's)")
+    ap.add_argument("--alpha-sweep", default=None,
+                    help="comma-separated CPU fractions for the streamed linears, each timed after the main "
+                         "measurement (e.g. 0,0.1,0.2,0.3,0.4,0.5)")
+    ap.add_argument("--sweep-steps", type=int, default=2)
+    ap.add_argument("--alpha-bench", action="store_true",
+                    help="refine the streamed linears' CPU fractions with the step-level alpha benchmark "
+                         "(Sec. 4.4) and time the step with both the closed-form and the refined fractions")
     ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: OpenMP default)")
     ap.add_argument("--chunk-mb", type=int, default=32)
     ap.add_argument("--ring", type=int, default=8)
@@ -102,6 +111,9 @@ def main():
 
     torch.cuda.set_device(0)
     L, H, F, dt, placement = OPT[args.model]
+    L_full = L
+    if args.layers:
+        L = min(L, args.layers)
     placement = args.placement or placement
     B = args.batch
     ctx = hg.hetegen_create(0, cpu_threads=args.threads, chunk_bytes=args.chunk_mb << 20, ring_depth=args.ring)
@@ -144,6 +156,7 @@ def main():
     alpha = hg.hetegen_layer_plan([(n, k, dt, resident[i]) for i, (n, k) in enumerate(shp)], bws)
     if args.alpha is not None:
         alpha = [0.0 if resident[i] else args.alpha for i in range(4 * L)]
+    alpha_closed = list(alpha)
     t0 = time.time()
     model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, resident, max(B, 1))
     log("model ready in %.1f s (resident layers %d of %d)" % (time.time() - t0, res_layers, L))
@@ -160,6 +173,16 @@ def main():
 
     def step(t):
         hg.hetegen_decode_step(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, sptr)
+
+    refined = None
+    if args.alpha_bench and streamed:
+        t0 = time.time()
+        delta, crossed = hg.hetegen_model_alpha_benchmark(ctx, model, xs[0].data_ptr(), out[0].data_ptr(), B,
+                                                          0.08, 0.02, 2, 2, hg.BENCH_WALL, sptr)
+        alpha = hg.hetegen_model_get_alpha(model, 4 * L)
+        refined = {"delta": round(delta, 4), "crossed": crossed,
+                   "alpha_cpu_by_linear": {NAMES[m]: round(alpha[streamed[0] + m], 4) for m in range(4)}}
+        log("step-level alpha benchmark (wall-time objective): delta %+.4f in %.1f s" % (delta, time.time() - t0))
 
     for t in range(args.warmup):
         step(t)
@@ -200,7 +223,8 @@ def main():
         "dtype": "bf16" if dt == 1 else "f16",
         "data": "synthetic: seeded N(0,0.02) weights, N(0,1) activations (no checkpoints)",
         "config": {"workload": "%s-shaped decode step, %d layers x {qkv,out,fc1,fc2}, %s, batch %d" %
-                               (args.model.upper(), L, desc, B),
+                               (args.model.upper(), L, desc, B) +
+                               ("" if L == L_full else " (first %d of the model's %d layers)" % (L, L_full)),
                    "layers": L, "hidden": H, "ffn": F, "batch": B, "weight_bytes_per_step": wbytes,
                    "resident_layers": res_layers, "parallelism": "single GPU"},
     }
@@ -262,6 +286,45 @@ def main():
             "profiled_ms_per_step": round(wall_ms / nprof, 3),
         }
         log("hetero: %s" % json.dumps(result["hetero"]))
+
+    if refined:
+        # the same step with the closed-form fractions, for comparison
+        hg.hetegen_model_set_alpha(model, alpha_closed)
+        step(0)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for t in range(args.steps):
+            step(args.warmup + t)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_closed = e0.elapsed_time(e1) / args.steps
+        hg.hetegen_model_set_alpha(model, alpha)
+        result["alpha_benchmark"] = dict(refined, ms_per_step_closed_form=round(ms_closed, 3),
+                                         ms_per_step_refined=round(ms_step, 3))
+        log("closed-form alpha: %.2f ms/token; refined: %.2f ms/token" % (ms_closed, ms_step))
+
+    # ---- latency vs CPU fraction of the streamed linears ----
+    if args.alpha_sweep and streamed:
+        sweep = []
+        for a_s in [float(v) for v in args.alpha_sweep.split(",")]:
+            hg.hetegen_model_set_alpha(model, [0.0 if resident[i] else a_s for i in range(4 * L)])
+            step(0)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for t in range(args.sweep_steps):
+                step(1 + t)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms_a = e0.elapsed_time(e1) / args.sweep_steps
+            h2d_a = sum((shp[i][0] - min(shp[i][0], int(np.floor(a_s * shp[i][0] + 0.5)))) * shp[i][1] * 2
+                        for i in streamed)
+            sweep.append({"alpha_cpu": a_s, "ms_per_step": round(ms_a, 3),
+                          "GBps": round(wbytes / (ms_a * 1e-3) / 1e9, 2),
+                          "h2d_GBps_over_step": round(h2d_a / (ms_a * 1e-3) / 1e9, 2)})
+            log("alpha %.2f: %.2f ms/token, %.1f GB/s, link %.1f GB/s" %
+                (a_s, ms_a, wbytes / (ms_a * 1e-3) / 1e9, h2d_a / (ms_a * 1e-3) / 1e9))
+        hg.hetegen_model_set_alpha(model, alpha)
+        result["alpha_sweep"] = sweep
 
     # ---- CPU baseline: the oracle on a bounded sample of the same linears ----
     if not args.no_cpu_baseline:

@@ -135,6 +135,37 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
 HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
                              int B, int reps, hetegen_bw* out);
 
+/* ---- Alpha benchmark (Sec. 4.4, Eq. 10-12) ----
+ * The closed form assumes speeds proportional to bytes; measured CPU and transfer
+ * times are not (contention for host memory, per-call overheads).  The alpha
+ * benchmark varies the CPU fraction over [alpha0 - gamma, alpha0 + gamma] in steps
+ * of lambda, measures at each point the CPU-share time and the GPU-side time
+ * (chunk transfers plus GEMV launches, Eq. 2's T_COM + T_GPU) of one heterogeneous
+ * linear, fits least-squares polynomials F_CPU and F_COM of the given degree and
+ * returns the CPU fraction where they meet.  When the fitted curves do not cross
+ * inside the bracket, the bracket point with the smallest max(F_CPU, F_COM) is
+ * returned and *crossed is 0. */
+
+/* Fit-and-solve on given samples (pure host arithmetic): alphas[n], t_cpu[n],
+ * t_com[n]; n >= degree + 1, degree in [1, 3], lo < hi. */
+HETEGEN_API hetegen_status hetegen_alpha_fit(const double* alphas, const double* t_cpu, const double* t_com, int n,
+                                             int degree, double lo, double hi, double* alpha_out, int* crossed);
+
+/* The CPU fraction in [lo, hi] minimising a least-squares polynomial of the given
+ * degree fitted to measured times (alphas[n], t[n]); a grid of 10^4 intervals.  Used
+ * by the step-level benchmark's wall-time objective. */
+HETEGEN_API hetegen_status hetegen_alpha_minimize(const double* alphas, const double* t, int n, int degree, double lo,
+                                                  double hi, double* alpha_out);
+
+/* Measure and solve for one linear (arguments as in hetegen_linear, GPU rows always
+ * streamed from W_host; y_dev receives the last run's output).  reps runs per point,
+ * medians are fitted.  Bracket ends are clamped to [0, 1]. */
+HETEGEN_API hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void* x_dev, int B, int K, const void* W_host,
+                                                   int N, hetegen_dtype dtype, const void* bias_host,
+                                                   const void* bias_dev, void* y_dev, double alpha0, double gamma,
+                                                   double lambda, int degree, int reps, void* stream,
+                                                   double* alpha_out, int* crossed);
+
 /* ---- Decode step over a stack of decoder layers (Sec. 4.2: heterogeneous
  * linears, every other module on the GPU) ----
  *
@@ -189,6 +220,30 @@ HETEGEN_API hetegen_status hetegen_model_set_exec(hetegen_model* model, int mode
 
 /* Mode the last hetegen_decode_step on the model used (HETEGEN_EXEC_*), or -1. */
 HETEGEN_API int hetegen_model_last_exec(const hetegen_model* model);
+
+/* Alpha benchmark at the granularity of the decode step (Sec. 4.4 applied to the
+ * chain of modules).  The call shifts the CPU fraction of every streamed linear by
+ * a common offset delta in [-gamma, gamma] (steps of lambda; each fraction clamped
+ * to [0, 1]) and times steps on x_dev -> out_dev at every point.
+ *   HETEGEN_BENCH_CROSSING: the paper's objective on step totals: fits F_CPU(delta)
+ *     (CPU-share time) and F_COM(delta) (transfers plus GEMVs) from profiled steps
+ *     and solves for their crossing (as hetegen_alpha_fit);
+ *   HETEGEN_BENCH_WALL: fits the steps' wall time and takes its minimiser (as
+ *     hetegen_alpha_minimize).  Within a step the ring lets transfers run ahead
+ *     across linears and the hand-offs and host-memory contention are not in either
+ *     summed time, so the wall-time objective is the one that tracks latency.
+ * reps timed steps per point (plus one warm-up).  The model keeps the refined
+ * fractions; *delta_out receives the offset; *crossed is set for the crossing
+ * objective.  Resident linears are unchanged. */
+#define HETEGEN_BENCH_CROSSING 0
+#define HETEGEN_BENCH_WALL 1
+HETEGEN_API hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, hetegen_model* model, const void* x_dev,
+                                                         void* out_dev, int B, double gamma, double lambda,
+                                                         int degree, int reps, int objective, void* stream,
+                                                         double* delta_out, int* crossed);
+
+/* Current CPU fraction of every linear (4L entries). */
+HETEGEN_API hetegen_status hetegen_model_get_alpha(const hetegen_model* model, double* alpha_out);
 
 /* Optional trace of every linear's input and output (model dtype), for
  * teacher-forced checks.  Linear i writes its input [B, K_i] and then its output

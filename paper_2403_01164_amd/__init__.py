@@ -24,10 +24,11 @@ F16, BF16, F32 = 0, 1, 2
 OK, ERR_INVALID_ARG, ERR_NOT_PINNED, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP = range(6)
 PLAN_APPROX = 1
 EXEC_AUTO, EXEC_PERSISTENT, EXEC_GRAPH, EXEC_EAGER = 0, 1, 2, 3
+BENCH_CROSSING, BENCH_WALL = 0, 1
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "NOT_PINNED", 3: "UNSUPPORTED", 4: "OOM", 5: "HIP"}
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libhetegen.so is not built: run `python -m paper_2403_01164_amd.build` "
+    raise ImportError("libhetegen.so is not built: run `python paper_2403_01164_amd/build.py` "
                       "(or __graft_entry__.build())")
 
 
@@ -65,10 +66,18 @@ _SIGS = {
     "hetegen_linear": ([_vp, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _d, _vp, _i, _vp], _i),
     "hetegen_layer_plan": ([ctypes.POINTER(Shape), _i, ctypes.POINTER(Bw), _i, _i, ctypes.POINTER(_d)], _i),
     "hetegen_probe": ([_vp, _vp, _i, _i, _i, _i, _i, ctypes.POINTER(Bw)], _i),
+    "hetegen_alpha_fit": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d,
+                           ctypes.POINTER(_d), ctypes.POINTER(_i)], _i),
+    "hetegen_alpha_benchmark": ([_vp, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _d, _d, _d, _i, _i, _vp,
+                                 ctypes.POINTER(_d), ctypes.POINTER(_i)], _i),
     "hetegen_model_create": ([_vp, _i, _i, _i, _i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_d),
                               ctypes.POINTER(_i), _i, ctypes.POINTER(_vp)], _i),
     "hetegen_model_set_alpha": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_set_exec": ([_vp, _i, ctypes.c_uint32], _i),
+    "hetegen_model_alpha_benchmark": ([_vp, _vp, _vp, _vp, _i, _d, _d, _i, _i, _i, _vp, ctypes.POINTER(_d),
+                                       ctypes.POINTER(_i)], _i),
+    "hetegen_alpha_minimize": ([ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d, ctypes.POINTER(_d)], _i),
+    "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_last_exec": ([_vp], _i),
     "hetegen_decode_step": ([_vp, _vp, _vp, _vp, _i, _vp], _i),
     "hetegen_model_trace_bytes": ([_vp, _i], _sz),
@@ -154,6 +163,28 @@ def hetegen_probe(ctx, W_host, N, K, dtype, B=1, reps=3):
     return {"cpu_Bps": bw.cpu_Bps, "h2d_Bps": bw.h2d_Bps, "hbm_gemv_Bps": bw.hbm_gemv_Bps, "pin_Bps": bw.pin_Bps}
 
 
+def hetegen_alpha_fit(alphas, t_cpu, t_com, degree, lo, hi):
+    """Refined CPU fraction from samples; returns (alpha, crossed)."""
+    n = len(alphas)
+    arr = lambda v: (_d * n)(*[float(x) for x in v])
+    out, crossed = _d(), _i()
+    rc = _lib.hetegen_alpha_fit(arr(alphas), arr(t_cpu), arr(t_com), n, degree, float(lo), float(hi),
+                                ctypes.byref(out), ctypes.byref(crossed))
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_alpha_fit")
+    return out.value, bool(crossed.value)
+
+
+def hetegen_alpha_benchmark(ctx, x_dev, B, K, W_host, N, dtype, bias_host, bias_dev, y_dev, alpha0, gamma=0.05,
+                            lam=0.01, degree=2, reps=2, stream=0):
+    """Measured refinement of one linear's CPU fraction; returns (alpha, crossed)."""
+    out, crossed = _d(), _i()
+    _check(_lib.hetegen_alpha_benchmark(ctx, x_dev, B, K, W_host, N, dtype, bias_host or None, bias_dev or None, y_dev,
+                                        float(alpha0), float(gamma), float(lam), degree, reps, stream or None,
+                                        ctypes.byref(out), ctypes.byref(crossed)), ctx)
+    return out.value, bool(crossed.value)
+
+
 def hetegen_model_create(ctx, L, H, F, dtype, W_host, bias_host, alpha, resident, max_batch=1):
     n = 4 * L
     W = (_vp * n)(*W_host)
@@ -170,6 +201,33 @@ def hetegen_model_set_alpha(model, alpha):
     rc = _lib.hetegen_model_set_alpha(model, a)
     if rc != OK:
         raise HetegenError(rc, "hetegen_model_set_alpha")
+
+
+def hetegen_model_alpha_benchmark(ctx, model, x_dev, out_dev, B, gamma=0.05, lam=0.01, degree=2, reps=1,
+                                  objective=BENCH_WALL, stream=0):
+    """Step-level refinement; returns (delta, crossed).  The model keeps the refined fractions."""
+    d, crossed = _d(), _i()
+    _check(_lib.hetegen_model_alpha_benchmark(ctx, model, x_dev, out_dev, B, float(gamma), float(lam), degree, reps,
+                                              objective, stream or None, ctypes.byref(d), ctypes.byref(crossed)), ctx)
+    return d.value, bool(crossed.value)
+
+
+def hetegen_alpha_minimize(alphas, t, degree, lo, hi):
+    n = len(alphas)
+    arr = lambda v: (_d * n)(*[float(x) for x in v])
+    out = _d()
+    rc = _lib.hetegen_alpha_minimize(arr(alphas), arr(t), n, degree, float(lo), float(hi), ctypes.byref(out))
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_alpha_minimize")
+    return out.value
+
+
+def hetegen_model_get_alpha(model, n):
+    out = (_d * n)()
+    rc = _lib.hetegen_model_get_alpha(model, out)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_model_get_alpha")
+    return [out[i] for i in range(n)]
 
 
 def hetegen_model_set_exec(model, mode, barrier_spin_limit=0):

@@ -1,6 +1,8 @@
 """Build libhetegen.so in-tree: hipcc for the gfx950 kernels, g++ for the host runtime.
 
-    python -m paper_2403_01164_amd.build
+    python paper_2403_01164_amd/build.py      (or __graft_entry__.build())
+
+Run as a script: importing the package requires the library this builds.
 """
 import os
 import subprocess

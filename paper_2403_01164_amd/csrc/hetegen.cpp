@@ -604,6 +604,194 @@ hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n, const hete
   return HETEGEN_OK;
 }
 
+}  // extern "C"
+
+// ---- alpha benchmark: least-squares polynomial fit and crossing ----
+namespace {
+
+// Coefficients c[0..d] of sum_j c[j] s^j fitted to (s_i, t_i), normal equations with
+// partial pivoting; s is the centred and scaled ratio, so the system stays well
+// conditioned.
+bool lsq_poly(const std::vector<double>& s, const double* t, int d, double* c) {
+  double A[4][5] = {};
+  for (size_t i = 0; i < s.size(); ++i) {
+    double p[7];
+    p[0] = 1.0;
+    for (int j = 1; j <= 2 * d; ++j) p[j] = p[j - 1] * s[i];
+    for (int r = 0; r <= d; ++r) {
+      for (int q = 0; q <= d; ++q) A[r][q] += p[r + q];
+      A[r][d + 1] += p[r] * t[i];
+    }
+  }
+  for (int col = 0; col <= d; ++col) {
+    int piv = col;
+    for (int r = col + 1; r <= d; ++r)
+      if (fabs(A[r][col]) > fabs(A[piv][col])) piv = r;
+    if (fabs(A[piv][col]) < 1e-300) return false;
+    if (piv != col)
+      for (int q = 0; q <= d + 1; ++q) std::swap(A[piv][q], A[col][q]);
+    for (int r = 0; r <= d; ++r) {
+      if (r == col) continue;
+      const double f = A[r][col] / A[col][col];
+      for (int q = col; q <= d + 1; ++q) A[r][q] -= f * A[col][q];
+    }
+  }
+  for (int r = 0; r <= d; ++r) c[r] = A[r][d + 1] / A[r][r];
+  return true;
+}
+
+double poly(const double* c, int d, double s) {
+  double v = c[d];
+  for (int j = d - 1; j >= 0; --j) v = v * s + c[j];
+  return v;
+}
+
+}  // namespace
+
+extern "C" hetegen_status hetegen_alpha_fit(const double* alphas, const double* t_cpu, const double* t_com, int n,
+                                            int degree, double lo, double hi, double* alpha_out, int* crossed) {
+  if (!alphas || !t_cpu || !t_com || !alpha_out || degree < 1 || degree > 3 || n < degree + 1 || !(lo < hi))
+    return HETEGEN_ERR_INVALID_ARG;
+  double amin = alphas[0], amax = alphas[0];
+  for (int i = 0; i < n; ++i) {
+    if (!std::isfinite(alphas[i]) || !std::isfinite(t_cpu[i]) || !std::isfinite(t_com[i]))
+      return HETEGEN_ERR_INVALID_ARG;
+    amin = std::min(amin, alphas[i]);
+    amax = std::max(amax, alphas[i]);
+  }
+  const double ctr = 0.5 * (amin + amax), half = amax > amin ? 0.5 * (amax - amin) : 1.0;
+  std::vector<double> sv(n);
+  for (int i = 0; i < n; ++i) sv[i] = (alphas[i] - ctr) / half;
+  double cc[4], cg[4];
+  if (!lsq_poly(sv, t_cpu, degree, cc) || !lsq_poly(sv, t_com, degree, cg)) return HETEGEN_ERR_INVALID_ARG;
+  auto fc = [&](double a) { return poly(cc, degree, (a - ctr) / half); };
+  auto fg = [&](double a) { return poly(cg, degree, (a - ctr) / half); };
+  auto g = [&](double a) { return fc(a) - fg(a); };
+  // sign changes of F_CPU - F_COM on a fine grid, each refined by bisection
+  const int M = 2000;
+  double best = 0, best_t = INFINITY;
+  bool found = false;
+  double a0 = lo, g0 = g(lo);
+  for (int i = 1; i <= M; ++i) {
+    const double a1 = lo + (hi - lo) * i / M, g1 = g(a1);
+    if (g0 == 0 || (g0 < 0) != (g1 < 0)) {
+      double l = a0, r = a1, gl = g0;
+      if (g0 == 0) r = a0;
+      for (int it = 0; it < 200 && r - l > 0; ++it) {
+        const double mid = 0.5 * (l + r), gm = g(mid);
+        if (mid <= l || mid >= r) break;
+        if ((gm < 0) == (gl < 0)) {
+          l = mid;
+          gl = gm;
+        } else {
+          r = mid;
+        }
+      }
+      const double root = 0.5 * (l + r);
+      if (fc(root) < best_t) {
+        best_t = fc(root);
+        best = root;
+        found = true;
+      }
+    }
+    a0 = a1;
+    g0 = g1;
+  }
+  if (!found) {  // no crossing: bracket point with the smallest max(F_CPU, F_COM)
+    const int G = 10000;
+    for (int i = 0; i <= G; ++i) {
+      const double a = lo + (hi - lo) * i / G, m = std::max(fc(a), fg(a));
+      if (m < best_t) {
+        best_t = m;
+        best = a;
+      }
+    }
+  }
+  *alpha_out = std::min(hi, std::max(lo, best));
+  if (crossed) *crossed = found ? 1 : 0;
+  return HETEGEN_OK;
+}
+
+extern "C" hetegen_status hetegen_alpha_minimize(const double* alphas, const double* t, int n, int degree, double lo,
+                                                 double hi, double* alpha_out) {
+  if (!alphas || !t || !alpha_out || degree < 1 || degree > 3 || n < degree + 1 || !(lo < hi))
+    return HETEGEN_ERR_INVALID_ARG;
+  double amin = alphas[0], amax = alphas[0];
+  for (int i = 0; i < n; ++i) {
+    if (!std::isfinite(alphas[i]) || !std::isfinite(t[i])) return HETEGEN_ERR_INVALID_ARG;
+    amin = std::min(amin, alphas[i]);
+    amax = std::max(amax, alphas[i]);
+  }
+  const double ctr = 0.5 * (amin + amax), half = amax > amin ? 0.5 * (amax - amin) : 1.0;
+  std::vector<double> sv(n);
+  for (int i = 0; i < n; ++i) sv[i] = (alphas[i] - ctr) / half;
+  double c[4];
+  if (!lsq_poly(sv, t, degree, c)) return HETEGEN_ERR_INVALID_ARG;
+  const int G = 10000;
+  double best = lo, best_t = INFINITY;
+  for (int i = 0; i <= G; ++i) {
+    const double a = lo + (hi - lo) * i / G, v = poly(c, degree, (a - ctr) / half);
+    if (v < best_t) {
+      best_t = v;
+      best = a;
+    }
+  }
+  *alpha_out = best;
+  return HETEGEN_OK;
+}
+
+extern "C" hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void* x_dev, int B, int K,
+                                                  const void* W_host, int N, hetegen_dtype dtype,
+                                                  const void* bias_host, const void* bias_dev, void* y_dev,
+                                                  double alpha0, double gamma, double lambda, int degree, int reps,
+                                                  void* stream, double* alpha_out, int* crossed) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  if (!alpha_out || !(gamma >= 0) || !(lambda > 0) || reps < 1 || !(alpha0 >= 0 && alpha0 <= 1) || degree < 1 ||
+      degree > 3)
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_alpha_benchmark: bad arguments");
+  const double lo = std::max(0.0, alpha0 - gamma), hi = std::min(1.0, alpha0 + gamma);
+  std::vector<double> as, tc, tg;
+  for (int i = 0;; ++i) {
+    const double a = lo + i * lambda;
+    if (a > hi + 1e-9) break;
+    as.push_back(std::min(a, hi));
+  }
+  if ((int)as.size() < degree + 1 || !(lo < hi))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bracket holds %zu points; degree %d needs %d", as.size(), degree,
+                degree + 1);
+  const bool was = ctx->profiling;
+  ctx->profiling = true;
+  TRY(flush_profile(ctx));
+  const hetegen_profile saved = ctx->prof;
+  hetegen_status st = HETEGEN_OK;
+  for (double a : as) {
+    std::vector<double> c, g;
+    for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
+      ctx->prof = hetegen_profile{};
+      st = hetegen_linear(ctx, x_dev, B, K, W_host, nullptr, N, dtype, bias_host, bias_dev, a, y_dev, HETEGEN_F32,
+                          stream);
+      if (st == HETEGEN_OK && r > 0) {  // the first run of each point warms it up
+        c.push_back(ctx->prof.cpu_ms);
+        g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
+      }
+    }
+    if (st != HETEGEN_OK) break;
+    std::sort(c.begin(), c.end());
+    std::sort(g.begin(), g.end());
+    tc.push_back(c[c.size() / 2]);
+    tg.push_back(g[g.size() / 2]);
+  }
+  ctx->prof = saved;
+  ctx->profiling = was;
+  if (st != HETEGEN_OK) return st;
+  hetegen_status fs = hetegen_alpha_fit(as.data(), tc.data(), tg.data(), (int)as.size(), degree, lo, hi, alpha_out,
+                                        crossed);
+  if (fs != HETEGEN_OK) return fail(ctx, fs, "alpha fit failed");
+  return HETEGEN_OK;
+}
+
+extern "C" {
+
 hetegen_status hetegen_set_profiling(hetegen_ctx* ctx, int on) {
   if (!ctx) return HETEGEN_ERR_INVALID_ARG;
   ctx->profiling = on != 0;
@@ -1031,6 +1219,92 @@ hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {
     l.n_cpu = split_cpu_rows(l.N, l.alpha);
     l.n_gpu = l.N - l.n_cpu;
   }
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_model_get_alpha(const hetegen_model* m, double* alpha_out) {
+  if (!m || !alpha_out) return HETEGEN_ERR_INVALID_ARG;
+  for (size_t i = 0; i < m->lin.size(); ++i) alpha_out[i] = m->lin[i].alpha;
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev,
+                                             int B, double gamma, double lambda, int degree, int reps, int objective,
+                                             void* stream, double* delta_out, int* crossed) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  if (!m || !delta_out || !(gamma > 0) || !(lambda > 0) || reps < 1 || degree < 1 || degree > 3 ||
+      (objective != HETEGEN_BENCH_CROSSING && objective != HETEGEN_BENCH_WALL))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_alpha_benchmark: bad arguments");
+  std::vector<double> base(m->lin.size());
+  bool any = false;
+  for (size_t i = 0; i < m->lin.size(); ++i) {
+    base[i] = m->lin[i].alpha;
+    any = any || !m->lin[i].resident;
+  }
+  if (!any) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "no streamed linear to balance");
+  auto apply = [&](double d) {
+    std::vector<double> a(base);
+    for (size_t i = 0; i < a.size(); ++i)
+      if (!m->lin[i].resident) a[i] = std::min(1.0, std::max(0.0, base[i] + d));
+    return hetegen_model_set_alpha(m, a.data());
+  };
+  std::vector<double> ds, tc, tg, tw;
+  for (int i = 0;; ++i) {
+    const double d = -gamma + i * lambda;
+    if (d > gamma + 1e-9) break;
+    ds.push_back(std::min(d, gamma));
+  }
+  if ((int)ds.size() < degree + 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "too few points in the bracket");
+  const bool was = ctx->profiling;
+  ctx->profiling = objective == HETEGEN_BENCH_CROSSING;
+  TRY(flush_profile(ctx));
+  const hetegen_profile saved = ctx->prof;
+  hetegen_status st = HETEGEN_OK;
+  auto med = [](std::vector<double> v) {
+    std::sort(v.begin(), v.end());
+    return v[v.size() / 2];
+  };
+  for (double d : ds) {
+    TRY(apply(d));
+    std::vector<double> c, g, w;
+    for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
+      ctx->prof = hetegen_profile{};
+      auto t0 = Clock::now();
+      st = hetegen_decode_step(ctx, m, x_dev, out_dev, B, stream);
+      if (st == HETEGEN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+        st = fail(ctx, HETEGEN_ERR_HIP, "hipStreamSynchronize failed");
+      const double wall = ms_since(t0);
+      if (st == HETEGEN_OK) st = flush_profile(ctx);
+      if (st == HETEGEN_OK && r > 0) {
+        c.push_back(ctx->prof.cpu_ms);
+        g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
+        w.push_back(wall);
+      }
+    }
+    if (st != HETEGEN_OK) break;
+    tc.push_back(med(c));
+    tg.push_back(med(g));
+    tw.push_back(med(w));
+  }
+  ctx->prof = saved;
+  ctx->profiling = was;
+  if (st != HETEGEN_OK) {
+    (void)hetegen_model_set_alpha(m, base.data());
+    return st;
+  }
+  double d_best = 0;
+  int cr = 0;
+  hetegen_status fs =
+      objective == HETEGEN_BENCH_CROSSING
+          ? hetegen_alpha_fit(ds.data(), tc.data(), tg.data(), (int)ds.size(), degree, -gamma, gamma, &d_best, &cr)
+          : hetegen_alpha_minimize(ds.data(), tw.data(), (int)ds.size(), degree, -gamma, gamma, &d_best);
+  if (fs != HETEGEN_OK) {
+    (void)hetegen_model_set_alpha(m, base.data());
+    return fail(ctx, fs, "alpha fit failed");
+  }
+  TRY(apply(d_best));
+  *delta_out = d_best;
+  if (crossed) *crossed = cr;
   return HETEGEN_OK;
 }
 

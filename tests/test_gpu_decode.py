@@ -287,3 +287,24 @@ def test_forced_modes_rejected_for_split_models(ctx):
         hg.hetegen_model_set_exec(m.m, hg.EXEC_EAGER)
     finally:
         m.free()
+
+
+def test_step_alpha_benchmark_refines_and_keeps_parity(ctx):
+    dtype, L, H, F = synth.F16, 2, 1024, 4096
+    m = Model(ctx, L, H, F, dtype, [0.5] * 8, 0, max_batch=1)
+    try:
+        x = synth.normal((1, H), dtype, 0, synth.act_id(3))
+        xd = torch_dev_from_np(x)
+        od = torch.empty((1, H), dtype=torch.int16, device="cuda")
+        for objective in (hg.BENCH_CROSSING, hg.BENCH_WALL):
+            hg.hetegen_model_set_alpha(m.m, [0.5] * 8)
+            d, crossed = hg.hetegen_model_alpha_benchmark(ctx, m.m, xd.data_ptr(), od.data_ptr(), 1, 0.1, 0.05, 2, 1,
+                                                          objective, torch.cuda.current_stream().cuda_stream)
+            assert -0.1 - 1e-9 <= d <= 0.1 + 1e-9
+            a = hg.hetegen_model_get_alpha(m.m, 4 * L)
+            assert all(abs(v - (0.5 + d)) < 1e-12 for v in a)
+        out, tr = m.step(x, trace=True)
+        last, _ = m.check_teacher_forced(x, tr)
+        assert np.array_equal(out, last)
+    finally:
+        m.free()

@@ -248,3 +248,21 @@ def test_full_size_opt_linears(ctx, N, K, dtype, alpha, resident, B):
         assert rel_err(y, p.ref()) <= TOL
     finally:
         p.free()
+
+
+def test_alpha_benchmark_runs_in_bracket_and_keeps_parity(ctx):
+    # OPT-13B fc1 shape; the closed-form start is the probe's Eq. 5 CPU fraction
+    p = Problem(ctx, 1, 5120, 20480, synth.F16, seed=11)
+    try:
+        bw = hg.hetegen_probe(ctx, p.W.ptr, p.N, p.K, p.dtype, 1, 2)
+        a0 = hg.hetegen_layer_plan([(p.N, p.K, p.dtype, 0)], [(bw["cpu_Bps"], bw["h2d_Bps"], bw["hbm_gemv_Bps"], 0.0)])[0]
+        y = torch.empty((1, p.N), dtype=torch.float32, device="cuda")
+        a, crossed = hg.hetegen_alpha_benchmark(ctx, p.x_dev.data_ptr(), 1, p.K, p.W.ptr, p.N, p.dtype, p.bias.ptr,
+                                                p.b_dev.data_ptr(), y.data_ptr(), a0, 0.05, 0.01, 2, 1,
+                                                torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        assert max(0.0, a0 - 0.05) - 1e-9 <= a <= min(1.0, a0 + 0.05) + 1e-9
+        assert rel_err(y.cpu().numpy(), p.ref()) <= TOL          # the last measured run's output
+        assert rel_err(p.run(a, False), p.ref()) <= TOL
+    finally:
+        p.free()
