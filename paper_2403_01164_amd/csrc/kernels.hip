@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace hg {
@@ -36,6 +38,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kX1MaxRows = 64;  // rows per wavefront the x-direct GEMV keeps bias/residual for
 constexpr float kLnEps = 1e-5f;
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
@@ -409,22 +412,29 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
 // ---------------------------------------------------------------------------
 template <class T, int U>
 __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
+  // per wavefront: bias and residual of its rows (row j of the wave: local row wave + j*kWaves)
+  __shared__ float sbias[kWaves][kX1MaxRows], sres[kWaves][kX1MaxRows];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int K = p.K, k8 = K >> 3, rpw = p.rpw;
   const int row_begin = blockIdx.x * rpw;
   const int nrows = min(rpw, p.rows - row_begin);  // >= 1: the grid covers rows exactly
   constexpr int SEG = 64 * U;
   const int nseg = (k8 + SEG - 1) / SEG;
-  const int my_rg = nrows > wave ? (nrows - wave + kWaves - 1) / kWaves : 0;
+  const int my_rg = nrows > wave ? (nrows - wave + kWaves - 1) / kWaves : 0;  // <= kX1MaxRows (launcher)
   const int ntask = my_rg * nseg;
   const uint16_t* W = (const uint16_t*)p.W;
   const uint4* x = (const uint4*)p.x;
   const uint16_t* bias = (const uint16_t*)p.bias;
-  const uint16_t* res = p.epi == EPI_RESID ? (const uint16_t*)p.resid : bias;
-  const bool has_bias = bias != nullptr;
+  const uint16_t* res = (const uint16_t*)p.resid;
+  // bias and residual first: waiting for them later does not wait for the weights
+  float bj = 0.f, rj = 0.f;
+  if (lane < my_rg) {
+    const int row = row_begin + wave + lane * kWaves;
+    if (bias) bj = T::to_f32(gmem(bias)[row]);
+    if (p.epi == EPI_RESID) rj = T::to_f32(gmem(res)[row]);
+  }
   struct Buf {
     uint4 w[U], x[U];
-    uint16_t b, r;
   };
   auto load = [&](int t, Buf& f) {
     const int j = t / nseg, seg = t - j * nseg;
@@ -435,10 +445,13 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
     for (int u = 0; u < U; ++u) f.w[u] = load_stream(wr + min(c0 + 64 * u, k8 - 1));
 #pragma unroll
     for (int u = 0; u < U; ++u) f.x[u] = load_g16(x + min(c0 + 64 * u, k8 - 1));
-    // the row's bias and residual travel with every task (no dependent load at the row end)
-    f.b = has_bias ? gmem(bias)[row] : (uint16_t)0;
-    f.r = res ? gmem(res)[row] : (uint16_t)0;
   };
+  Buf fa, fb;
+  if (ntask > 0) load(0, fa);
+  if (lane < my_rg) {
+    sbias[wave][lane] = bj;
+    sres[wave][lane] = rj;
+  }
   float acc = 0.f;
   auto compute = [&](int t, const Buf& f) {
     const int j = t / nseg, seg = t - j * nseg;
@@ -451,13 +464,10 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
       acc = 0.f;
       if (lane == 0) {
         const int row = row_begin + wave + j * kWaves;
-        const float v = apply_epi(s + (has_bias ? T::to_f32(f.b) : 0.f), p.epi, T::to_f32(f.r));
-        store_y<T>(p.y, row, p.y_f32, v);
+        store_y<T>(p.y, row, p.y_f32, apply_epi(s + sbias[wave][j], p.epi, sres[wave][j]));
       }
     }
   };
-  Buf fa, fb;
-  if (ntask > 0) load(0, fa);
   int t = 0;
   for (; t + 2 < ntask; t += 2) {
     load(t + 1, fb);
@@ -730,7 +740,7 @@ hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
   if (B == 1 && !p.ln) {
     constexpr int U1 = 4;
     const long long units = (p.rows + kWaves - 1) / kWaves;
-    const long long per = (units + cap - 1) / cap;
+    const long long per = std::min<long long>((units + cap - 1) / cap, kX1MaxRows);
     p.rpw = (int)(per * kWaves);
     const int grid = (int)((p.rows + p.rpw - 1) / p.rpw);
     hipLaunchKernelGGL((gemv_x1_kernel<T, U1>), dim3(grid), dim3(kThreads), 0, s, p);
