@@ -77,8 +77,11 @@ def main():
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N decoder layers (0: all); reported in config")
-    ap.add_argument("--placement", choices=("all", "half", "none"), default=None,
-                    help="HBM-resident layers: all, the first half, or none (default per model)")
+    ap.add_argument("--placement", choices=("all", "half", "none", "sched"), default=None,
+                    help="HBM-resident modules: all, the first half of the layers, none, or the module "
+                         "scheduler's choice under --hbm-budget (Sec. 4.5) (default per model)")
+    ap.add_argument("--hbm-budget", type=float, default=None,
+                    help="GB of HBM for resident weights with --placement sched (default: half the weights)")
     ap.add_argument("--alpha", type=float, default=None,
                     help="fixed CPU fraction for every streamed linear (default: the planner's)")
     ap.add_argument("--alpha-sweep", default=None,
@@ -142,6 +145,7 @@ def main():
     # ---- planner: speeds per shape from the probe (streamed linears only) ----
     bws = [(1.0, 1.0, 1.0, 0.0)] * (4 * L)
     probe = {}
+    schedule = None
     if streamed:
         last = 4 * (L - 1)
         for m in range(4):
@@ -153,13 +157,28 @@ def main():
                 (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9, time.time() - t0))
         bws = [tuple(probe[NAMES[i % 4]][f] for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps", "pin_Bps"))
                for i in range(4 * L)]
+    if placement == "sched":
+        # module scheduler (Sec. 4.5, Eq. 13): each module's heterogeneous time at its
+        # planned split, predicted from the probed CPU speed, against its HBM bytes
+        a_all = hg.hetegen_layer_plan([(n, k, dt, 0) for n, k in shp], bws)
+        t_het = [a_all[i] * n * k * 2 / bws[i][0] for i, (n, k) in enumerate(shp)]
+        mem = [float(n * k * 2) for n, k in shp]
+        budget = args.hbm_budget * 1e9 if args.hbm_budget is not None else sum(mem) / 2
+        resident, used = hg.hetegen_module_schedule(t_het, mem, [i // 4 for i in range(4 * L)], budget)
+        streamed = [i for i in range(4 * L) if not resident[i]]
+        schedule = {"hbm_budget_GB": round(budget / 1e9, 3), "resident_GB": round(used / 1e9, 3),
+                    "resident_modules": sum(resident),
+                    "resident_by_linear": {NAMES[m]: sum(resident[m::4]) for m in range(4)},
+                    "gain_s_per_GB": {NAMES[m]: round(t_het[4 * (L - 1) + m] / mem[4 * (L - 1) + m] * 1e9, 5)
+                                      for m in range(4)}}
+        log("module scheduler: %s" % json.dumps(schedule))
     alpha = hg.hetegen_layer_plan([(n, k, dt, resident[i]) for i, (n, k) in enumerate(shp)], bws)
     if args.alpha is not None:
         alpha = [0.0 if resident[i] else args.alpha for i in range(4 * L)]
     alpha_closed = list(alpha)
     t0 = time.time()
     model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, resident, max(B, 1))
-    log("model ready in %.1f s (resident layers %d of %d)" % (time.time() - t0, res_layers, L))
+    log("model ready in %.1f s (resident modules %d of %d)" % (time.time() - t0, sum(resident), 4 * L))
     if args.exec != "auto" and not streamed:
         hg.hetegen_model_set_exec(model, {"persistent": hg.EXEC_PERSISTENT, "graph": hg.EXEC_GRAPH,
                                           "eager": hg.EXEC_EAGER}[args.exec])
@@ -181,7 +200,9 @@ def main():
                                                           0.08, 0.02, 2, 2, hg.BENCH_WALL, sptr)
         alpha = hg.hetegen_model_get_alpha(model, 4 * L)
         refined = {"delta": round(delta, 4), "crossed": crossed,
-                   "alpha_cpu_by_linear": {NAMES[m]: round(alpha[streamed[0] + m], 4) for m in range(4)}}
+                   "alpha_cpu_by_linear": {NAMES[m]: round(alpha[i], 4) for m in range(4)
+                                           for i in [next((j for j in streamed if j % 4 == m), None)]
+                                           if i is not None}}
         log("step-level alpha benchmark (wall-time objective): delta %+.4f in %.1f s" % (delta, time.time() - t0))
 
     for t in range(args.warmup):
@@ -204,6 +225,9 @@ def main():
         desc = "all linears HBM-resident (alpha=0), GEMV-only"
     elif placement == "half":
         desc = "layers 0-%d HBM-resident, %d-%d streamed from pinned host" % (res_layers - 1, res_layers, L - 1)
+    elif placement == "sched":
+        desc = "module scheduler: %d of %d linears HBM-resident (%.2f of %.2f GB budget), rest streamed from " \
+               "pinned host" % (sum(resident), 4 * L, schedule["resident_GB"], schedule["hbm_budget_GB"])
     else:
         desc = "all linears in pinned host memory, streamed + CPU share"
     if placement != "all":
@@ -226,8 +250,11 @@ def main():
                                (args.model.upper(), L, desc, B) +
                                ("" if L == L_full else " (first %d of the model's %d layers)" % (L, L_full)),
                    "layers": L, "hidden": H, "ffn": F, "batch": B, "weight_bytes_per_step": wbytes,
-                   "resident_layers": res_layers, "parallelism": "single GPU"},
+                   "resident_layers": res_layers, "resident_modules": sum(resident),
+                   "parallelism": "single GPU"},
     }
+    if schedule:
+        result["config"]["schedule"] = schedule
 
     exec_mode = {1: "persistent", 2: "graph", 3: "eager"}.get(hg.hetegen_model_last_exec(model), "?")
     result["config"]["exec"] = exec_mode
@@ -272,7 +299,8 @@ def main():
         hg.hetegen_set_profiling(ctx, 0)
         wall_ms = prof["wall_ms"]
         result["hetero"] = {
-            "alpha_cpu_by_linear": {NAMES[m]: round(alpha[streamed[0] + m], 4) for m in range(4)},
+            "alpha_cpu_by_linear": {NAMES[m]: round(alpha[i], 4) for m in range(4)
+                                    for i in [next((j for j in streamed if j % 4 == m), None)] if i is not None},
             "probe_GBps": {k: {f: round(v[f] / 1e9, 2) for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps")}
                            for k, v in probe.items()},
             "streamed_bytes_per_step": sb, "h2d_bytes_per_step": h2d_b, "cpu_bytes_per_step": cpu_b,

@@ -166,6 +166,21 @@ HETEGEN_API hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void*
                                                    double lambda, int degree, int reps, void* stream,
                                                    double* alpha_out, int* crossed);
 
+/* ---- Heterogeneous module scheduler (Sec. 4.5, Eq. 13) ----
+ * Decides which whole modules become GPU-resident when HBM is left over.  Moving
+ * module i onto the GPU saves its heterogeneous time t_cpu[i] (seconds, the
+ * benchmarked balanced time of Eq. 11) and takes mem[i] bytes of HBM; its gain is
+ * g = t_cpu[i] / mem[i].  Modules are visited round robin over the layers
+ * (layer[i] >= 0, layers in increasing order): every layer's highest-g module,
+ * then every layer's second-highest, and so on, equal gains in index order.  A
+ * visited module becomes resident when it fits in what is left of budget_bytes
+ * (a sum of doubles in visit order, compared with <=); one that does not fit is
+ * skipped and the walk continues.  resident_out[n] receives 1/0; *used_out (may be
+ * NULL) the bytes taken.  t_cpu[i] must be finite and >= 0, mem[i] finite and > 0,
+ * budget_bytes >= 0 (+inf: no limit).  Pure host arithmetic. */
+HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const double* mem, const int* layer, int n,
+                                                   double budget_bytes, int* resident_out, double* used_out);
+
 /* ---- Decode step over a stack of decoder layers (Sec. 4.2: heterogeneous
  * linears, every other module on the GPU) ----
  *

@@ -78,6 +78,8 @@ _SIGS = {
                                        ctypes.POINTER(_i)], _i),
     "hetegen_alpha_minimize": ([ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d, ctypes.POINTER(_d)], _i),
     "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_module_schedule": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_i), _i, _d,
+                                 ctypes.POINTER(_i), ctypes.POINTER(_d)], _i),
     "hetegen_model_last_exec": ([_vp], _i),
     "hetegen_decode_step": ([_vp, _vp, _vp, _vp, _i, _vp], _i),
     "hetegen_model_trace_bytes": ([_vp, _i], _sz),
@@ -210,6 +212,20 @@ def hetegen_model_alpha_benchmark(ctx, model, x_dev, out_dev, B, gamma=0.05, lam
     _check(_lib.hetegen_model_alpha_benchmark(ctx, model, x_dev, out_dev, B, float(gamma), float(lam), degree, reps,
                                               objective, stream or None, ctypes.byref(d), ctypes.byref(crossed)), ctx)
     return d.value, bool(crossed.value)
+
+
+def hetegen_module_schedule(t_cpu, mem, layer, budget):
+    """Resident flag per module (Sec. 4.5, Eq. 13) and the bytes they take."""
+    n = len(t_cpu)
+    res = (_i * max(n, 1))()
+    used = _d()
+    rc = _lib.hetegen_module_schedule((_d * max(n, 1))(*[float(v) for v in t_cpu]),
+                                      (_d * max(n, 1))(*[float(v) for v in mem]),
+                                      (_i * max(n, 1))(*[int(v) for v in layer]), n, float(budget), res,
+                                      ctypes.byref(used))
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_module_schedule")
+    return [res[i] for i in range(n)], used.value
 
 
 def hetegen_alpha_minimize(alphas, t, degree, lo, hi):

@@ -25,6 +25,7 @@
 #include <algorithm>
 #include <chrono>
 #include <deque>
+#include <map>
 #include <string>
 #include <vector>
 
@@ -787,6 +788,42 @@ extern "C" hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void* 
   hetegen_status fs = hetegen_alpha_fit(as.data(), tc.data(), tg.data(), (int)as.size(), degree, lo, hi, alpha_out,
                                         crossed);
   if (fs != HETEGEN_OK) return fail(ctx, fs, "alpha fit failed");
+  return HETEGEN_OK;
+}
+
+// ---- heterogeneous module scheduler (Sec. 4.5, Eq. 13) ----
+extern "C" hetegen_status hetegen_module_schedule(const double* t_cpu, const double* mem, const int* layer, int n,
+                                                  double budget_bytes, int* resident_out, double* used_out) {
+  if (n < 0 || (n > 0 && (!t_cpu || !mem || !layer || !resident_out)) || !(budget_bytes >= 0))
+    return HETEGEN_ERR_INVALID_ARG;
+  std::vector<double> g(n);
+  std::map<int, std::vector<int>> by_layer;  // layers in increasing order
+  for (int i = 0; i < n; ++i) {
+    if (!std::isfinite(t_cpu[i]) || t_cpu[i] < 0 || !std::isfinite(mem[i]) || !(mem[i] > 0) || layer[i] < 0)
+      return HETEGEN_ERR_INVALID_ARG;
+    g[i] = t_cpu[i] / mem[i];
+    by_layer[layer[i]].push_back(i);
+  }
+  // modules of each layer by decreasing gain (stable: index order among equal gains)
+  size_t depth = 0;
+  for (auto& kv : by_layer) {
+    std::stable_sort(kv.second.begin(), kv.second.end(), [&](int a, int b) { return g[a] > g[b]; });
+    depth = std::max(depth, kv.second.size());
+  }
+  double used = 0.0;
+  for (int i = 0; i < n; ++i) resident_out[i] = 0;
+  for (size_t r = 0; r < depth; ++r) {
+    for (const auto& kv : by_layer) {
+      const auto& v = kv.second;
+      if (r >= v.size()) continue;
+      const int i = v[r];
+      if (used + mem[i] <= budget_bytes) {
+        resident_out[i] = 1;
+        used += mem[i];
+      }
+    }
+  }
+  if (used_out) *used_out = used;
   return HETEGEN_OK;
 }
 
