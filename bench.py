@@ -157,11 +157,26 @@ def main():
                 (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9, time.time() - t0))
         bws = [tuple(probe[NAMES[i % 4]][f] for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps", "pin_Bps"))
                for i in range(4 * L)]
+    # fresh input per step, resident in HBM before timing
+    nstep = args.warmup + args.steps
+    xs = torch.empty((nstep, B, H), dtype=torch.int16, device="cuda")
+    for t in range(nstep):
+        xs[t] = torch.from_numpy(synth.normal((B, H), dt, 0, synth.act_id(t)).view(np.int16))
+    out = torch.empty((2, B, H), dtype=torch.int16, device="cuda")
+
     if placement == "sched":
-        # module scheduler (Sec. 4.5, Eq. 13): each module's heterogeneous time at its
-        # planned split, predicted from the probed CPU speed, against its HBM bytes
+        # module scheduler (Sec. 4.5, Eq. 13): each module's benchmarked heterogeneous
+        # time (host critical-path time in steps with every linear heterogeneous at its
+        # planned split) against the HBM bytes of its resident copy
         a_all = hg.hetegen_layer_plan([(n, k, dt, 0) for n, k in shp], bws)
-        t_het = [a_all[i] * n * k * 2 / bws[i][0] for i, (n, k) in enumerate(shp)]
+        mcal = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, a_all, [0] * (4 * L), max(B, 1))
+        t_het = [0.0] * (4 * L)
+        for t in range(3):
+            hg.hetegen_decode_step(ctx, mcal, xs[t % nstep].data_ptr(), out[0].data_ptr(), B, sptr)
+            if t > 0:
+                t_het = [a + v * 1e-3 / 2 for a, v in zip(t_het, hg.hetegen_model_linear_ms(mcal, 4 * L))]
+        torch.cuda.synchronize()
+        hg.hetegen_model_destroy(ctx, mcal)
         mem = [float(n * k * 2) for n, k in shp]
         budget = args.hbm_budget * 1e9 if args.hbm_budget is not None else sum(mem) / 2
         resident, used = hg.hetegen_module_schedule(t_het, mem, [i // 4 for i in range(4 * L)], budget)
@@ -169,8 +184,9 @@ def main():
         schedule = {"hbm_budget_GB": round(budget / 1e9, 3), "resident_GB": round(used / 1e9, 3),
                     "resident_modules": sum(resident),
                     "resident_by_linear": {NAMES[m]: sum(resident[m::4]) for m in range(4)},
-                    "gain_s_per_GB": {NAMES[m]: round(t_het[4 * (L - 1) + m] / mem[4 * (L - 1) + m] * 1e9, 5)
-                                      for m in range(4)}}
+                    "gain_s_per_GB_mean": {NAMES[m]: round(float(np.mean([t_het[i] / mem[i] * 1e9
+                                                                          for i in range(m, 4 * L, 4)])), 5)
+                                           for m in range(4)}}
         log("module scheduler: %s" % json.dumps(schedule))
     alpha = hg.hetegen_layer_plan([(n, k, dt, resident[i]) for i, (n, k) in enumerate(shp)], bws)
     if args.alpha is not None:
@@ -182,13 +198,6 @@ def main():
     if args.exec != "auto" and not streamed:
         hg.hetegen_model_set_exec(model, {"persistent": hg.EXEC_PERSISTENT, "graph": hg.EXEC_GRAPH,
                                           "eager": hg.EXEC_EAGER}[args.exec])
-
-    # fresh input per step, resident in HBM before timing
-    nstep = args.warmup + args.steps
-    xs = torch.empty((nstep, B, H), dtype=torch.int16, device="cuda")
-    for t in range(nstep):
-        xs[t] = torch.from_numpy(synth.normal((B, H), dt, 0, synth.act_id(t)).view(np.int16))
-    out = torch.empty((2, B, H), dtype=torch.int16, device="cuda")
 
     def step(t):
         hg.hetegen_decode_step(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, sptr)

@@ -131,7 +131,7 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
  * distribution law): the CPU share GEMV over all N rows of W_host (alpha = 1), the
  * chunked host-to-device copy of W_host through the staging ring, and the GPU
  * GEMV over the staged chunks; each is the median of `reps` runs in weight bytes
- * per second.  W_host is pinned [N, K]; batch B.  pin_Bps is set to 0. */
+ * per second (the CPU share after one untimed pass).  W_host is pinned [N, K]; batch B.  pin_Bps is set to 0. */
 HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
                              int B, int reps, hetegen_bw* out);
 
@@ -259,6 +259,14 @@ HETEGEN_API hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, heteg
 
 /* Current CPU fraction of every linear (4L entries). */
 HETEGEN_API hetegen_status hetegen_model_get_alpha(const hetegen_model* model, double* alpha_out);
+
+/* Host milliseconds each linear (4L entries) took in the last step that ran linear
+ * by linear (HETEGEN_EXEC_EAGER, or any step with CPU rows or streamed rows): from
+ * the start of its enqueue to the end of its CPU share and the enqueue of its
+ * return, i.e. its share of the calling thread's critical path.  The module
+ * scheduler's benchmarked heterogeneous time (Sec. 4.5) when every linear is
+ * heterogeneous.  Zeros before such a step. */
+HETEGEN_API hetegen_status hetegen_model_linear_ms(const hetegen_model* model, double* ms_out);
 
 /* Optional trace of every linear's input and output (model dtype), for
  * teacher-forced checks.  Linear i writes its input [B, K_i] and then its output

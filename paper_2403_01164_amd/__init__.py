@@ -78,6 +78,7 @@ _SIGS = {
                                        ctypes.POINTER(_i)], _i),
     "hetegen_alpha_minimize": ([ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d, ctypes.POINTER(_d)], _i),
     "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_model_linear_ms": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_module_schedule": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_i), _i, _d,
                                  ctypes.POINTER(_i), ctypes.POINTER(_d)], _i),
     "hetegen_model_last_exec": ([_vp], _i),
@@ -243,6 +244,14 @@ def hetegen_model_get_alpha(model, n):
     rc = _lib.hetegen_model_get_alpha(model, out)
     if rc != OK:
         raise HetegenError(rc, "hetegen_model_get_alpha")
+    return [out[i] for i in range(n)]
+
+
+def hetegen_model_linear_ms(model, n):
+    out = (_d * n)()
+    rc = _lib.hetegen_model_linear_ms(model, out)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_model_linear_ms")
     return [out[i] for i in range(n)]
 
 

@@ -308,3 +308,15 @@ def test_step_alpha_benchmark_refines_and_keeps_parity(ctx):
         assert np.array_equal(out, last)
     finally:
         m.free()
+
+
+def test_linear_times_reported_for_heterogeneous_steps(ctx):
+    dtype, L, H, F = synth.F16, 2, 256, 1024
+    m = Model(ctx, L, H, F, dtype, [0.5, 0.0, 0.4, 0.3] * L, [0, 1, 0, 0] * L)
+    try:
+        assert hg.hetegen_model_linear_ms(m.m, 4 * L) == [0.0] * (4 * L)
+        m.step(synth.normal((1, H), dtype, 0, synth.act_id(0)))
+        ms = hg.hetegen_model_linear_ms(m.m, 4 * L)
+        assert all(np.isfinite(v) and v > 0 for v in ms)
+    finally:
+        m.free()
