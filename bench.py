@@ -13,6 +13,9 @@ pinned host with the planner's CPU fraction), opt-30b (all linears in pinned hos
 memory, planner alpha), opt-66b (bf16, all host, --alpha sweep).  For those the
 planner's speeds come from hetegen_probe on the box, and the JSON line adds the
 heterogeneous figures (link and CPU rates, Table-2-style busy fractions).
+--placement sched lets the module scheduler (Sec. 4.5) pick the resident linears
+under --hbm-budget; --pageable keeps the weights in plain pageable memory, streamed
+through the hybrid pin || transfer path (Sec. 4.2-4.3).
 
 Prints ONE JSON line.  `value` is the effective weight bandwidth of the whole step
 (weight bytes per step / time per step); `ms_per_step` is the decode latency per
@@ -24,8 +27,10 @@ average is the region's time over its launches.  Peak: 8 TB/s HBM.
 the same linears.
 """
 import argparse
+import ctypes
 import hashlib
 import json
+import mmap
 import os
 import sys
 import time
@@ -92,6 +97,11 @@ def main():
                     help="refine the streamed linears' CPU fractions with the step-level alpha benchmark "
                          "(Sec. 4.4) and time the step with both the closed-form and the refined fractions")
     ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: OpenMP default)")
+    ap.add_argument("--pageable", action="store_true",
+                    help="weights in plain pageable host memory (transparent huge pages), streamed through the "
+                         "hybrid pin || transfer path (Sec. 4.2); biases stay pinned")
+    ap.add_argument("--pin-threads", type=int, default=0, help="pin team threads for --pageable (0: library default)")
+    ap.add_argument("--pin-ring", type=int, default=0, help="pinned staging buffers for --pageable (0: default)")
     ap.add_argument("--chunk-mb", type=int, default=32)
     ap.add_argument("--ring", type=int, default=8)
     ap.add_argument("--exec", choices=("auto", "persistent", "graph", "eager"), default="auto",
@@ -119,16 +129,25 @@ def main():
         L = min(L, args.layers)
     placement = args.placement or placement
     B = args.batch
-    ctx = hg.hetegen_create(0, cpu_threads=args.threads, chunk_bytes=args.chunk_mb << 20, ring_depth=args.ring)
+    ctx = hg.hetegen_create(0, cpu_threads=args.threads, chunk_bytes=args.chunk_mb << 20, ring_depth=args.ring,
+                            pin_threads=args.pin_threads, pin_ring=args.pin_ring)
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
 
-    # ---- synthetic OPT-shaped weights in pinned host memory ----
+    # ---- synthetic OPT-shaped weights in pinned (or pageable) host memory ----
     t0 = time.time()
     W, b, shp = [], [], []
+    maps = []
     for l in range(L):
         for i, (n, k) in enumerate(shapes(H, F)):
-            w = hg.hetegen_host_alloc(ctx, n * k * 2)
+            if args.pageable:
+                mm = mmap.mmap(-1, n * k * 2)
+                if hasattr(mm, "madvise") and hasattr(mmap, "MADV_HUGEPAGE"):
+                    mm.madvise(mmap.MADV_HUGEPAGE)
+                maps.append(mm)
+                w = ctypes.addressof(ctypes.c_char.from_buffer(mm))
+            else:
+                w = hg.hetegen_host_alloc(ctx, n * k * 2)
             bb = hg.hetegen_host_alloc(ctx, n * 2)
             synth.fill_normal_ptr(w, n * k, dt, 0, synth.weight_id(l, NAMES[i]), 0.0, 0.02)
             synth.fill_normal_ptr(bb, n, dt, 0, synth.bias_id(l, NAMES[i]), 0.0, 0.02)
@@ -153,8 +172,9 @@ def main():
             t0 = time.time()
             probe[NAMES[m]] = hg.hetegen_probe(ctx, W[last + m], n, k, dt, B, 3)
             p = probe[NAMES[m]]
-            log("probe %s [%d,%d]: V_CPU %.1f GB/s, V_COM %.1f GB/s, V_GPU %.0f GB/s (%.1f s)" %
-                (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9, time.time() - t0))
+            log("probe %s [%d,%d]: V_CPU %.1f GB/s, V_COM %.1f GB/s, V_GPU %.0f GB/s, V_PIN %.1f GB/s (%.1f s)" %
+                (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9,
+                 p["pin_Bps"] / 1e9, time.time() - t0))
         bws = [tuple(probe[NAMES[i % 4]][f] for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps", "pin_Bps"))
                for i in range(4 * L)]
     # fresh input per step, resident in HBM before timing
@@ -238,7 +258,7 @@ def main():
         desc = "module scheduler: %d of %d linears HBM-resident (%.2f of %.2f GB budget), rest streamed from " \
                "pinned host" % (sum(resident), 4 * L, schedule["resident_GB"], schedule["hbm_budget_GB"])
     else:
-        desc = "all linears in pinned host memory, streamed + CPU share"
+        desc = "all linears in %s host memory, streamed + CPU share" % ("pageable" if args.pageable else "pinned")
     if placement != "all":
         desc += ", %s" % ("planner alpha" if args.alpha is None else "alpha=%g" % args.alpha)
     result = {
@@ -293,7 +313,9 @@ def main():
         cpu_b = sum(n_cpu[i] * shp[i][1] * 2 for i in streamed)
         h2d_b = sb - cpu_b
         v_cpu = float(np.mean([p["cpu_Bps"] for p in probe.values()]))
-        v_com = float(np.mean([p["h2d_Bps"] for p in probe.values()]))
+        # Eq. 8: with pageable weights the link side runs at min(V_PIN, V_TRANS)
+        v_com = float(np.mean([min(p["h2d_Bps"], p["pin_Bps"]) if p["pin_Bps"] > 0 else p["h2d_Bps"]
+                               for p in probe.values()]))
         v_gpu = float(np.mean([p["hbm_gemv_Bps"] for p in probe.values()]))
         v_g = 1.0 / (1.0 / v_com + 1.0 / v_gpu)
         hbm_b = wbytes - sb
@@ -310,7 +332,7 @@ def main():
         result["hetero"] = {
             "alpha_cpu_by_linear": {NAMES[m]: round(alpha[i], 4) for m in range(4)
                                     for i in [next((j for j in streamed if j % 4 == m), None)] if i is not None},
-            "probe_GBps": {k: {f: round(v[f] / 1e9, 2) for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps")}
+            "probe_GBps": {k: {f: round(v[f] / 1e9, 2) for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps", "pin_Bps")}
                            for k, v in probe.items()},
             "streamed_bytes_per_step": sb, "h2d_bytes_per_step": h2d_b, "cpu_bytes_per_step": cpu_b,
             "h2d_GBps_over_step": round(h2d_b / (ms_step * 1e-3) / 1e9, 2),
@@ -319,7 +341,7 @@ def main():
             "ideal_ms_per_step": round(ideal_s * 1e3, 3),
             "frac_of_ideal": round(ideal_s * 1e3 / ms_step, 4),
             "busy_frac": {"cpu": round(prof["cpu_ms"] / wall_ms, 4), "io": round(prof["h2d_ms"] / wall_ms, 4),
-                          "gpu": round(prof["gpu_ms"] / wall_ms, 4)},
+                          "gpu": round(prof["gpu_ms"] / wall_ms, 4), "pin": round(prof["pin_ms"] / wall_ms, 4)},
             "profiled_ms_per_step": round(wall_ms / nprof, 3),
         }
         log("hetero: %s" % json.dumps(result["hetero"]))
@@ -395,7 +417,7 @@ def main():
         torch.cuda.synchronize()
 
     hg.hetegen_model_destroy(ctx, model)
-    for p in W + b:
+    for p in (b if args.pageable else W + b):
         hg.hetegen_host_free(ctx, p)
     hg.hetegen_destroy(ctx)
     print(json.dumps(result), flush=True)

@@ -55,10 +55,24 @@ typedef struct {
   int cpu_threads;    /* host threads for the CPU share; <= 0: the OpenMP default */
   size_t chunk_bytes; /* weight bytes per streamed chunk; 0: 32 MiB */
   int ring_depth;     /* device staging slots for streamed chunks, in [2, 64]; 0: 8 */
+  int pin_threads;    /* host threads that stage pageable weights into pinned memory
+                         (Sec. 4.2 hybrid pin || transfer), in [1, 64]; 0: 4;
+                         < 0: pageable weights are refused with HETEGEN_ERR_NOT_PINNED */
+  int pin_ring;       /* pinned staging buffers of chunk_bytes each, in [2, 64]; 0: 4 */
 } hetegen_config;
 
 /* Create a context on cfg->device: a copy stream, the staging ring
- * (ring_depth x chunk_bytes of HBM), pinned hand-off buffers and events.
+ * (ring_depth x chunk_bytes of HBM), pinned hand-off buffers, events and the
+ * parameter manager thread (Sec. 4.3), which owns the copy stream: it walks the
+ * streamed chunks of a call in order and copies each into the staging ring as soon
+ * as the slot is free, running ahead of the GEMVs across linears and layers.  A
+ * chunk of pageable weights is first copied into a pinned staging buffer by the
+ * pin team (pin_threads threads, the manager included) while earlier chunks are in
+ * flight over PCIe, so pinning and transfer overlap (Eq. 8: T_COM = max(T_PIN,
+ * T_TRANS)); pinned memory stays bounded by pin_ring x chunk_bytes, allocated at
+ * the first pageable chunk.  For full overlap with the CPU share, ring_depth x
+ * chunk_bytes should hold the largest GPU share of a streamed linear: the GEMVs of
+ * chunks that were not yet staged when the CPU share starts are enqueued after it.
  * cfg may be NULL (device 0, defaults).  *out receives the context. */
 HETEGEN_API hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out);
 
@@ -82,7 +96,8 @@ HETEGEN_API hetegen_status hetegen_host_free(hetegen_ctx* ctx, void* p);
  *
  * rows j < n_gpu on the GPU, rows j >= n_gpu on host threads (see alpha above).
  *   x_dev          device, [B, K] in w_dtype, row stride K, 16-byte aligned.
- *   W_host         pinned host (hetegen_host_alloc or hipHostMalloc), [N, K] w_dtype.
+ *   W_host         host [N, K] w_dtype: pinned (hetegen_host_alloc or hipHostMalloc),
+ *                  or pageable (staged through pinned buffers, see hetegen_create).
  *   W_dev_resident optional device copy of rows [0, n_gpu) (row stride K); when
  *                  NULL the GPU rows are streamed from W_host through the staging
  *                  ring in chunks, overlapped with the CPU share.
@@ -92,7 +107,8 @@ HETEGEN_API hetegen_status hetegen_host_free(hetegen_ctx* ctx, void* p);
  *   y_dev          device [B, N] of y_dtype (w_dtype or HETEGEN_F32), row stride N.
  * GPU work is enqueued on `stream`.  The call returns after the CPU share is
  * computed and its upload is enqueued; y is complete in `stream` order.
- * B in [1, 8], K % 8 == 0, K >= 8, N >= 1.  W_host must be pinned (NOT_PINNED). */
+ * B in [1, 8], K % 8 == 0, K >= 8, N >= 1.  NOT_PINNED if W_host is pageable and
+ * the context refuses pageable weights (pin_threads < 0). */
 HETEGEN_API hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K, const void* W_host,
                               const void* W_dev_resident, int N, hetegen_dtype w_dtype,
                               const void* bias_host, const void* bias_dev, double alpha, void* y_dev,
@@ -131,7 +147,10 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
  * distribution law): the CPU share GEMV over all N rows of W_host (alpha = 1), the
  * chunked host-to-device copy of W_host through the staging ring, and the GPU
  * GEMV over the staged chunks; each is the median of `reps` runs in weight bytes
- * per second (the CPU share after one untimed pass).  W_host is pinned [N, K]; batch B.  pin_Bps is set to 0. */
+ * per second (the CPU share after one untimed pass).  W_host is [N, K]; batch B.
+ * Pinned W_host: pin_Bps is set to 0 (no pinning).  Pageable W_host: pin_Bps is the
+ * pin team's rate staging W_host into the pinned buffers, h2d_Bps the copy rate
+ * from those buffers, each measured alone (the planner takes the smaller, Eq. 8). */
 HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
                              int B, int reps, hetegen_bw* out);
 
@@ -192,8 +211,9 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * intermediate stored in the model's 16-bit type (round to nearest even) and
  * a value-only attention (one position, empty KV cache: the result is V). */
 
-/* W_host[i], bias_host[i]: pinned host weights and host biases of linear i
- * (caller-owned, must outlive the model).  alpha[i]: CPU fraction of linear i.
+/* W_host[i], bias_host[i]: host weights (pinned, or pageable as for
+ * hetegen_linear) and host biases of linear i (caller-owned, must outlive the
+ * model).  alpha[i]: CPU fraction of linear i.
  * resident[i] != 0: rows [0, n_gpu) of linear i are copied to HBM at creation;
  * otherwise they are streamed every step.  max_batch in [1, 8]. */
 HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
@@ -289,6 +309,8 @@ typedef struct {
   double gpu_bytes;    /* weight bytes read by GPU GEMV launches */
   double cpu_bytes;    /* weight bytes read by CPU shares */
   int64_t gemv_launches;
+  double pin_ms;       /* host time the pin team spent staging pageable chunks */
+  double pin_bytes;    /* bytes staged */
 } hetegen_profile;
 
 /* on != 0: bracket every chunk copy and GEMV launch with events and synchronise at

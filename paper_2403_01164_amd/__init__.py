@@ -34,7 +34,7 @@ if not os.path.exists(LIB_PATH):
 
 class Config(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int), ("cpu_threads", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
-                ("ring_depth", ctypes.c_int)]
+                ("ring_depth", ctypes.c_int), ("pin_threads", ctypes.c_int), ("pin_ring", ctypes.c_int)]
 
 
 class Shape(ctypes.Structure):
@@ -49,7 +49,8 @@ class Bw(ctypes.Structure):
 class Profile(ctypes.Structure):
     _fields_ = [("wall_ms", ctypes.c_double), ("cpu_ms", ctypes.c_double), ("h2d_ms", ctypes.c_double),
                 ("gpu_ms", ctypes.c_double), ("h2d_bytes", ctypes.c_double), ("gpu_bytes", ctypes.c_double),
-                ("cpu_bytes", ctypes.c_double), ("gemv_launches", ctypes.c_int64)]
+                ("cpu_bytes", ctypes.c_double), ("gemv_launches", ctypes.c_int64), ("pin_ms", ctypes.c_double),
+                ("pin_bytes", ctypes.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -109,8 +110,8 @@ def _check(rc, ctx=None):
         raise HetegenError(rc, msg.decode() if msg else "")
 
 
-def hetegen_create(device=0, cpu_threads=0, chunk_bytes=0, ring_depth=0):
-    cfg = Config(device, cpu_threads, chunk_bytes, ring_depth)
+def hetegen_create(device=0, cpu_threads=0, chunk_bytes=0, ring_depth=0, pin_threads=0, pin_ring=0):
+    cfg = Config(device, cpu_threads, chunk_bytes, ring_depth, pin_threads, pin_ring)
     out = _vp()
     _check(_lib.hetegen_create(ctypes.byref(cfg), ctypes.byref(out)))
     return out.value

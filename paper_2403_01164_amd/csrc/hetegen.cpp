@@ -14,7 +14,10 @@
 //   4. a kernel reads the CPU rows from pinned memory, finishes them like the GPU
 //      rows (ReLU / residual / rounding) and writes them into the output.
 // Weights for later chunks are copied as soon as a ring slot is free, across
-// linear and layer boundaries (Sec. 3.1: idle time is hidden by prefetching).
+// linear and layer boundaries (Sec. 3.1: idle time is hidden by prefetching), by
+// the context's parameter manager thread (Sec. 4.3), which owns the copy stream.
+// Pageable weights take one more stage: the pin team copies each chunk into a
+// pinned staging buffer while earlier chunks cross PCIe (Sec. 4.2, Fig. 5c).
 #include <hip/hip_runtime_api.h>
 
 #include <math.h>
@@ -24,9 +27,12 @@
 
 #include <algorithm>
 #include <chrono>
+#include <condition_variable>
 #include <deque>
 #include <map>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/hetegen.h"
@@ -49,6 +55,88 @@ constexpr int kBarrierGroups = 16;
 constexpr size_t kCounterBytes = 256;
 constexpr int kDefaultRing = 8;
 constexpr int kMaxBatch = 8;
+constexpr int kDefaultPinThreads = 4;
+constexpr int kDefaultPinRing = 4;
+
+// Fork-join team for large host copies: the calling thread takes the first part,
+// helpers the others (page-aligned contiguous parts).
+class PinTeam {
+ public:
+  ~PinTeam() { shutdown(); }
+  bool started() const { return parts_ > 0; }
+  bool start(int threads) {
+    parts_ = std::max(1, threads);
+    try {
+      for (int i = 1; i < parts_; ++i) th_.emplace_back([this, i] { work(i); });
+    } catch (...) {
+      shutdown();
+      return false;
+    }
+    return true;
+  }
+  void copy(char* dst, const char* src, size_t n) {
+    if (parts_ <= 1 || n < ((size_t)1 << 20)) {
+      memcpy(dst, src, n);
+      return;
+    }
+    {
+      std::lock_guard<std::mutex> lk(m_);
+      dst_ = dst;
+      src_ = src;
+      n_ = n;
+      pending_ = parts_ - 1;
+      ++gen_;
+    }
+    cv_.notify_all();
+    part(dst, src, n, 0);
+    std::unique_lock<std::mutex> lk(m_);
+    done_.wait(lk, [&] { return pending_ == 0; });
+  }
+  void shutdown() {
+    {
+      std::lock_guard<std::mutex> lk(m_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto& t : th_) t.join();
+    th_.clear();
+    parts_ = 0;
+    stop_ = false;
+  }
+
+ private:
+  void part(char* dst, const char* src, size_t n, int i) const {
+    const size_t per = (n / parts_ + 4095) & ~(size_t)4095;
+    const size_t b = per * i;
+    if (b >= n) return;
+    memcpy(dst + b, src + b, std::min(n, b + per) - b);
+  }
+  void work(int i) {
+    long long seen = 0;
+    std::unique_lock<std::mutex> lk(m_);
+    for (;;) {
+      cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
+      if (stop_) return;
+      seen = gen_;
+      char* d = dst_;
+      const char* s = src_;
+      const size_t n = n_;
+      lk.unlock();
+      part(d, s, n, i);
+      lk.lock();
+      if (--pending_ == 0) done_.notify_one();
+    }
+  }
+  std::vector<std::thread> th_;
+  std::mutex m_;
+  std::condition_variable cv_, done_;
+  long long gen_ = 0;
+  int pending_ = 0, parts_ = 0;
+  bool stop_ = false;
+  char* dst_ = nullptr;
+  const char* src_ = nullptr;
+  size_t n_ = 0;
+};
 
 }  // namespace
 
@@ -68,15 +156,31 @@ struct hetegen_ctx {
   float* y_host = nullptr;
   size_t y_host_bytes = 0;
   bool y_pending = false;  // ev_y recorded after the last read of y_host
-  // streamed-chunk pipeline
+  // streamed-chunk pipeline, shared with the parameter manager thread under `mu`.
+  // Chunk number s goes to ring slot s % ring; its copy may be enqueued once the
+  // GEMV of chunk s - ring has been enqueued (head > s - ring).
   struct Chunk {
     const char* src;
     size_t bytes;
+    bool pageable;
   };
-  std::deque<Chunk> planned;  // not yet consumed; the first `copied` have copies enqueued
-  int copied = 0;
-  long long seq_head = 0;  // sequence number of planned.front()
-  // profiling
+  std::mutex mu;
+  std::condition_variable cv;
+  std::deque<Chunk> jobs;  // planned chunks whose GEMV is not enqueued; front() is number `head`
+  long long head = 0;
+  long long copy_enq = 0;  // copies of chunks numbered below copy_enq are enqueued
+  bool busy = false, stop = false, failed = false;
+  std::string mgr_err;
+  std::thread mgr;
+  // pageable weights: pinned staging buffers and the team that fills them
+  int pin_threads = kDefaultPinThreads;  // < 0: pageable weights refused
+  int pin_ring = kDefaultPinRing;
+  std::vector<void*> bounce;
+  std::vector<hipEvent_t> ev_bounce;
+  long long bounce_seq = 0;  // manager thread only
+  PinTeam team;
+  // profiling (the manager records copy events too: `prof_mu`)
+  std::mutex prof_mu;
   bool profiling = false;
   struct Timed {
     hipEvent_t a, b;
@@ -97,6 +201,7 @@ struct hetegen_model {
     double alpha = 0;
     int resident = 0;
     int n_gpu = 0, n_cpu = 0;
+    bool pageable = false;     // W_host is plain host memory (staged when streamed)
     void* W_dev = nullptr;     // rows [0, n_gpu) when resident
     void* bias_dev = nullptr;  // all N biases
   };
@@ -187,6 +292,25 @@ hetegen_status ensure_host(hetegen_ctx* ctx, float** buf, size_t* have, size_t n
   return HETEGEN_OK;
 }
 
+hetegen_status check_pinned(hetegen_ctx* ctx, const void* p, size_t bytes);
+
+// Pinned weights are copied straight from W_host; pageable ones (plain host memory
+// that HIP does not know) are staged through the pinned buffers unless the context
+// refuses them.
+hetegen_status check_weight(hetegen_ctx* ctx, const void* p, size_t bytes, bool* pageable) {
+  *pageable = false;
+  hipPointerAttribute_t a;
+  hipError_t e = hipPointerGetAttributes(&a, p);
+  if (e != hipSuccess) (void)hipGetLastError();
+  if (e != hipSuccess || a.type == hipMemoryTypeUnregistered) {
+    if (ctx->pin_threads < 0)
+      return fail(ctx, HETEGEN_ERR_NOT_PINNED, "host weight %p is not page-locked memory", p);
+    *pageable = true;
+    return HETEGEN_OK;
+  }
+  return check_pinned(ctx, p, bytes);
+}
+
 hetegen_status check_pinned(hetegen_ctx* ctx, const void* p, size_t bytes) {
   const char* ends[2] = {(const char*)p, (const char*)p + bytes - 1};
   for (const char* q : ends) {
@@ -205,6 +329,7 @@ hetegen_status check_pinned(hetegen_ctx* ctx, const void* p, size_t bytes) {
 
 // ---- profiling helpers ----
 hipEvent_t pool_event(hetegen_ctx* ctx) {
+  std::lock_guard<std::mutex> lk(ctx->prof_mu);
   if (!ctx->ev_pool.empty()) {
     hipEvent_t e = ctx->ev_pool.back();
     ctx->ev_pool.pop_back();
@@ -219,6 +344,7 @@ hipEvent_t pool_event(hetegen_ctx* ctx) {
 }
 
 hetegen_status flush_profile(hetegen_ctx* ctx) {
+  std::lock_guard<std::mutex> lk(ctx->prof_mu);
   for (auto& t : ctx->timed) {
     HIPCHK(ctx, hipEventSynchronize(t.b));
     float ms = 0;
@@ -255,25 +381,74 @@ struct TimedScope {
     hipEvent_t b = pool_event(ctx);
     if (!b) return;
     (void)hipEventRecord(b, s);
+    std::lock_guard<std::mutex> lk(ctx->prof_mu);
     ctx->timed.push_back({a, b, kind, bytes});
     a = nullptr;
   }
 };
 
-// ---- streamed-chunk pipeline ----
-hetegen_status pump(hetegen_ctx* ctx) {
-  while (ctx->copied < (int)ctx->planned.size() && ctx->copied < ctx->ring) {
-    const long long seq = ctx->seq_head + ctx->copied;
-    const int s = (int)(seq % ctx->ring);
-    const auto& c = ctx->planned[ctx->copied];
-    HIPCHK(ctx, hipStreamWaitEvent(ctx->copy_stream, ctx->ev_free[s], 0));
-    TimedScope ts(ctx, ctx->copy_stream, 0, (double)c.bytes);
-    HIPCHK(ctx, hipMemcpyAsync(ctx->slot[s], c.src, c.bytes, hipMemcpyHostToDevice, ctx->copy_stream));
-    ts.end();
-    HIPCHK(ctx, hipEventRecord(ctx->ev_ready[s], ctx->copy_stream));
-    ctx->copied++;
+// ---- streamed-chunk pipeline: the parameter manager ----
+// Copy chunk number s into its ring slot: wait (on the copy stream) for the GEMV
+// that last read the slot; a pageable chunk is first staged into a pinned buffer
+// whose previous copy has completed.  Runs on the manager thread.
+bool copy_chunk(hetegen_ctx* ctx, long long s, const hetegen_ctx::Chunk& c, std::string* err) {
+  const int slot = (int)(s % ctx->ring);
+  hipError_t e;
+#define MGR_HIP(expr)                                                           \
+  do {                                                                        \
+    if ((e = (expr)) != hipSuccess) {                                         \
+      *err = std::string(#expr) + " failed: " + hipGetErrorString(e);         \
+      return false;                                                           \
+    }                                                                         \
+  } while (0)
+  MGR_HIP(hipStreamWaitEvent(ctx->copy_stream, ctx->ev_free[slot], 0));
+  const void* src = c.src;
+  int b = -1;
+  if (c.pageable) {
+    b = (int)(ctx->bounce_seq++ % ctx->pin_ring);
+    MGR_HIP(hipEventSynchronize(ctx->ev_bounce[b]));  // its previous copy has read it
+    const auto t0 = Clock::now();
+    ctx->team.copy((char*)ctx->bounce[b], c.src, c.bytes);
+    {
+      std::lock_guard<std::mutex> lk(ctx->prof_mu);
+      ctx->prof.pin_ms += ms_since(t0);
+      ctx->prof.pin_bytes += (double)c.bytes;
+    }
+    src = ctx->bounce[b];
   }
-  return HETEGEN_OK;
+  TimedScope ts(ctx, ctx->copy_stream, 0, (double)c.bytes);
+  MGR_HIP(hipMemcpyAsync(ctx->slot[slot], src, c.bytes, hipMemcpyHostToDevice, ctx->copy_stream));
+  ts.end();
+  MGR_HIP(hipEventRecord(ctx->ev_ready[slot], ctx->copy_stream));
+  if (b >= 0) MGR_HIP(hipEventRecord(ctx->ev_bounce[b], ctx->copy_stream));
+#undef MGR_HIP
+  return true;
+}
+
+void manager_main(hetegen_ctx* ctx) {
+  (void)hipSetDevice(ctx->device);
+  std::unique_lock<std::mutex> lk(ctx->mu);
+  for (;;) {
+    ctx->cv.wait(lk, [&] {
+      return ctx->stop || (!ctx->failed && ctx->copy_enq < ctx->head + (long long)ctx->jobs.size() &&
+                           ctx->copy_enq - ctx->head < ctx->ring);
+    });
+    if (ctx->stop) return;
+    const long long s = ctx->copy_enq;
+    const hetegen_ctx::Chunk c = ctx->jobs[(size_t)(s - ctx->head)];
+    ctx->busy = true;
+    lk.unlock();
+    std::string err;
+    const bool ok = copy_chunk(ctx, s, c, &err);
+    lk.lock();
+    ctx->busy = false;
+    if (ok) ctx->copy_enq = s + 1;
+    else {
+      ctx->failed = true;
+      ctx->mgr_err = err;
+    }
+    ctx->cv.notify_all();
+  }
 }
 
 int chunk_rows_for(const hetegen_ctx* ctx, int K, int dtype) {
@@ -282,13 +457,87 @@ int chunk_rows_for(const hetegen_ctx* ctx, int K, int dtype) {
   return r < 1 ? 1 : (int)std::min<size_t>(r, (size_t)1 << 30);
 }
 
-void plan_chunks(hetegen_ctx* ctx, const void* W_host, int n_gpu, int K, int dtype) {
+bool pipeline_idle(hetegen_ctx* ctx) {
+  std::lock_guard<std::mutex> lk(ctx->mu);
+  return ctx->jobs.empty();
+}
+
+// Pinned staging buffers and the pin team, at the first pageable chunk.
+// Called with the pipeline idle (no copy in flight on the manager thread).
+hetegen_status ensure_pin_resources(hetegen_ctx* ctx) {
+  if (ctx->team.started()) return HETEGEN_OK;
+  ctx->bounce.resize(ctx->pin_ring, nullptr);
+  ctx->ev_bounce.resize(ctx->pin_ring, nullptr);
+  for (int i = 0; i < ctx->pin_ring; ++i) {
+    if (!ctx->bounce[i] && hipHostMalloc(&ctx->bounce[i], ctx->chunk_bytes, hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      ctx->bounce[i] = nullptr;
+      return fail(ctx, HETEGEN_ERR_OOM, "pinned staging buffer of %zu bytes", ctx->chunk_bytes);
+    }
+    if (!ctx->ev_bounce[i]) {
+      HIPCHK(ctx, hipEventCreateWithFlags(&ctx->ev_bounce[i], hipEventDisableTiming));
+      HIPCHK(ctx, hipEventRecord(ctx->ev_bounce[i], ctx->copy_stream));
+    }
+  }
+  if (!ctx->team.start(ctx->pin_threads)) return fail(ctx, HETEGEN_ERR_OOM, "pin team threads");
+  return HETEGEN_OK;
+}
+
+// Queue the chunks of rows [0, n_gpu) of one streamed weight; the manager starts
+// copying at once.
+void plan_chunks(hetegen_ctx* ctx, const void* W_host, int n_gpu, int K, int dtype, bool pageable) {
   const size_t row = (size_t)K * elem_size(dtype);
   const int cr = chunk_rows_for(ctx, K, dtype);
-  for (int r0 = 0; r0 < n_gpu; r0 += cr) {
-    int nr = std::min(cr, n_gpu - r0);
-    ctx->planned.push_back({(const char*)W_host + (size_t)r0 * row, (size_t)nr * row});
+  {
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    for (int r0 = 0; r0 < n_gpu; r0 += cr) {
+      int nr = std::min(cr, n_gpu - r0);
+      ctx->jobs.push_back({(const char*)W_host + (size_t)r0 * row, (size_t)nr * row, pageable});
+    }
   }
+  ctx->cv.notify_all();
+}
+
+// The oldest planned chunk: whether its copy is enqueued (waiting for it when
+// `block`, or when `block_pinned` and the chunk is pinned), its number and size.
+hetegen_status front_chunk(hetegen_ctx* ctx, bool block, bool block_pinned, bool* ready, long long* seq,
+                           size_t* bytes) {
+  std::unique_lock<std::mutex> lk(ctx->mu);
+  if (ctx->jobs.empty()) {
+    lk.unlock();
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk pipeline is empty");
+  }
+  if (block || (block_pinned && !ctx->jobs.front().pageable))
+    ctx->cv.wait(lk, [&] { return ctx->failed || ctx->copy_enq > ctx->head; });
+  if (ctx->failed) {
+    const std::string m = ctx->mgr_err;
+    lk.unlock();
+    return fail(ctx, HETEGEN_ERR_HIP, "parameter manager: %s", m.c_str());
+  }
+  *ready = ctx->copy_enq > ctx->head;
+  *seq = ctx->head;
+  *bytes = ctx->jobs.front().bytes;
+  return HETEGEN_OK;
+}
+
+void pop_chunk(hetegen_ctx* ctx) {
+  {
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    ctx->jobs.pop_front();
+    ctx->head++;
+  }
+  ctx->cv.notify_all();
+}
+
+// Drop the planned chunks after a failed call (copies already enqueued complete on
+// the copy stream; nothing reads them).
+void reset_pipeline(hetegen_ctx* ctx) {
+  std::unique_lock<std::mutex> lk(ctx->mu);
+  ctx->cv.wait(lk, [&] { return !ctx->busy; });
+  ctx->jobs.clear();
+  ctx->head = ctx->copy_enq;
+  ctx->failed = false;
+  ctx->mgr_err.clear();
 }
 
 // ---- one linear ----
@@ -359,27 +608,38 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   if (j.trace_in && !fused_ln)
     HIPCHK(ctx, hipMemcpy2DAsync(j.trace_in, (size_t)j.K * s, xin, (size_t)ldin * s, (size_t)j.K * s, j.B,
                                  hipMemcpyDeviceToDevice, st));
-  // 2. GPU rows
-  if (j.n_gpu > 0) {
-    if (j.W_dev) {
-      TRY(run_gemv(ctx, j, xin, ldin, fused_ln ? 1 : 0, j.W_dev, 0, j.n_gpu, st, fused_ln ? j.trace_in : nullptr));
-    } else {
-      const int cr = chunk_rows_for(ctx, j.K, j.dtype);
-      for (int r0 = 0; r0 < j.n_gpu; r0 += cr) {
-        const int nr = std::min(cr, j.n_gpu - r0);
-        if (ctx->copied < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk pipeline is empty");
-        const int slot = (int)(ctx->seq_head % ctx->ring);
-        if (ctx->planned.front().bytes != (size_t)nr * j.K * s)
-          return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk plan out of step");
-        HIPCHK(ctx, hipStreamWaitEvent(st, ctx->ev_ready[slot], 0));
-        TRY(run_gemv(ctx, j, xin, ldin, 0, ctx->slot[slot], r0, nr, st, nullptr));
-        HIPCHK(ctx, hipEventRecord(ctx->ev_free[slot], st));
-        ctx->planned.pop_front();
-        ctx->copied--;
-        ctx->seq_head++;
-        TRY(pump(ctx));
-      }
-    }
+  // 2. GPU rows: one GEMV when resident; otherwise one GEMV per streamed chunk, each
+  //    waiting on the copy stream for its slot.  Before the CPU share only chunks
+  //    whose copy is already enqueued, or will be at once (pinned chunks wait only
+  //    for slots that these GEMVs free), so that staging pageable weights does not
+  //    hold up the CPU share; the rest after it.
+  const bool streamed = j.n_gpu > 0 && !j.W_dev;
+  int r0 = 0;
+  const int cr = chunk_rows_for(ctx, j.K, j.dtype);
+  auto next_chunk = [&](bool block, bool* did) -> hetegen_status {
+    *did = false;
+    bool ready = false;
+    long long seq = 0;
+    size_t bytes = 0;
+    TRY(front_chunk(ctx, block, true, &ready, &seq, &bytes));
+    if (!ready) return HETEGEN_OK;
+    const int nr = std::min(cr, j.n_gpu - r0);
+    if (bytes != (size_t)nr * j.K * s) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk plan out of step");
+    const int slot = (int)(seq % ctx->ring);
+    HIPCHK(ctx, hipStreamWaitEvent(st, ctx->ev_ready[slot], 0));
+    TRY(run_gemv(ctx, j, xin, ldin, 0, ctx->slot[slot], r0, nr, st, nullptr));
+    HIPCHK(ctx, hipEventRecord(ctx->ev_free[slot], st));
+    pop_chunk(ctx);
+    r0 += nr;
+    *did = true;
+    return HETEGEN_OK;
+  };
+  if (j.n_gpu > 0 && j.W_dev)
+    TRY(run_gemv(ctx, j, xin, ldin, fused_ln ? 1 : 0, j.W_dev, 0, j.n_gpu, st, fused_ln ? j.trace_in : nullptr));
+  while (streamed && r0 < j.n_gpu) {
+    bool did = false;
+    TRY(next_chunk(j.n_cpu == 0, &did));
+    if (!did) break;
   }
   // 3. CPU rows on the calling thread's OpenMP team
   if (j.n_cpu > 0) {
@@ -400,6 +660,10 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
                                        j.ldr, st));
     HIPCHK(ctx, hipEventRecord(ctx->ev_y, st));
     ctx->y_pending = true;
+  }
+  while (streamed && r0 < j.n_gpu) {
+    bool did = false;
+    TRY(next_chunk(true, &did));
   }
   if (j.trace_out)
     HIPCHK(ctx, hipMemcpy2DAsync(j.trace_out, (size_t)j.N * s, j.y, (size_t)j.ldy * s, (size_t)j.N * s, j.B,
@@ -429,6 +693,11 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
   if (c.chunk_bytes < 4096 || (c.chunk_bytes & 15u))
     return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "chunk_bytes %zu must be >= 4096 and a multiple of 16",
                 c.chunk_bytes);
+  if (c.pin_threads == 0) c.pin_threads = kDefaultPinThreads;
+  if (c.pin_ring == 0) c.pin_ring = kDefaultPinRing;
+  if (c.pin_threads > 64 || c.pin_ring < 2 || c.pin_ring > 64)
+    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "pin_threads %d must be <= 64 and pin_ring %d in [2, 64]",
+                c.pin_threads, c.pin_ring);
   int ndev = 0;
   hipError_t e = hipGetDeviceCount(&ndev);
   if (e != hipSuccess || ndev <= 0) {
@@ -442,6 +711,8 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
   ctx->cpu_threads = c.cpu_threads;
   ctx->chunk_bytes = c.chunk_bytes;
   ctx->ring = c.ring_depth;
+  ctx->pin_threads = c.pin_threads < 0 ? -1 : c.pin_threads;
+  ctx->pin_ring = c.pin_ring;
   auto bail = [&](hetegen_status st) {
     g_create_error = ctx->err;
     hetegen_destroy(ctx);
@@ -470,14 +741,32 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
     if (hipEventRecord(ctx->ev_free[i], ctx->copy_stream) != hipSuccess)
       return bail(fail(ctx, HETEGEN_ERR_HIP, "hipEventRecord failed"));
   }
+  try {
+    ctx->mgr = std::thread(manager_main, ctx);
+  } catch (...) {
+    return bail(fail(ctx, HETEGEN_ERR_OOM, "parameter manager thread"));
+  }
   *out = ctx;
   return HETEGEN_OK;
 }
 
 hetegen_status hetegen_destroy(hetegen_ctx* ctx) {
   if (!ctx) return HETEGEN_OK;
+  if (ctx->mgr.joinable()) {
+    {
+      std::lock_guard<std::mutex> lk(ctx->mu);
+      ctx->stop = true;
+    }
+    ctx->cv.notify_all();
+    ctx->mgr.join();
+  }
+  ctx->team.shutdown();
   (void)hipSetDevice(ctx->device);
   (void)hipDeviceSynchronize();
+  for (size_t i = 0; i < ctx->bounce.size(); ++i) {
+    if (ctx->bounce[i]) (void)hipHostFree(ctx->bounce[i]);
+    if (ctx->ev_bounce[i]) (void)hipEventDestroy(ctx->ev_bounce[i]);
+  }
   for (auto& t : ctx->timed) {
     (void)hipEventDestroy(t.a);
     (void)hipEventDestroy(t.b);
@@ -540,7 +829,8 @@ hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K,
   const int n_cpu = split_cpu_rows(N, alpha), n_gpu = N - n_cpu;
   if ((n_cpu > 0 && !bias_host && bias_dev) || (n_gpu > 0 && !bias_dev && bias_host))
     return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bias: pass bias_host and bias_dev, or neither");
-  TRY(check_pinned(ctx, W_host, (size_t)N * K * 2));
+  bool pageable = false;
+  TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
   const size_t row = (size_t)K * 2;
   if (!W_dev_resident && n_gpu > 0 && row > ctx->chunk_bytes)
     return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "a weight row (%zu bytes) exceeds chunk_bytes", row);
@@ -564,14 +854,13 @@ hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K,
   j.y_f32 = y_dtype == HETEGEN_F32;
   j.epi = hg::EPI_NONE;
   if (!W_dev_resident && n_gpu > 0) {
-    if (!ctx->planned.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
-    plan_chunks(ctx, W_host, n_gpu, K, w_dtype);
-    TRY(pump(ctx));
+    if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+    if (pageable) TRY(ensure_pin_resources(ctx));
+    plan_chunks(ctx, W_host, n_gpu, K, w_dtype, pageable);
   }
   hetegen_status stt = run_linear(ctx, j, st);
   if (stt != HETEGEN_OK) {
-    ctx->planned.clear();
-    ctx->copied = 0;
+    reset_pipeline(ctx);
     return stt;
   }
   return finish_call(ctx, t0);
@@ -852,8 +1141,12 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
   if (!ctx || !W_host || !out || N < 1 || K < 8 || K % 8 || B < 1 || B > kMaxBatch || reps < 1 ||
       (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
     return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe: bad arguments");
-  TRY(check_pinned(ctx, W_host, (size_t)N * K * 2));
+  bool pageable = false;
+  TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
   HIPCHK(ctx, hipSetDevice(ctx->device));
+  if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+  HIPCHK(ctx, hipDeviceSynchronize());  // earlier GEMVs may still read the staging slots
+  if (pageable) TRY(ensure_pin_resources(ctx));
   const size_t wbytes = (size_t)N * K * 2;
   auto median = [](std::vector<double> v) {
     std::sort(v.begin(), v.end());
@@ -871,20 +1164,31 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
     hg::cpu_share(ctx->x_host, B, K, (const uint16_t*)W_host, dtype, nullptr, 0, N, ctx->y_host, N, ctx->cpu_threads);
     if (r >= 0) tc.push_back(ms_since(t0) * 1e-3);
   }
-  // V_COM: chunked pinned copies through the ring on the copy stream
+  // V_PIN (pageable weights): the pin team staging W_host chunk by chunk
+  const size_t row = (size_t)K * 2;
+  const size_t cbytes = (size_t)chunk_rows_for(ctx, K, dtype) * row;
+  std::vector<double> tp;
+  for (int r = 0; pageable && r < reps; ++r) {
+    HIPCHK(ctx, hipStreamSynchronize(ctx->copy_stream));  // no copy reads the staging buffers
+    auto t0 = Clock::now();
+    int i = 0;
+    for (size_t off = 0; off < wbytes; off += cbytes, ++i)
+      ctx->team.copy((char*)ctx->bounce[i % ctx->pin_ring], (const char*)W_host + off, std::min(cbytes, wbytes - off));
+    tp.push_back(ms_since(t0) * 1e-3);
+  }
+  // V_COM: chunked copies through the ring on the copy stream, from W_host or (pageable)
+  // from the pinned staging buffers
   hipEvent_t a, b;
   HIPCHK(ctx, hipEventCreate(&a));
   HIPCHK(ctx, hipEventCreate(&b));
-  const size_t row = (size_t)K * 2;
-  const size_t cbytes = (size_t)chunk_rows_for(ctx, K, dtype) * row;
   std::vector<double> tm;
   for (int r = 0; r < reps; ++r) {
     HIPCHK(ctx, hipEventRecord(a, ctx->copy_stream));
     int i = 0;
     for (size_t off = 0; off < wbytes; off += cbytes, ++i) {
       const size_t nb = std::min(cbytes, wbytes - off);
-      HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], (const char*)W_host + off, nb, hipMemcpyHostToDevice,
-                                 ctx->copy_stream));
+      const void* src = pageable ? ctx->bounce[i % ctx->pin_ring] : (const char*)W_host + off;
+      HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], src, nb, hipMemcpyHostToDevice, ctx->copy_stream));
     }
     HIPCHK(ctx, hipEventRecord(b, ctx->copy_stream));
     HIPCHK(ctx, hipEventSynchronize(b));
@@ -934,7 +1238,7 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
   out->cpu_Bps = wbytes / median(tc);
   out->h2d_Bps = wbytes / median(tm);
   out->hbm_gemv_Bps = wbytes / median(tg);
-  out->pin_Bps = 0;
+  out->pin_Bps = pageable ? wbytes / median(tp) : 0;
   return HETEGEN_OK;
 }
 
@@ -961,10 +1265,11 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
   const int H = m->H, F = m->F;
   // plan every streamed chunk of the step up front so the copy stream can run
   // ahead across linears and layers, bounded by the ring
-  if (!ctx->planned.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+  if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
   for (const auto& l : m->lin)
-    if (!l.W_dev && l.n_gpu > 0) plan_chunks(ctx, l.W_host, l.n_gpu, l.K, m->dtype);
-  TRY(pump(ctx));
+    if (!l.W_dev && l.n_gpu > 0 && l.pageable) TRY(ensure_pin_resources(ctx));
+  for (const auto& l : m->lin)
+    if (!l.W_dev && l.n_gpu > 0) plan_chunks(ctx, l.W_host, l.n_gpu, l.K, m->dtype, l.pageable);
   char* tr = (char*)m->trace;
   auto take = [&](size_t elems) -> void* {
     if (!tr) return nullptr;
@@ -1156,7 +1461,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       model_free(m);
       return fail(ctx, HETEGEN_ERR_INVALID_ARG, "linear %d: weight pointer or alpha invalid", i);
     }
-    hetegen_status st = check_pinned(ctx, l.W_host, (size_t)l.N * l.K * 2);
+    hetegen_status st = check_weight(ctx, l.W_host, (size_t)l.N * l.K * 2, &l.pageable);
     if (st != HETEGEN_OK) {
       model_free(m);
       return st;
@@ -1441,8 +1746,7 @@ hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* m, const voi
   m->last_exec = HETEGEN_EXEC_EAGER;
   hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, st);
   if (s != HETEGEN_OK) {
-    ctx->planned.clear();
-    ctx->copied = 0;
+    reset_pipeline(ctx);
     return s;
   }
   return finish_call(ctx, t0);

@@ -46,3 +46,18 @@ class Pinned:
         if self.ptr:
             self.hg.hetegen_host_free(self.ctx, self.ptr)
             self.ptr = 0
+
+
+class Pageable:
+    """Plain (pageable) host buffer from an anonymous mapping, with a numpy view."""
+
+    def __init__(self, shape, np_dtype):
+        import mmap
+        n = int(np.prod(shape))
+        self.nbytes = n * np.dtype(np_dtype).itemsize
+        self.mm = mmap.mmap(-1, max(self.nbytes, 4096))
+        self.a = np.frombuffer(self.mm, dtype=np_dtype, count=n).reshape(shape)
+        self.ptr = self.a.ctypes.data
+
+    def free(self):
+        pass  # the mapping goes with the object

@@ -223,9 +223,6 @@ def test_argument_errors(ctx):
         assert status(N=0) == hg.ERR_INVALID_ARG
         assert status(ydt=hg.BF16) == hg.ERR_UNSUPPORTED
         assert status(bh=0) == hg.ERR_INVALID_ARG
-        pageable = np.zeros((16, 64), np.uint16)
-        assert status(W=pageable.ctypes.data) == hg.ERR_NOT_PINNED
-        assert "pinned" in hg.hetegen_last_error(ctx) or "page-locked" in hg.hetegen_last_error(ctx)
         torch.cuda.synchronize()
         assert status() == hg.OK  # the context still works after errors
         torch.cuda.synchronize()
