@@ -58,17 +58,27 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
+def kernel_code_sha(path):
+    """Hash of a kernel source with comments and blank lines removed (comment edits
+    do not change the code the counters were taken on)."""
+    lines = []
+    for l in open(path).read().splitlines():
+        code = l.split("//", 1)[0].rstrip()
+        if code:
+            lines.append(code)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()[:16]
+
+
 def counter_traffic(model, dt, B):
     """HBM bytes per GEMV launch from the committed counter summary, if it was taken
-    on this workload with the current kernel source; else None."""
+    on this workload with the current kernel code; else None."""
     name = "gemv_%s_b%d_%s_decode_hbm_counters.md" % ("bf16" if dt == 1 else "f16", B, model.replace("-", ""))
     path = os.path.join(ROOT, "profiles", name)
     src = os.path.join(ROOT, "paper_2403_01164_amd", "csrc", "kernels.hip")
     if not os.path.exists(path):
         return None
     fields = dict(l.split(": ", 1) for l in open(path).read().splitlines() if ": " in l and not l.startswith("#"))
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if fields.get("kernel_source_sha256_16", "").strip() != sha:
+    if fields.get("kernel_code_sha256_16", "").strip() != kernel_code_sha(src):
         return None
     return float(fields["traffic_bytes_per_launch"])
 

@@ -147,7 +147,8 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
  * distribution law): the CPU share GEMV over all N rows of W_host (alpha = 1), the
  * chunked host-to-device copy of W_host through the staging ring, and the GPU
  * GEMV over the staged chunks; each is the median of `reps` runs in weight bytes
- * per second (the CPU share after one untimed pass).  W_host is [N, K]; batch B.
+ * per second (the CPU share after one untimed pass; host caches are flushed
+ * before every CPU pass, as a step's weights always come from DRAM).  W_host is [N, K]; batch B.
  * Pinned W_host: pin_Bps is set to 0 (no pinning).  Pageable W_host: pin_Bps is the
  * pin team's rate staging W_host into the pinned buffers, h2d_Bps the copy rate
  * from those buffers, each measured alone (the planner takes the smaller, Eq. 8). */

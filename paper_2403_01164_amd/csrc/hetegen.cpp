@@ -1158,8 +1158,23 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
   TRY(ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, (size_t)B * K * 4));
   TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)B * N * 4));
   memset(ctx->x_host, 0, (size_t)B * K * 4);
+  // In a step every weight comes from DRAM (a step's weights dwarf the host caches);
+  // a single linear re-read by the probe can sit in a large L3, so the caches are
+  // flushed by writing a 1 GiB buffer before every pass.
+  std::vector<char> flush;
+  try {
+    flush.resize((size_t)1 << 30);
+  } catch (...) {
+    return fail(ctx, HETEGEN_ERR_OOM, "probe cache-flush buffer");
+  }
+  auto flush_caches = [&](int v) {
+    const long long nb = (long long)(flush.size() >> 20);
+#pragma omp parallel for schedule(static)
+    for (long long i = 0; i < nb; ++i) memset(flush.data() + (i << 20), v, (size_t)1 << 20);
+  };
   std::vector<double> tc;
-  for (int r = -1; r < reps; ++r) {  // one untimed pass first: threads up, caches and TLBs warm
+  for (int r = -1; r < reps; ++r) {  // one untimed pass first: threads up, TLBs warm
+    flush_caches(r & 0xff);
     auto t0 = Clock::now();
     hg::cpu_share(ctx->x_host, B, K, (const uint16_t*)W_host, dtype, nullptr, 0, N, ctx->y_host, N, ctx->cpu_threads);
     if (r >= 0) tc.push_back(ms_since(t0) * 1e-3);
@@ -1170,6 +1185,7 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
   std::vector<double> tp;
   for (int r = 0; pageable && r < reps; ++r) {
     HIPCHK(ctx, hipStreamSynchronize(ctx->copy_stream));  // no copy reads the staging buffers
+    flush_caches(r & 0xff);
     auto t0 = Clock::now();
     int i = 0;
     for (size_t off = 0; off < wbytes; off += cbytes, ++i)

@@ -405,8 +405,9 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
 // ---------------------------------------------------------------------------
 // Batch-1 GEMV without a fused LayerNorm: x is read straight from L1/L2 inside
 // the task loop (it is the same 2*K bytes for every wavefront, so it stays
-// cached), which removes the LDS prologue and its barrier; bias and residual are
-// requested with the task's weights and lane 0 stores each finished row.  Each
+// cached), which removes the LDS prologue and its barrier; the bias and residual
+// of a wavefront's rows are loaded once, ahead of its weight stream, into that
+// wavefront's slice of LDS, and lane 0 stores each finished row.  Each
 // lane accumulates its chunks in the same order as gemv_block, so both kernels
 // give bit-identical results.
 // ---------------------------------------------------------------------------
