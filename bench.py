@@ -116,6 +116,10 @@ def main():
     ap.add_argument("--ring", type=int, default=8)
     ap.add_argument("--exec", choices=("auto", "persistent", "graph", "eager"), default="auto",
                     help="execution mode of an all-resident step")
+    ap.add_argument("--context", type=int, default=0,
+                    help="full decode steps with attention over a KV cache holding this many earlier positions "
+                         "(synthetic keys/values standing in for a prefill; Sec. 2.1, Eq. 1); 0: the GEMV-only "
+                         "step (empty-cache attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with one plain 256 MiB device-to-device copy, the reference dispatch for "
@@ -229,8 +233,24 @@ def main():
         hg.hetegen_model_set_exec(model, {"persistent": hg.EXEC_PERSISTENT, "graph": hg.EXEC_GRAPH,
                                           "eager": hg.EXEC_EAGER}[args.exec])
 
+    P = args.context
+    if P > 0:
+        # KV cache for positions [0, P + warmup + steps); positions [0, P) get synthetic
+        # keys and values (the same for every layer), step t decodes position P + t
+        hd = 128
+        hg.hetegen_model_kv_create(ctx, model, P + nstep, hd)
+        kd = torch.from_numpy(synth.normal((B, P, H), dt, 0, 7001).view(np.int16)).cuda()
+        vd = torch.from_numpy(synth.normal((B, P, H), dt, 0, 7002).view(np.int16)).cuda()
+        for l in range(L):
+            hg.hetegen_model_kv_write(ctx, model, l, B, 0, P, kd.data_ptr(), vd.data_ptr(), sptr)
+        torch.cuda.synchronize()
+        del kd, vd
+
     def step(t):
-        hg.hetegen_decode_step(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, sptr)
+        if P > 0:
+            hg.hetegen_decode_step_kv(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, P + t, sptr)
+        else:
+            hg.hetegen_decode_step(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, sptr)
 
     refined = None
     if args.alpha_bench and streamed:
@@ -271,6 +291,9 @@ def main():
         desc = "all linears in %s host memory, streamed + CPU share" % ("pageable" if args.pageable else "pinned")
     if placement != "all":
         desc += ", %s" % ("planner alpha" if args.alpha is None else "alpha=%g" % args.alpha)
+    if P > 0:
+        desc += ", attention over a %d-position KV cache (positions %d-%d decoded)" % (P, P + args.warmup,
+                                                                                      P + nstep - 1)
     result = {
         "metric": "decode latency ms/token + effective weight GB/s (frac of HBM/PCIe roofline)",
         "value": round(gbps, 2),
@@ -297,7 +320,14 @@ def main():
 
     exec_mode = {1: "persistent", 2: "graph", 3: "eager"}.get(hg.hetegen_model_last_exec(model), "?")
     result["config"]["exec"] = exec_mode
-    if not streamed:
+    if P > 0:
+        # keys and values read per step (positions 0..pos of every layer), mean over the timed steps
+        kv_b = np.mean([2 * L * B * (P + t + 1) * H * 2 for t in range(args.warmup, nstep)])
+        result["kv"] = {"context": P, "head_dim": 128, "kv_bytes_per_step": int(kv_b),
+                        "tokens_per_s": round(B * 1e3 / ms_step, 2),
+                        "weight_plus_kv_GBps": round((wbytes + kv_b) / (ms_step * 1e-3) / 1e9, 1)}
+        log("kv: %s" % json.dumps(result["kv"]))
+    if not streamed and P == 0:
         # dominant kernel: every dispatch of the timed region is the GEMV kernel (LayerNorm,
         # value slice, ReLU and residual are fused into it): one persistent step kernel per
         # step, or one GEMV launch per linear; its average launch time is the event-timed
@@ -316,7 +346,7 @@ def main():
                                                            "gemv_kernel", "BF16" if dt == 1 else "F16", B),
                               "avg_launch_us": round(avg_us, 3), "bytes_per_launch": round(bytes_per_launch),
                               "launches_per_step": launches}
-    else:
+    elif streamed:
         # heterogeneous figures: link and CPU rates, the ideal rate of Eq. 4, busy fractions
         sb = sum(shp[i][0] * shp[i][1] * 2 for i in streamed)
         n_cpu = [min(shp[i][0], int(np.floor(alpha[i] * shp[i][0] + 0.5))) for i in range(4 * L)]

@@ -289,6 +289,37 @@ HETEGEN_API hetegen_status hetegen_model_get_alpha(const hetegen_model* model, d
  * heterogeneous.  Zeros before such a step. */
 HETEGEN_API hetegen_status hetegen_model_linear_ms(const hetegen_model* model, double* ms_out);
 
+/* ---- KV cache and attention over it (Sec. 2.1, Eq. 1) ----
+ * hetegen_decode_step uses the attention of an empty cache (the value slice).
+ * With a KV cache the model runs full decode steps: at position pos each layer's
+ * attention appends the new token's key and value (qkv[:, H:2H], qkv[:, 2H:3H])
+ * to the cache at pos and attends its query qkv[:, 0:H] to positions [0, pos]:
+ *   per head h (head_dim D, H / D heads): s_j = q_h . K_j,h / sqrt(D),
+ *   a_h = sum_j softmax(s)_j V_j,h, rounded to the model dtype (RNE);
+ * a [B, H] then feeds the out linear.  Softmax in binary32 with exact max
+ * subtraction; every sequence of the batch is at the same position. */
+
+/* Give the model a cache of max_seq positions, 1 <= max_seq <= 16384 (device
+ * memory: 2 * L * max_batch * max_seq * H * 2 bytes, zeroed) and the attention's
+ * scratch.  head_dim: 64 or 128, dividing H.  Once per model. */
+HETEGEN_API hetegen_status hetegen_model_kv_create(hetegen_ctx* ctx, hetegen_model* model, int max_seq, int head_dim);
+
+/* Copy positions [pos0, pos0 + n) of layer `layer` for sequences [0, B) between the
+ * cache and device buffers k_dev, v_dev of layout [B, n, H] (model dtype, one row per
+ * token, heads concatenated as in the qkv output); enqueued on `stream`.  Writing
+ * stands in for a prefill; reading is for inspection. */
+HETEGEN_API hetegen_status hetegen_model_kv_write(hetegen_ctx* ctx, hetegen_model* model, int layer, int B, int pos0,
+                                                  int n, const void* k_dev, const void* v_dev, void* stream);
+HETEGEN_API hetegen_status hetegen_model_kv_read(hetegen_ctx* ctx, hetegen_model* model, int layer, int B, int pos0,
+                                                 int n, void* k_dev, void* v_dev, void* stream);
+
+/* One full decode step of the token at position pos (0 <= pos < max_seq; the cache
+ * holds positions [0, pos) of every layer): as hetegen_decode_step with the
+ * attention above; runs linear by linear (HETEGEN_EXEC_EAGER).  Heterogeneous and
+ * streamed linears work as in hetegen_decode_step. */
+HETEGEN_API hetegen_status hetegen_decode_step_kv(hetegen_ctx* ctx, hetegen_model* model, const void* x_dev,
+                                                  void* out_dev, int B, int pos, void* stream);
+
 /* Optional trace of every linear's input and output (model dtype), for
  * teacher-forced checks.  Linear i writes its input [B, K_i] and then its output
  * [B, N_i] (after the fused ReLU or residual sum), packed in order of i; the

@@ -10,6 +10,10 @@ decoders and its own loops).
   (HeteGen Sec. 3.1, Fig. 3a, Eq. 2; Sec. 4.2, Fig. 5a: the partitioned module
   computes the same output as the unpartitioned one).
 - ``planner``: the computation-distribution law (Sec. 3.2, Eq. 4-7; Eq. 8-9).
+- ``attention``: decode attention over a KV cache and the decode step with it
+  (Sec. 2.1, Eq. 1).
+- ``alpha_bench``, ``scheduler``: the alpha benchmark's fit and solve (Sec. 4.4)
+  and the module scheduler (Sec. 4.5, Eq. 13).
 - ``decode_step``: the stack of decoder-layer linears with the GPU-side glue
   (Sec. 4.2 keeps non-linear modules on the GPU; glue defined in the design
   notes: pre-LayerNorm, V slice of a one-position attention, ReLU, residual).

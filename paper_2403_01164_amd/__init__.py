@@ -80,6 +80,10 @@ _SIGS = {
     "hetegen_alpha_minimize": ([ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d, ctypes.POINTER(_d)], _i),
     "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_linear_ms": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_model_kv_create": ([_vp, _vp, _i, _i], _i),
+    "hetegen_model_kv_write": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
+    "hetegen_model_kv_read": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
+    "hetegen_decode_step_kv": ([_vp, _vp, _vp, _vp, _i, _i, _vp], _i),
     "hetegen_module_schedule": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_i), _i, _d,
                                  ctypes.POINTER(_i), ctypes.POINTER(_d)], _i),
     "hetegen_model_last_exec": ([_vp], _i),
@@ -299,3 +303,19 @@ def host_view(ptr, shape, np_dtype):
     count = int(np.prod(shape))
     buf = (ctypes.c_char * (count * np.dtype(np_dtype).itemsize)).from_address(ptr)
     return np.frombuffer(buf, dtype=np_dtype, count=count).reshape(shape)
+
+
+def hetegen_model_kv_create(ctx, model, max_seq, head_dim):
+    _check(_lib.hetegen_model_kv_create(ctx, model, max_seq, head_dim), ctx)
+
+
+def hetegen_model_kv_write(ctx, model, layer, B, pos0, n, k_dev, v_dev, stream=0):
+    _check(_lib.hetegen_model_kv_write(ctx, model, layer, B, pos0, n, k_dev, v_dev, stream or None), ctx)
+
+
+def hetegen_model_kv_read(ctx, model, layer, B, pos0, n, k_dev, v_dev, stream=0):
+    _check(_lib.hetegen_model_kv_read(ctx, model, layer, B, pos0, n, k_dev, v_dev, stream or None), ctx)
+
+
+def hetegen_decode_step_kv(ctx, model, x_dev, out_dev, B, pos, stream=0):
+    _check(_lib.hetegen_decode_step_kv(ctx, model, x_dev, out_dev, B, pos, stream or None), ctx)

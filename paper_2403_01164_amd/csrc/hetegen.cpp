@@ -36,6 +36,7 @@
 #include <vector>
 
 #include "../../include/hetegen.h"
+#include "attention.h"
 #include "cpu_share.h"
 #include "kernels.h"
 
@@ -234,6 +235,13 @@ struct hetegen_model {
   uint32_t spin_limit = 0;       // 0: the kernel's default
   int exec_mode = HETEGEN_EXEC_AUTO;
   int last_exec = 0;
+  // KV cache of attention steps (Sec. 2.1, Eq. 1): K then V of every layer, each
+  // [max_batch][heads][kv_seq][head_dim] in the model dtype
+  int kv_seq = 0, head_dim = 0, heads = 0, kv_chunks = 0;
+  void* kv = nullptr;
+  float* kv_part = nullptr;    // chunk partials of the attention merge
+  uint32_t* kv_cnt = nullptr;  // arrival counters of the merge, zero between launches
+  void* abuf = nullptr;        // attention output [max_batch, H]
 };
 
 namespace {
@@ -1270,14 +1278,46 @@ void model_free(hetegen_model* m) {
   if (m->err_host) (void)hipHostFree(m->err_host);
   if (m->arena) (void)hipFree(m->arena);
   if (m->act) (void)hipFree(m->act);
+  if (m->kv) (void)hipFree(m->kv);
+  if (m->kv_part) (void)hipFree(m->kv_part);
+  if (m->kv_cnt) (void)hipFree(m->kv_cnt);
+  if (m->abuf) (void)hipFree(m->abuf);
   (void)hipGetLastError();
   delete m;
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+size_t kv_layer_elems(const hetegen_model* m) {
+  return (size_t)m->max_batch * m->heads * m->kv_seq * m->head_dim;
+}
+
+// Attention of layer l at position pos over the cache: reads q | k | v from the
+// qkv buffer, appends k and v at pos, writes the output to abuf.
+hetegen_status run_attention(hetegen_ctx* ctx, hetegen_model* m, int l, int B, int pos, hipStream_t st) {
+  hg::AttnParams a{};
+  const size_t per = kv_layer_elems(m);
+  a.qkv = m->qkv;
+  a.ldq = 3LL * m->H;
+  a.kc = (uint16_t*)m->kv + (size_t)(2 * l) * per;
+  a.vc = (uint16_t*)m->kv + (size_t)(2 * l + 1) * per;
+  a.out = m->abuf;
+  a.ldo = m->H;
+  a.part = m->kv_part;
+  a.cnt = m->kv_cnt;
+  a.heads = m->heads;
+  a.head_dim = m->head_dim;
+  a.max_seq = m->kv_seq;
+  a.max_chunks = m->kv_chunks;
+  a.pos = pos;
+  HIPCHK(ctx, hg::launch_attention(a, m->dtype, B, st));
+  return HETEGEN_OK;
+}
+
+// One step.  pos < 0: the attention of every layer is that of an empty cache (the
+// value slice of qkv); pos >= 0: attention over the KV cache at position pos.
 hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
-                            hipStream_t st) {
+                            hipStream_t st, int pos = -1) {
   const int H = m->H, F = m->F;
   // plan every streamed chunk of the step up front so the copy stream can run
   // ahead across linears and layers, bounded by the ring
@@ -1315,8 +1355,14 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
           j.x = xl; j.ldx = H; j.ln = 1;
           j.y = m->qkv; j.ldy = 3 * H; j.epi = hg::EPI_NONE;
           break;
-        case 1:  // x = x + (V Wout^T + b), V = qkv[:, 2H:3H]
-          j.x = (const char*)m->qkv + (size_t)2 * H * 2; j.ldx = 3 * H; j.ln = 0;
+        case 1:  // x = x + (A Wout^T + b): A = attention over the cache, or V = qkv[:, 2H:3H]
+          if (pos >= 0) {
+            TRY(run_attention(ctx, m, l, B, pos, st));
+            j.x = m->abuf; j.ldx = H;
+          } else {
+            j.x = (const char*)m->qkv + (size_t)2 * H * 2; j.ldx = 3 * H;
+          }
+          j.ln = 0;
           j.y = m->xbuf; j.ldy = H; j.epi = hg::EPI_RESID; j.resid = xl; j.ldr = H;
           break;
         case 2:  // f = ReLU(LN(x) Wfc1^T + b)
@@ -1761,6 +1807,115 @@ hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* m, const voi
   }
   m->last_exec = HETEGEN_EXEC_EAGER;
   hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, st);
+  if (s != HETEGEN_OK) {
+    reset_pipeline(ctx);
+    return s;
+  }
+  return finish_call(ctx, t0);
+}
+
+// ---- KV cache and attention steps (Sec. 2.1, Eq. 1) ----
+hetegen_status hetegen_model_kv_create(hetegen_ctx* ctx, hetegen_model* m, int max_seq, int head_dim) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->err.clear();
+  if (!m || max_seq < 1 || max_seq > hg::attn_max_positions())
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv_create: max_seq %d outside [1, %d]", max_seq,
+                hg::attn_max_positions());
+  if ((head_dim != 64 && head_dim != 128) || m->H % head_dim)
+    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "head_dim %d: 64 or 128, dividing H = %d", head_dim, m->H);
+  if (m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv_create: the model already has a KV cache");
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  const int chunk = hg::attn_chunk();
+  m->heads = m->H / head_dim;
+  m->head_dim = head_dim;
+  m->kv_seq = max_seq;
+  m->kv_chunks = (max_seq + chunk - 1) / chunk;
+  const size_t kv_bytes = 2 * (size_t)m->L * kv_layer_elems(m) * 2;
+  const size_t part_bytes = (size_t)m->max_batch * m->heads * m->kv_chunks * (head_dim + 2) * sizeof(float);
+  const size_t cnt_bytes = (size_t)m->max_batch * m->heads * sizeof(uint32_t);
+  if (hipMalloc(&m->kv, kv_bytes) != hipSuccess || hipMalloc((void**)&m->kv_part, part_bytes) != hipSuccess ||
+      hipMalloc((void**)&m->kv_cnt, cnt_bytes) != hipSuccess ||
+      hipMalloc(&m->abuf, (size_t)m->max_batch * m->H * 2) != hipSuccess) {
+    (void)hipGetLastError();
+    if (m->kv) (void)hipFree(m->kv);
+    if (m->kv_part) (void)hipFree(m->kv_part);
+    if (m->kv_cnt) (void)hipFree(m->kv_cnt);
+    if (m->abuf) (void)hipFree(m->abuf);
+    m->kv = nullptr;
+    m->kv_part = nullptr;
+    m->kv_cnt = nullptr;
+    m->abuf = nullptr;
+    m->kv_seq = 0;
+    return fail(ctx, HETEGEN_ERR_OOM, "KV cache of %zu bytes", kv_bytes);
+  }
+  HIPCHK(ctx, hipMemset(m->kv_cnt, 0, cnt_bytes));
+  HIPCHK(ctx, hipMemset(m->kv, 0, kv_bytes));
+  return HETEGEN_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Copy positions [pos0, pos0 + n) of layer l between the cache and token-major
+// device buffers [B, n, H] (to_cache: buffers -> cache).
+hetegen_status kv_copy(hetegen_ctx* ctx, hetegen_model* m, int l, int B, int pos0, int n, void* k, void* v,
+                       hipStream_t st, bool to_cache) {
+  if (!m || !m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "the model has no KV cache");
+  if (!k || !v || l < 0 || l >= m->L || B < 1 || B > m->max_batch || pos0 < 0 || n < 1 || pos0 + n > m->kv_seq)
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv copy: bad arguments");
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  const size_t per = kv_layer_elems(m), D = m->head_dim, row = D * 2, tok = (size_t)m->H * 2;
+  for (int which = 0; which < 2; ++which) {
+    char* cache = (char*)m->kv + (size_t)(2 * l + which) * per * 2;
+    char* buf = (char*)(which ? v : k);
+    for (int b = 0; b < B; ++b) {
+      for (int h = 0; h < m->heads; ++h) {
+        char* c = cache + (((size_t)b * m->heads + h) * m->kv_seq + pos0) * row;
+        char* t = buf + (size_t)b * n * tok + (size_t)h * row;
+        if (to_cache) HIPCHK(ctx, hipMemcpy2DAsync(c, row, t, tok, row, n, hipMemcpyDeviceToDevice, st));
+        else HIPCHK(ctx, hipMemcpy2DAsync(t, tok, c, row, row, n, hipMemcpyDeviceToDevice, st));
+      }
+    }
+  }
+  return HETEGEN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hetegen_status hetegen_model_kv_write(hetegen_ctx* ctx, hetegen_model* m, int layer, int B, int pos0, int n,
+                                      const void* k_dev, const void* v_dev, void* stream) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->err.clear();
+  return kv_copy(ctx, m, layer, B, pos0, n, const_cast<void*>(k_dev), const_cast<void*>(v_dev),
+                 (hipStream_t)stream, true);
+}
+
+hetegen_status hetegen_model_kv_read(hetegen_ctx* ctx, hetegen_model* m, int layer, int B, int pos0, int n,
+                                     void* k_dev, void* v_dev, void* stream) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->err.clear();
+  return kv_copy(ctx, m, layer, B, pos0, n, k_dev, v_dev, (hipStream_t)stream, false);
+}
+
+hetegen_status hetegen_decode_step_kv(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
+                                      int pos, void* stream) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  auto t0 = Clock::now();
+  ctx->err.clear();
+  if (!m || !x_dev || !out_dev || x_dev == out_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "decode_step: bad pointers");
+  if (!m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "the model has no KV cache (hetegen_model_kv_create)");
+  if (pos < 0 || pos >= m->kv_seq)
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "position %d outside the cache [0, %d)", pos, m->kv_seq);
+  if (B < 1 || B > m->max_batch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, m->max_batch);
+  if (!aligned16(x_dev) || !aligned16(out_dev)) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
+  if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  m->last_exec = HETEGEN_EXEC_EAGER;
+  hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, (hipStream_t)stream, pos);
   if (s != HETEGEN_OK) {
     reset_pipeline(ctx);
     return s;

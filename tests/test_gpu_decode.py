@@ -12,6 +12,7 @@ import pytest
 
 import oracle
 import synth
+from oracle import attention as oat
 from oracle import decode_step as ods
 from common import TOL, U_ACT, Pinned, np_from_dev, rel_err, torch_dev_from_np
 
@@ -74,7 +75,24 @@ class Model:
                 items.append((name, l, xin, yout))
         return items
 
-    def check_teacher_forced(self, x_bits, tr):
+    def step_kv(self, x_bits, pos, trace=False):
+        B = x_bits.shape[0]
+        x = torch_dev_from_np(x_bits)
+        out = torch.full((B, self.H), -1, dtype=torch.int16, device="cuda")
+        tr = None
+        if trace:
+            nb = hg.hetegen_model_trace_bytes(self.m, B)
+            tr = torch.full((nb // 2,), -1, dtype=torch.int16, device="cuda")
+            hg.hetegen_model_set_trace(self.m, tr.data_ptr(), nb)
+        s = torch.cuda.current_stream().cuda_stream
+        hg.hetegen_decode_step_kv(self.ctx, self.m, x.data_ptr(), out.data_ptr(), B, pos, s)
+        torch.cuda.synchronize()
+        if trace:
+            hg.hetegen_model_set_trace(self.m, 0, 0)
+        o = np_from_dev(out, np.uint16)
+        return (o, np_from_dev(tr, np.uint16)) if trace else o
+
+    def check_teacher_forced(self, x_bits, tr, attn=None):
         dt, H = self.dtype, self.H
         B = x_bits.shape[0]
         items = self.split_trace(tr, B)
@@ -90,7 +108,11 @@ class Model:
                 ref = lin
                 qkv_out = yout
             elif name == "out":
-                assert np.array_equal(xin, qkv_out[:, 2 * H:3 * H]), ("V slice", l)
+                if attn is None:
+                    assert np.array_equal(xin, qkv_out[:, 2 * H:3 * H]), ("V slice", l)
+                else:  # attention over the cache, from the traced q | k | v
+                    e = rel_err(oracle.decode(xin, dt), attn(l, qkv_out))
+                    assert e <= TOL + U_ACT[dt], ("attention", l, e)
                 ref = oracle.decode(x_l, dt).astype(np.float64) + lin
                 x_mid = yout
             elif name == "fc1":
@@ -318,5 +340,174 @@ def test_linear_times_reported_for_heterogeneous_steps(ctx):
         m.step(synth.normal((1, H), dtype, 0, synth.act_id(0)))
         ms = hg.hetegen_model_linear_ms(m.m, 4 * L)
         assert all(np.isfinite(v) and v > 0 for v in ms)
+    finally:
+        m.free()
+
+
+
+# ---- full decode steps with a KV cache (Sec. 2.1, Eq. 1) ----
+def _fill_cache(m, B, P, seed=0):
+    """Synthetic keys and values of positions [0, P) for every layer (stands in for a
+    prefill); returns the host copies per layer ([B, P, H] bits, or None)."""
+    kc, vc, keep = [], [], []
+    s = torch.cuda.current_stream().cuda_stream
+    for l in range(m.L):
+        if P == 0:
+            kc.append(None)
+            vc.append(None)
+            continue
+        k = synth.normal((B, P, m.H), m.dtype, seed, 5000 + 2 * l)
+        v = synth.normal((B, P, m.H), m.dtype, seed, 5001 + 2 * l)
+        kd, vd = torch_dev_from_np(k), torch_dev_from_np(v)
+        keep += [kd, vd]
+        hg.hetegen_model_kv_write(m.ctx, m.m, l, B, 0, P, kd.data_ptr(), vd.data_ptr(), s)
+        kc.append(k)
+        vc.append(v)
+    torch.cuda.synchronize()
+    return kc, vc
+
+
+def _attn_ref(m, kc, vc, head_dim):
+    H, dt = m.H, m.dtype
+
+    def ref(l, qkv):
+        K = oat.append(kc[l], qkv[:, H:2 * H])
+        V = oat.append(vc[l], qkv[:, 2 * H:3 * H])
+        return oat.attend(oracle.decode(qkv[:, :H], dt), oracle.decode(K, dt), oracle.decode(V, dt), head_dim)
+    return ref
+
+
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+@pytest.mark.parametrize("B", [1, 3])
+@pytest.mark.parametrize("P", [0, 1, 63, 64, 65, 150])
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_kv_step_teacher_forced(ctx, dtype, B, P, head_dim):
+    L, H, F = 2, 256, 512
+    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    try:
+        hg.hetegen_model_kv_create(ctx, m.m, 160, head_dim)
+        kc, vc = _fill_cache(m, B, P)
+        x = synth.normal((B, H), dtype, 0, synth.act_id(P))
+        out, tr = m.step_kv(x, P, trace=True)
+        last, _ = m.check_teacher_forced(x, tr, attn=_attn_ref(m, kc, vc, head_dim))
+        assert np.array_equal(out, last)
+    finally:
+        m.free()
+
+
+def test_kv_cache_appended_and_steps_chain(ctx):
+    dtype, L, H, F, B, P, D = synth.F16, 2, 256, 512, 2, 70, 64
+    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    try:
+        hg.hetegen_model_kv_create(ctx, m.m, 80, D)
+        kc, vc = _fill_cache(m, B, P)
+        layers = [{n: (m.W[4 * l + i].a, m.b[4 * l + i].a) for i, n in enumerate(NAMES)} for l in range(L)]
+        x = synth.normal((B, H), dtype, 0, synth.act_id(0))
+        ref_k, ref_v = list(kc), list(vc)
+        s = torch.cuda.current_stream().cuda_stream
+        for t in range(3):
+            pos = P + t
+            out, tr = m.step_kv(x, pos, trace=True)
+            m.check_teacher_forced(x, tr, attn=_attn_ref(m, kc, vc, D))
+            items = m.split_trace(tr, B)
+            for l in range(L):
+                qkv = items[4 * l][3]
+                kd = torch.zeros((B, 1, H), dtype=torch.int16, device="cuda")
+                vd = torch.zeros((B, 1, H), dtype=torch.int16, device="cuda")
+                hg.hetegen_model_kv_read(ctx, m.m, l, B, pos, 1, kd.data_ptr(), vd.data_ptr(), s)
+                torch.cuda.synchronize()
+                assert np.array_equal(np_from_dev(kd, np.uint16)[:, 0], qkv[:, H:2 * H]), (t, l)
+                assert np.array_equal(np_from_dev(vd, np.uint16)[:, 0], qkv[:, 2 * H:]), (t, l)
+                kc[l] = oat.append(kc[l], qkv[:, H:2 * H])
+                vc[l] = oat.append(vc[l], qkv[:, 2 * H:])
+            # the oracle's own chain from the same input and caches
+            want, _, ref_k, ref_v = oat.decode_step_kv(x, layers, H, dtype, ref_k, ref_v, D)
+            assert rel_err(oracle.decode(out, dtype), oracle.decode(want, dtype)) <= 2e-2, t
+            x = out
+    finally:
+        m.free()
+
+
+def test_kv_step_at_position_zero_equals_empty_cache_step(ctx):
+    dtype, L, H, F = synth.BF16, 2, 256, 512
+    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    try:
+        x = synth.normal((3, H), dtype, 0, synth.act_id(4))
+        want = m.step(x)
+        hg.hetegen_model_kv_create(ctx, m.m, 8, 128)
+        assert np.array_equal(m.step_kv(x, 0), want)
+    finally:
+        m.free()
+
+
+@pytest.mark.parametrize("mode", ["streamed", "hetero"])
+def test_kv_step_with_host_linears(ctx, mode):
+    dtype, L, H, F, B, P, D = synth.F16, 2, 256, 1024, 2, 100, 128
+    alpha = 0.0 if mode == "streamed" else [0.4, 0.3, 0.5, 0.2] * L
+    m = Model(ctx, L, H, F, dtype, alpha, 0)
+    try:
+        hg.hetegen_model_kv_create(ctx, m.m, 128, D)
+        kc, vc = _fill_cache(m, B, P)
+        x = synth.normal((B, H), dtype, 0, synth.act_id(9))
+        out, tr = m.step_kv(x, P, trace=True)
+        last, _ = m.check_teacher_forced(x, tr, attn=_attn_ref(m, kc, vc, D))
+        assert np.array_equal(out, last)
+    finally:
+        m.free()
+
+
+def test_kv_opt67b_shape_one_layer_context_512(ctx):
+    # OPT-6.7B layer shapes (32 heads of 128), a 512-position context
+    dtype, L, H, F, B, P, D = synth.F16, 1, 4096, 16384, 1, 512, 128
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
+    try:
+        hg.hetegen_model_kv_create(ctx, m.m, 576, D)
+        kc, vc = _fill_cache(m, B, P)
+        x = synth.normal((B, H), dtype, 0, synth.act_id(3))
+        out, tr = m.step_kv(x, P, trace=True)
+        m.check_teacher_forced(x, tr, attn=_attn_ref(m, kc, vc, D))
+    finally:
+        m.free()
+
+
+def test_kv_argument_errors(ctx):
+    dtype, L, H, F = synth.F16, 1, 256, 512
+    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    try:
+        x = torch.zeros((1, H), dtype=torch.int16, device="cuda")
+        o = torch.zeros((1, H), dtype=torch.int16, device="cuda")
+        s = torch.cuda.current_stream().cuda_stream
+        with pytest.raises(hg.HetegenError):  # no cache yet
+            hg.hetegen_decode_step_kv(ctx, m.m, x.data_ptr(), o.data_ptr(), 1, 0, s)
+        with pytest.raises(hg.HetegenError) as e:
+            hg.hetegen_model_kv_create(ctx, m.m, 16, 96)
+        assert e.value.status == hg.ERR_UNSUPPORTED
+        hg.hetegen_model_kv_create(ctx, m.m, 16, 64)
+        with pytest.raises(hg.HetegenError):  # only once
+            hg.hetegen_model_kv_create(ctx, m.m, 16, 64)
+        for pos in (-1, 16):
+            with pytest.raises(hg.HetegenError) as e:
+                hg.hetegen_decode_step_kv(ctx, m.m, x.data_ptr(), o.data_ptr(), 1, pos, s)
+            assert e.value.status == hg.ERR_INVALID_ARG
+        with pytest.raises(hg.HetegenError):  # past the cache end
+            hg.hetegen_model_kv_write(ctx, m.m, 0, 1, 10, 7, x.data_ptr(), x.data_ptr(), s)
+        hg.hetegen_decode_step_kv(ctx, m.m, x.data_ptr(), o.data_ptr(), 1, 15, s)
+        torch.cuda.synchronize()
+    finally:
+        m.free()
+
+
+@pytest.mark.parametrize("P", [1023, 1100])
+def test_kv_long_context_merge(ctx, P):
+    # more chunks than the merge requests at once (16 x 64 positions)
+    dtype, L, H, F, B, D = synth.BF16, 1, 256, 512, 2, 128
+    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    try:
+        hg.hetegen_model_kv_create(ctx, m.m, 1200, D)
+        kc, vc = _fill_cache(m, B, P)
+        x = synth.normal((B, H), dtype, 0, synth.act_id(P))
+        out, tr = m.step_kv(x, P, trace=True)
+        last, _ = m.check_teacher_forced(x, tr, attn=_attn_ref(m, kc, vc, D))
+        assert np.array_equal(out, last)
     finally:
         m.free()
