@@ -155,6 +155,16 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
 HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
                              int B, int reps, hetegen_bw* out);
 
+/* The CPU share alone (Sec. 3.2: the host cores compute the rows whose parameters
+ * stay in host memory), on the calling thread's OpenMP team, no device involved:
+ *   y[b * ldy + (j - r0)] = sum_k x[b * K + k] * W[j * K + k] + bias[j],
+ *   j in [r0, r1), b < B,
+ * x binary32 [B, K] host, W [N, K] host (pinned or pageable), bias host [N] or NULL,
+ * y binary32 host.  Binary32 accumulation, 16-bit weights widened exactly.
+ * threads <= 0: the OpenMP default.  B in [1, 8], K % 8 == 0, 0 <= r0 <= r1. */
+HETEGEN_API hetegen_status hetegen_cpu_linear(const float* x, int B, int K, const void* W_host, hetegen_dtype dtype,
+                                              const void* bias_host, int r0, int r1, float* y, int ldy, int threads);
+
 /* ---- Alpha benchmark (Sec. 4.4, Eq. 10-12) ----
  * The closed form assumes speeds proportional to bytes; measured CPU and transfer
  * times are not (contention for host memory, per-call overheads).  The alpha

@@ -80,6 +80,7 @@ _SIGS = {
     "hetegen_alpha_minimize": ([ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d, ctypes.POINTER(_d)], _i),
     "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_linear_ms": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_cpu_linear": ([_vp, _i, _i, _vp, _i, _vp, _i, _i, _vp, _i, _i], _i),
     "hetegen_model_kv_create": ([_vp, _vp, _i, _i], _i),
     "hetegen_model_kv_write": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
     "hetegen_model_kv_read": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
@@ -319,3 +320,16 @@ def hetegen_model_kv_read(ctx, model, layer, B, pos0, n, k_dev, v_dev, stream=0)
 
 def hetegen_decode_step_kv(ctx, model, x_dev, out_dev, B, pos, stream=0):
     _check(_lib.hetegen_decode_step_kv(ctx, model, x_dev, out_dev, B, pos, stream or None), ctx)
+
+
+def hetegen_cpu_linear(x_f32, W_ptr, bias_ptr, dtype, r0, r1, threads=0):
+    """CPU share of rows [r0, r1): x_f32 numpy float32 [B, K]; returns float32 [B, r1 - r0]."""
+    import numpy as np
+    x = np.ascontiguousarray(x_f32, dtype=np.float32)
+    B, K = x.shape
+    y = np.zeros((B, max(r1 - r0, 0)), np.float32)
+    rc = _lib.hetegen_cpu_linear(x.ctypes.data, B, K, W_ptr, dtype, bias_ptr or None, r0, r1, y.ctypes.data,
+                                 max(r1 - r0, 1), threads)
+    if rc != OK:
+        raise HetegenError(rc, "hetegen_cpu_linear")
+    return y

@@ -1089,6 +1089,15 @@ extern "C" hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void* 
   return HETEGEN_OK;
 }
 
+extern "C" hetegen_status hetegen_cpu_linear(const float* x, int B, int K, const void* W_host, hetegen_dtype dtype,
+                                             const void* bias_host, int r0, int r1, float* y, int ldy, int threads) {
+  if (!x || !W_host || !y || B < 1 || B > kMaxBatch || K < 8 || K % 8 || r0 < 0 || r1 < r0 || ldy < r1 - r0 ||
+      (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
+    return HETEGEN_ERR_INVALID_ARG;
+  hg::cpu_share(x, B, K, (const uint16_t*)W_host, dtype, (const uint16_t*)bias_host, r0, r1, y, ldy, threads);
+  return HETEGEN_OK;
+}
+
 // ---- heterogeneous module scheduler (Sec. 4.5, Eq. 13) ----
 extern "C" hetegen_status hetegen_module_schedule(const double* t_cpu, const double* mem, const int* layer, int n,
                                                   double budget_bytes, int* resident_out, double* used_out) {
