@@ -2,7 +2,7 @@
 // part of the module whose parameters stay in host memory, concurrently with the
 // transfer and GPU compute of the other part; Sec. 5 runs it on host cores).
 //
-// Each thread takes a contiguous block of output rows (static schedule), so it
+// Threads take runs of 32 consecutive output rows from a shared queue, so each
 // streams whole weight rows sequentially from DRAM.  A row block of R rows is
 // processed together so that each binary32 x vector loaded from cache is used R
 // times; 16-bit weights are widened to binary32 in registers (vcvtph2ps for fp16,
@@ -179,30 +179,34 @@ typedef void (*BlockFn)(const float*, int, const uint16_t*, const uint16_t*, int
 
 // Four rows per block (four weight streams per core; measured best at every batch
 // size, also at B = 8 where the 32 accumulators exceed the register file); the
-// AVX-512 loop is unrolled twice at B <= 2.
+// AVX-512 loop is unrolled twice at B <= 2.  Blocks [ba, bb) of 4 rows from r0; the
+// last block of the share may be partial.
 template <bool BF, int B>
-void run_rows(Isa isa, const float* x, int K, const uint16_t* W, const uint16_t* bias, int r0, int ra, int rb, float* y,
-              int ldy) {
+void run_blocks(Isa isa, const float* x, int K, const uint16_t* W, const uint16_t* bias, int r0, int r1, int ba,
+                int bb, float* y, int ldy) {
   constexpr int R = 4, UN = B <= 2 ? 2 : 1;
   BlockFn blk = isa == ISA_AVX512 ? block512<BF, B, R, UN> : block256<BF, B, R>;
   BlockFn one = isa == ISA_AVX512 ? block512<BF, B, 1, 1> : block256<BF, B, 1>;
-  int r = ra;
-  for (; r + R <= rb; r += R) blk(x, K, W, bias, r0, r, y, ldy);
-  for (; r < rb; ++r) one(x, K, W, bias, r0, r, y, ldy);
+  for (int i = ba; i < bb; ++i) {
+    const int r = r0 + R * i;
+    if (r + R <= r1) blk(x, K, W, bias, r0, r, y, ldy);
+    else
+      for (int q = r; q < r1; ++q) one(x, K, W, bias, r0, q, y, ldy);
+  }
 }
 
 template <bool BF>
-void run_rows_b(Isa isa, const float* x, int B, int K, const uint16_t* W, const uint16_t* bias, int r0, int ra, int rb,
-                float* y, int ldy) {
+void run_blocks_b(Isa isa, const float* x, int B, int K, const uint16_t* W, const uint16_t* bias, int r0, int r1,
+                  int ba, int bb, float* y, int ldy) {
   switch (B) {
-    case 1: run_rows<BF, 1>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    case 2: run_rows<BF, 2>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    case 3: run_rows<BF, 3>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    case 4: run_rows<BF, 4>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    case 5: run_rows<BF, 5>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    case 6: run_rows<BF, 6>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    case 7: run_rows<BF, 7>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
-    default: run_rows<BF, 8>(isa, x, K, W, bias, r0, ra, rb, y, ldy); break;
+    case 1: run_blocks<BF, 1>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 2: run_blocks<BF, 2>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 3: run_blocks<BF, 3>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 4: run_blocks<BF, 4>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 5: run_blocks<BF, 5>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 6: run_blocks<BF, 6>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 7: run_blocks<BF, 7>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    default: run_blocks<BF, 8>(isa, x, K, W, bias, r0, r1, ba, bb, y, ldy); break;
   }
 }
 
@@ -221,21 +225,23 @@ void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const
   int nt = (n + 7) / 8;
   if (nt > nt_max) nt = nt_max;
   if (nt < 1) nt = 1;
-#pragma omp parallel num_threads(nt)
-  {
-    const int t = omp_get_thread_num(), T = omp_get_num_threads();
-    // contiguous row ranges, aligned to 4 rows so blocks stay whole
-    const int blocks = (n + 3) / 4;
-    const int ba = (int)((int64_t)blocks * t / T), bb = (int)((int64_t)blocks * (t + 1) / T);
-    const int ra = r0 + 4 * ba, rb = r0 + (4 * bb < n ? 4 * bb : n);
-    if (ra < rb) {
-      if (g_isa == ISA_SCALAR)
-        rows_scalar(x, B, K, W, dtype, bias, r0, ra, rb, y, ldy);
-      else if (dtype == 1)
-        run_rows_b<true>(g_isa, x, B, K, W, bias, r0, ra, rb, y, ldy);
-      else
-        run_rows_b<false>(g_isa, x, B, K, W, bias, r0, ra, rb, y, ldy);
-    }
+  if (g_isa == ISA_SCALAR) {
+#pragma omp parallel for schedule(static) num_threads(nt)
+    for (int r = r0; r < r1; ++r) rows_scalar(x, B, K, W, dtype, bias, r0, r, r + 1, y, ldy);
+    return;
+  }
+  // blocks of 4 rows handed out 8 at a time (32 rows, long sequential streams): a
+  // core slowed by other work hands its remaining blocks to the others, which a
+  // static split cannot (measured +5-38 % at batch 1 on the 16-core host).  Every
+  // row is computed by one thread in the same order whatever the schedule.
+  const int blocks = (n + 3) / 4;
+  constexpr int kGrain = 8;
+  const int grains = (blocks + kGrain - 1) / kGrain;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
+  for (int g = 0; g < grains; ++g) {
+    const int ba = g * kGrain, bb = ba + kGrain < blocks ? ba + kGrain : blocks;
+    if (dtype == 1) run_blocks_b<true>(g_isa, x, B, K, W, bias, r0, r1, ba, bb, y, ldy);
+    else run_blocks_b<false>(g_isa, x, B, K, W, bias, r0, r1, ba, bb, y, ldy);
   }
 }
 
