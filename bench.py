@@ -199,18 +199,12 @@ def main():
     out = torch.empty((2, B, H), dtype=torch.int16, device="cuda")
 
     if placement == "sched":
-        # module scheduler (Sec. 4.5, Eq. 13): each module's benchmarked heterogeneous
-        # time (host critical-path time in steps with every linear heterogeneous at its
-        # planned split) against the HBM bytes of its resident copy
+        # module scheduler (Sec. 4.5, Eq. 13): T_CPU of each module is its CPU time at
+        # the planned split (CPU rows x K x 2 bytes over the probed CPU speed of its
+        # shape, Eq. 11 read off the distribution law), against the HBM bytes of its
+        # resident copy
         a_all = hg.hetegen_layer_plan([(n, k, dt, 0) for n, k in shp], bws)
-        mcal = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, a_all, [0] * (4 * L), max(B, 1))
-        t_het = [0.0] * (4 * L)
-        for t in range(3):
-            hg.hetegen_decode_step(ctx, mcal, xs[t % nstep].data_ptr(), out[0].data_ptr(), B, sptr)
-            if t > 0:
-                t_het = [a + v * 1e-3 / 2 for a, v in zip(t_het, hg.hetegen_model_linear_ms(mcal, 4 * L))]
-        torch.cuda.synchronize()
-        hg.hetegen_model_destroy(ctx, mcal)
+        t_het = [a_all[i] * n * k * 2 / bws[i][0] for i, (n, k) in enumerate(shp)]
         mem = [float(n * k * 2) for n, k in shp]
         budget = args.hbm_budget * 1e9 if args.hbm_budget is not None else sum(mem) / 2
         resident, used = hg.hetegen_module_schedule(t_het, mem, [i // 4 for i in range(4 * L)], budget)
