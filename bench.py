@@ -103,9 +103,9 @@ def main():
                     help="comma-separated CPU fractions for the streamed linears, each timed after the main "
                          "measurement (e.g. 0,0.1,0.2,0.3,0.4,0.5)")
     ap.add_argument("--sweep-steps", type=int, default=2)
-    ap.add_argument("--alpha-bench", action="store_true",
-                    help="refine the streamed linears' CPU fractions with the step-level alpha benchmark "
-                         "(Sec. 4.4) and time the step with both the closed-form and the refined fractions")
+    ap.add_argument("--no-alpha-bench", dest="alpha_bench", action="store_false",
+                    help="keep the closed-form CPU fractions (default for streamed linears: refine them with the "
+                         "step-level alpha benchmark, Sec. 4.4, and also time the closed-form fractions)")
     ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: OpenMP default)")
     ap.add_argument("--pageable", action="store_true",
                     help="weights in plain pageable host memory (transparent huge pages), streamed through the "
@@ -247,7 +247,7 @@ def main():
             hg.hetegen_decode_step(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, sptr)
 
     refined = None
-    if args.alpha_bench and streamed:
+    if args.alpha_bench and streamed and args.alpha is None:
         t0 = time.time()
         delta, crossed = hg.hetegen_model_alpha_benchmark(ctx, model, xs[0].data_ptr(), out[0].data_ptr(), B,
                                                           0.08, 0.02, 2, 2, hg.BENCH_WALL, sptr)

@@ -278,9 +278,11 @@ HETEGEN_API int hetegen_model_last_exec(const hetegen_model* model);
  *     hetegen_alpha_minimize).  Within a step the ring lets transfers run ahead
  *     across linears and the hand-offs and host-memory contention are not in either
  *     summed time, so the wall-time objective is the one that tracks latency.
- * reps timed steps per point (plus one warm-up).  The model keeps the refined
- * fractions; *delta_out receives the offset; *crossed is set for the crossing
- * objective.  Resident linears are unchanged. */
+ * When the solution is a bracket end (no crossing inside, or the time still falls
+ * at the end), the bracket is re-centred on it and measured again: at most three
+ * brackets in all.  reps timed steps per point (plus one warm-up).  The model keeps
+ * the refined fractions; *delta_out receives the total offset; *crossed is set for
+ * the crossing objective.  Resident linears are unchanged. */
 #define HETEGEN_BENCH_CROSSING 0
 #define HETEGEN_BENCH_WALL 1
 HETEGEN_API hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, hetegen_model* model, const void* x_dev,

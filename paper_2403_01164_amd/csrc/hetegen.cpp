@@ -1671,59 +1671,74 @@ hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, hetegen_model* m,
       if (!m->lin[i].resident) a[i] = std::min(1.0, std::max(0.0, base[i] + d));
     return hetegen_model_set_alpha(m, a.data());
   };
-  std::vector<double> ds, tc, tg, tw;
-  for (int i = 0;; ++i) {
-    const double d = -gamma + i * lambda;
-    if (d > gamma + 1e-9) break;
-    ds.push_back(std::min(d, gamma));
-  }
-  if ((int)ds.size() < degree + 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "too few points in the bracket");
   const bool was = ctx->profiling;
-  ctx->profiling = objective == HETEGEN_BENCH_CROSSING;
   TRY(flush_profile(ctx));
   const hetegen_profile saved = ctx->prof;
-  hetegen_status st = HETEGEN_OK;
   auto med = [](std::vector<double> v) {
     std::sort(v.begin(), v.end());
     return v[v.size() / 2];
   };
-  for (double d : ds) {
-    TRY(apply(d));
-    std::vector<double> c, g, w;
-    for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
-      ctx->prof = hetegen_profile{};
-      auto t0 = Clock::now();
-      st = hetegen_decode_step(ctx, m, x_dev, out_dev, B, stream);
-      if (st == HETEGEN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
-        st = fail(ctx, HETEGEN_ERR_HIP, "hipStreamSynchronize failed");
-      const double wall = ms_since(t0);
-      if (st == HETEGEN_OK) st = flush_profile(ctx);
-      if (st == HETEGEN_OK && r > 0) {
-        c.push_back(ctx->prof.cpu_ms);
-        g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
-        w.push_back(wall);
-      }
+  // One pass measures the bracket [center - gamma, center + gamma]; when its solution
+  // is a bracket end (the curves do not meet inside, or the time still falls there),
+  // the bracket is re-centred on that end and measured again, up to kPasses in all.
+  constexpr int kPasses = 3;
+  double center = 0.0, d_best = 0.0;
+  int cr = 0;
+  hetegen_status st = HETEGEN_OK;
+  for (int pass = 0; pass < kPasses && st == HETEGEN_OK; ++pass) {
+    std::vector<double> ds, tc, tg, tw;
+    for (int i = 0;; ++i) {
+      const double d = -gamma + i * lambda;
+      if (d > gamma + 1e-9) break;
+      ds.push_back(center + std::min(d, gamma));
     }
+    if ((int)ds.size() < degree + 1) {
+      st = fail(ctx, HETEGEN_ERR_INVALID_ARG, "too few points in the bracket");
+      break;
+    }
+    ctx->profiling = objective == HETEGEN_BENCH_CROSSING;
+    for (double d : ds) {
+      st = apply(d);
+      std::vector<double> c, g, w;
+      for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
+        ctx->prof = hetegen_profile{};
+        auto t0 = Clock::now();
+        st = hetegen_decode_step(ctx, m, x_dev, out_dev, B, stream);
+        if (st == HETEGEN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+          st = fail(ctx, HETEGEN_ERR_HIP, "hipStreamSynchronize failed");
+        const double wall = ms_since(t0);
+        if (st == HETEGEN_OK) st = flush_profile(ctx);
+        if (st == HETEGEN_OK && r > 0) {
+          c.push_back(ctx->prof.cpu_ms);
+          g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
+          w.push_back(wall);
+        }
+      }
+      if (st != HETEGEN_OK) break;
+      tc.push_back(med(c));
+      tg.push_back(med(g));
+      tw.push_back(med(w));
+    }
+    ctx->profiling = was;
     if (st != HETEGEN_OK) break;
-    tc.push_back(med(c));
-    tg.push_back(med(g));
-    tw.push_back(med(w));
+    const double lo = center - gamma, hi = center + gamma;
+    hetegen_status fs = objective == HETEGEN_BENCH_CROSSING
+                            ? hetegen_alpha_fit(ds.data(), tc.data(), tg.data(), (int)ds.size(), degree, lo, hi,
+                                                &d_best, &cr)
+                            : hetegen_alpha_minimize(ds.data(), tw.data(), (int)ds.size(), degree, lo, hi, &d_best);
+    if (fs != HETEGEN_OK) {
+      st = fail(ctx, fs, "alpha fit failed");
+      break;
+    }
+    const bool at_end = (d_best <= lo || d_best >= hi) && !(objective == HETEGEN_BENCH_CROSSING && cr);
+    if (!at_end) break;
+    center = d_best;
   }
   ctx->prof = saved;
   ctx->profiling = was;
   if (st != HETEGEN_OK) {
     (void)hetegen_model_set_alpha(m, base.data());
     return st;
-  }
-  double d_best = 0;
-  int cr = 0;
-  hetegen_status fs =
-      objective == HETEGEN_BENCH_CROSSING
-          ? hetegen_alpha_fit(ds.data(), tc.data(), tg.data(), (int)ds.size(), degree, -gamma, gamma, &d_best, &cr)
-          : hetegen_alpha_minimize(ds.data(), tw.data(), (int)ds.size(), degree, -gamma, gamma, &d_best);
-  if (fs != HETEGEN_OK) {
-    (void)hetegen_model_set_alpha(m, base.data());
-    return fail(ctx, fs, "alpha fit failed");
   }
   TRY(apply(d_best));
   *delta_out = d_best;

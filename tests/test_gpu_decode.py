@@ -322,7 +322,7 @@ def test_step_alpha_benchmark_refines_and_keeps_parity(ctx):
             hg.hetegen_model_set_alpha(m.m, [0.5] * 8)
             d, crossed = hg.hetegen_model_alpha_benchmark(ctx, m.m, xd.data_ptr(), od.data_ptr(), 1, 0.1, 0.05, 2, 1,
                                                           objective, torch.cuda.current_stream().cuda_stream)
-            assert -0.1 - 1e-9 <= d <= 0.1 + 1e-9
+            assert -0.3 - 1e-9 <= d <= 0.3 + 1e-9  # up to three brackets of +-0.1
             a = hg.hetegen_model_get_alpha(m.m, 4 * L)
             assert all(abs(v - (0.5 + d)) < 1e-12 for v in a)
         out, tr = m.step(x, trace=True)
