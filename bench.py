@@ -184,7 +184,7 @@ def main():
         for m in range(4):
             n, k = shp[last + m]
             t0 = time.time()
-            probe[NAMES[m]] = hg.hetegen_probe(ctx, W[last + m], n, k, dt, B, 3)
+            probe[NAMES[m]] = hg.hetegen_probe(ctx, W[last + m], n, k, dt, B, 3, hg.PROBE_CONCURRENT)
             p = probe[NAMES[m]]
             log("probe %s [%d,%d]: V_CPU %.1f GB/s, V_COM %.1f GB/s, V_GPU %.0f GB/s, V_PIN %.1f GB/s (%.1f s)" %
                 (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9,

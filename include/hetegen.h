@@ -148,12 +148,20 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
  * chunked host-to-device copy of W_host through the staging ring, and the GPU
  * GEMV over the staged chunks; each is the median of `reps` runs in weight bytes
  * per second (the CPU share after one untimed pass; host caches are flushed
- * before every CPU pass, as a step's weights always come from DRAM).  W_host is [N, K]; batch B.
+ * before every CPU pass, as a step's weights always come from DRAM).  W_host is
+ * [N, K]; batch B.
  * Pinned W_host: pin_Bps is set to 0 (no pinning).  Pageable W_host: pin_Bps is the
  * pin team's rate staging W_host into the pinned buffers, h2d_Bps the copy rate
- * from those buffers, each measured alone (the planner takes the smaller, Eq. 8). */
+ * from those buffers, each measured alone (the planner takes the smaller, Eq. 8).
+ * flags & HETEGEN_PROBE_CONCURRENT (pinned W_host): cpu_Bps and h2d_Bps are instead
+ * measured with the CPU share and the copies running at the same time, as they do
+ * in a heterogeneous linear (both read host memory; Sec. 4.4 notes that measured
+ * speeds depend on such system conditions): the copies of W_host run once while
+ * the CPU share repeats over W_host, on flushed caches each time; the CPU rate
+ * counts the passes that ended before the copies did. */
+#define HETEGEN_PROBE_CONCURRENT 1
 HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
-                             int B, int reps, hetegen_bw* out);
+                                         int B, int reps, int flags, hetegen_bw* out);
 
 /* The CPU share alone (Sec. 3.2: the host cores compute the rows whose parameters
  * stay in host memory), on the calling thread's OpenMP team, no device involved:

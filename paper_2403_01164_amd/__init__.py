@@ -66,7 +66,7 @@ _SIGS = {
     "hetegen_host_free": ([_vp, _vp], _i),
     "hetegen_linear": ([_vp, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _d, _vp, _i, _vp], _i),
     "hetegen_layer_plan": ([ctypes.POINTER(Shape), _i, ctypes.POINTER(Bw), _i, _i, ctypes.POINTER(_d)], _i),
-    "hetegen_probe": ([_vp, _vp, _i, _i, _i, _i, _i, ctypes.POINTER(Bw)], _i),
+    "hetegen_probe": ([_vp, _vp, _i, _i, _i, _i, _i, _i, ctypes.POINTER(Bw)], _i),
     "hetegen_alpha_fit": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d,
                            ctypes.POINTER(_d), ctypes.POINTER(_i)], _i),
     "hetegen_alpha_benchmark": ([_vp, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _vp, _d, _d, _d, _i, _i, _vp,
@@ -166,9 +166,12 @@ def hetegen_layer_plan(shapes, bws, flags=0):
     return [out[i] for i in range(n)]
 
 
-def hetegen_probe(ctx, W_host, N, K, dtype, B=1, reps=3):
+PROBE_CONCURRENT = 1
+
+
+def hetegen_probe(ctx, W_host, N, K, dtype, B=1, reps=3, flags=0):
     bw = Bw()
-    _check(_lib.hetegen_probe(ctx, W_host, N, K, dtype, B, reps, ctypes.byref(bw)), ctx)
+    _check(_lib.hetegen_probe(ctx, W_host, N, K, dtype, B, reps, flags, ctypes.byref(bw)), ctx)
     return {"cpu_Bps": bw.cpu_Bps, "h2d_Bps": bw.h2d_Bps, "hbm_gemv_Bps": bw.hbm_gemv_Bps, "pin_Bps": bw.pin_Bps}
 
 

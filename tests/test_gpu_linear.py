@@ -263,3 +263,15 @@ def test_alpha_benchmark_runs_in_bracket_and_keeps_parity(ctx):
         assert rel_err(p.run(a, False), p.ref()) <= TOL
     finally:
         p.free()
+
+
+def test_probe_concurrent_rates(ctx):
+    p = Problem(ctx, 1, 2048, 4096, synth.F16)
+    try:
+        alone = hg.hetegen_probe(ctx, p.W.ptr, p.N, p.K, p.dtype, 1, 2)
+        both = hg.hetegen_probe(ctx, p.W.ptr, p.N, p.K, p.dtype, 1, 2, hg.PROBE_CONCURRENT)
+        for bw in (alone, both):
+            assert all(np.isfinite(bw[f]) and bw[f] > 0 for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps"))
+            assert bw["pin_Bps"] == 0
+    finally:
+        p.free()
