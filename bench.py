@@ -332,14 +332,21 @@ def main():
         achieved = bytes_per_launch / (avg_us * 1e-6) / 1e9
         log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
             (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
+        tname = "BF16" if dt == 1 else "F16"
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
+        # achievable read bandwidth of this device (streaming read of 4 GiB), for information
+        read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
+        log("HBM streaming read: %.1f GB/s" % read_gbps)
         result["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                               "frac": round(achieved / HBM_PEAK_GBPS, 4),
                               "traffic": counter_traffic(args.model, dt, B),
-                              "kernel": "%s<%s,%d,...>" % ("step_kernel" if exec_mode == "persistent" else
-                                                           "gemv_kernel", "BF16" if dt == 1 else "F16", B),
+                              "kernel": ("step_kernel<%s,%d,...>" % (tname, B) if exec_mode == "persistent" else
+                                         "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4> (out, fc2)" %
+                                         (tname, tname) if B == 1 else "gemv_kernel<%s,%d,...>" % (tname, B)),
                               "avg_launch_us": round(avg_us, 3), "bytes_per_launch": round(bytes_per_launch),
-                              "launches_per_step": launches}
+                              "launches_per_step": launches,
+                              "hbm_read_achievable_GBps": round(read_gbps, 1),
+                              "frac_of_achievable": round(achieved / read_gbps, 4)}
     elif streamed:
         # heterogeneous figures: link and CPU rates, the ideal rate of Eq. 4, busy fractions
         sb = sum(shp[i][0] * shp[i][1] * 2 for i in streamed)
@@ -427,7 +434,7 @@ def main():
         done_bytes, t_cpu, n_lin = 0, 0.0, 0
         xb = {k: synth.normal((B, k), dt, 0, 99) for k in (H, F)}
         ybuf = {}
-        while t_cpu < budget_s and n_lin < 4 * len(shp):
+        while t_cpu < budget_s and n_lin < 64 * len(shp):
             i = n_lin % len(shp)
             n, k = shp[i]
             y = ybuf.setdefault(n, np.empty((B, n), np.float32))

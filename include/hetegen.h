@@ -163,6 +163,12 @@ HETEGEN_API hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n
 HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype,
                                          int B, int reps, int flags, hetegen_bw* out);
 
+/* Achievable HBM read bandwidth: a streaming read of `bytes` (>= 1 MiB, a multiple
+ * of 16) of device memory with 16-byte non-temporal loads (those of the GEMV), four
+ * workgroups per CU; *Bps_out = bytes / median time of `reps` runs.  The
+ * denominator the resident GEMV is compared with next to the nominal HBM peak. */
+HETEGEN_API hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out);
+
 /* The CPU share alone (Sec. 3.2: the host cores compute the rows whose parameters
  * stay in host memory), on the calling thread's OpenMP team, no device involved:
  *   y[b * ldy + (j - r0)] = sum_k x[b * K + k] * W[j * K + k] + bias[j],

@@ -81,6 +81,7 @@ _SIGS = {
     "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_linear_ms": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_cpu_linear": ([_vp, _i, _i, _vp, _i, _vp, _i, _i, _vp, _i, _i], _i),
+    "hetegen_probe_hbm": ([_vp, _sz, _i, ctypes.POINTER(_d)], _i),
     "hetegen_model_kv_create": ([_vp, _vp, _i, _i], _i),
     "hetegen_model_kv_write": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
     "hetegen_model_kv_read": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
@@ -336,3 +337,10 @@ def hetegen_cpu_linear(x_f32, W_ptr, bias_ptr, dtype, r0, r1, threads=0):
     if rc != OK:
         raise HetegenError(rc, "hetegen_cpu_linear")
     return y
+
+
+def hetegen_probe_hbm(ctx, nbytes, reps=5):
+    """Achievable HBM read bandwidth in bytes/s."""
+    out = _d()
+    _check(_lib.hetegen_probe_hbm(ctx, nbytes, reps, ctypes.byref(out)), ctx)
+    return out.value

@@ -38,6 +38,7 @@
 #include "../../include/hetegen.h"
 #include "attention.h"
 #include "cpu_share.h"
+#include "hbm_probe.h"
 #include "kernels.h"
 
 namespace {
@@ -1312,6 +1313,50 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
   out->h2d_Bps = wbytes / median(cm.empty() ? tm : cm);
   out->hbm_gemv_Bps = wbytes / median(tg);
   out->pin_Bps = pageable ? wbytes / median(tp) : 0;
+  return HETEGEN_OK;
+}
+
+// ---- achievable HBM read bandwidth ----
+extern "C" hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->err.clear();
+  if (!Bps_out || reps < 1 || bytes < ((size_t)1 << 20) || (bytes & 15))
+    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe_hbm: bad arguments");
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  void* buf = nullptr;
+  uint32_t* sink = nullptr;
+  if (hipMalloc(&buf, bytes) != hipSuccess || hipMalloc((void**)&sink, 256) != hipSuccess) {
+    (void)hipGetLastError();
+    if (buf) (void)hipFree(buf);
+    return fail(ctx, HETEGEN_ERR_OOM, "probe buffer of %zu bytes", bytes);
+  }
+  hipEvent_t a = nullptr, b = nullptr;
+  hetegen_status st = HETEGEN_OK;
+  std::vector<double> t;
+  int ncu = 0;
+  if (hipMemset(buf, 0x11, bytes) != hipSuccess || hipEventCreate(&a) != hipSuccess ||
+      hipEventCreate(&b) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess)
+    st = fail(ctx, HETEGEN_ERR_HIP, "probe setup failed");
+  for (int r = 0; st == HETEGEN_OK && r <= reps; ++r) {  // the first run warms up
+    float ms = 0;
+    if (hipEventRecord(a, ctx->capture_stream) != hipSuccess ||
+        hg::launch_read(buf, bytes, sink, 4 * std::max(ncu, 1), ctx->capture_stream) != hipSuccess ||
+        hipEventRecord(b, ctx->capture_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess ||
+        hipEventElapsedTime(&ms, a, b) != hipSuccess) {
+      st = fail(ctx, HETEGEN_ERR_HIP, "probe read kernel failed");
+      break;
+    }
+    if (r > 0) t.push_back(ms * 1e-3);
+  }
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  (void)hipFree(buf);
+  (void)hipFree(sink);
+  (void)hipGetLastError();
+  if (st != HETEGEN_OK) return st;
+  std::sort(t.begin(), t.end());
+  *Bps_out = (double)bytes / t[t.size() / 2];
   return HETEGEN_OK;
 }
 

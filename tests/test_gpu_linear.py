@@ -275,3 +275,10 @@ def test_probe_concurrent_rates(ctx):
             assert bw["pin_Bps"] == 0
     finally:
         p.free()
+
+
+def test_probe_hbm_read_bandwidth(ctx):
+    bps = hg.hetegen_probe_hbm(ctx, 256 << 20, 3)
+    assert 5e11 < bps < 9e12  # between a slow link and above the nominal 8 TB/s peak
+    with pytest.raises(hg.HetegenError):
+        hg.hetegen_probe_hbm(ctx, 1000, 3)
