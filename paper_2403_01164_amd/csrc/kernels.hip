@@ -183,11 +183,20 @@ template <class T>
 __device__ __forceinline__ uint4 normalize8(const uint4& v, float mean, float rstd) {
   float f[8];
   unpack8<T>(v, f);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    f[e] = (f[e] - mean) * rstd;
+    // the binary32 value is materialised before it is rounded to the activation type:
+    // otherwise instruction selection may fold the scaling into a mixed-precision
+    // multiply-add that rounds once to 16 bits, and results at ties would depend on
+    // the surrounding code (the kernels that fuse this must agree bit for bit)
+    asm volatile("" : "+v"(f[e]));
+  }
   uint4 o;
-  o.x = pack2<T>((f[0] - mean) * rstd, (f[1] - mean) * rstd);
-  o.y = pack2<T>((f[2] - mean) * rstd, (f[3] - mean) * rstd);
-  o.z = pack2<T>((f[4] - mean) * rstd, (f[5] - mean) * rstd);
-  o.w = pack2<T>((f[6] - mean) * rstd, (f[7] - mean) * rstd);
+  o.x = pack2<T>(f[0], f[1]);
+  o.y = pack2<T>(f[2], f[3]);
+  o.z = pack2<T>(f[4], f[5]);
+  o.w = pack2<T>(f[6], f[7]);
   return o;
 }
 
@@ -198,10 +207,20 @@ __device__ __forceinline__ float apply_epi(float v, int epi, float resid) {
   return v;
 }
 
+// A binary32 result rounded to the activation type.  The value is materialised first
+// so that it is rounded once from binary32 in every kernel (instruction selection
+// could otherwise fold the last add into a mixed-precision operation that rounds
+// straight to 16 bits, which differs at ties).
+template <class T>
+__device__ __forceinline__ uint16_t round_act(float v) {
+  asm volatile("" : "+v"(v));
+  return T::from_f32(v);
+}
+
 template <class T>
 __device__ __forceinline__ void store_y(void* y, long long i, int y_f32, float v) {
   if (y_f32) ((float*)y)[i] = v;
-  else ((uint16_t*)y)[i] = T::from_f32(v);
+  else ((uint16_t*)y)[i] = round_act<T>(v);
 }
 
 // ---------------------------------------------------------------------------
@@ -242,7 +261,7 @@ __device__ __forceinline__ void store_y_c(void* yrow, uint32_t n, uint32_t i, in
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc(yrow, n * 4), (int)(i * 4), 0,
                                             kCoherent);
     else
-      __builtin_amdgcn_raw_buffer_store_b16(T::from_f32(v), rsrc(yrow, n * 2), (int)(i * 2), 0, kCoherent);
+      __builtin_amdgcn_raw_buffer_store_b16(round_act<T>(v), rsrc(yrow, n * 2), (int)(i * 2), 0, kCoherent);
     return;
   }
   store_y<T>(yrow, i, y_f32, v);
@@ -482,6 +501,113 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
     compute(t + 1, fb);
   } else if (t < ntask) {
     compute(t, fa);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Batch-1 GEMV with a fused LayerNorm for K = 512 * NC (NC <= 8): every wavefront
+// loads the whole input row into registers (lane l holds the 16-byte chunks
+// l + 64u, exactly the chunks it multiplies in every row), normalises it there and
+// keeps it for all its rows: no LDS staging and no workgroup barrier.  The
+// statistics are summed in the order of ln_stats and the products in the order of
+// gemv_block, so the result is bit-identical to the workgroup kernels.
+// ---------------------------------------------------------------------------
+template <class T, int NC>
+__device__ __forceinline__ void ln_stats_wave(const uint4 (&xv)[NC], int K, float& mean, float& rstd) {
+  // "thread" t = 64 w + l of ln_stats sums chunks t + 256 i, i.e. chunks u = w + 4 i of lane l
+  float part[kWaves];
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    float s = 0.f;
+#pragma unroll
+    for (int u = w; u < NC; u += kWaves) {
+      float f[8];
+      unpack8<T>(xv[u], f);
+      s += ((f[0] + f[1]) + (f[2] + f[3])) + ((f[4] + f[5]) + (f[6] + f[7]));
+    }
+    part[w] = wave_sum(s);
+  }
+  mean = ((part[0] + part[1]) + (part[2] + part[3])) / (float)K;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    float s = 0.f;
+#pragma unroll
+    for (int u = w; u < NC; u += kWaves) {
+      float f[8];
+      unpack8<T>(xv[u], f);
+      float acc = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float d = f[e] - mean;
+        acc += d * d;
+      }
+      s += acc;
+    }
+    part[w] = wave_sum(s);
+  }
+  const float var = ((part[0] + part[1]) + (part[2] + part[3])) / (float)K;
+  rstd = 1.0f / sqrtf(var + kLnEps);
+}
+
+template <class T, int NC>
+__global__ __launch_bounds__(kThreads) void gemv_ln1_kernel(GemvParams p) {
+  __shared__ float sbias[kWaves][kX1MaxRows], sres[kWaves][kX1MaxRows];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int K = p.K, rpw = p.rpw;  // K == 512 * NC (launcher)
+  const int row_begin = blockIdx.x * rpw;
+  const int nrows = min(rpw, p.rows - row_begin);  // >= 1: the grid covers rows exactly
+  const int my_rg = nrows > wave ? (nrows - wave + kWaves - 1) / kWaves : 0;  // <= kX1MaxRows (launcher)
+  const uint16_t* W = (const uint16_t*)p.W;
+  const uint16_t* bias = (const uint16_t*)p.bias;
+  const uint16_t* res = (const uint16_t*)p.resid;
+  float bj = 0.f, rj = 0.f;
+  if (lane < my_rg) {
+    const int row = row_begin + wave + lane * kWaves;
+    if (bias) bj = T::to_f32(gmem(bias)[row]);
+    if (p.epi == EPI_RESID) rj = T::to_f32(gmem(res)[row]);
+  }
+  auto load = [&](int j, uint4 (&w)[NC]) {
+    const uint4* wr = (const uint4*)(W + (long long)(row_begin + wave + j * kWaves) * K);
+#pragma unroll
+    for (int u = 0; u < NC; ++u) w[u] = load_stream(wr + lane + 64 * u);
+  };
+  uint4 wa[NC], wb[NC], xn[NC];
+  if (my_rg > 0) load(0, wa);
+  const uint4* x = (const uint4*)p.x;
+#pragma unroll
+  for (int u = 0; u < NC; ++u) xn[u] = load_g16(x + lane + 64 * u);
+  if (lane < my_rg) {
+    sbias[wave][lane] = bj;
+    sres[wave][lane] = rj;
+  }
+  float mean, rstd;
+  ln_stats_wave<T, NC>(xn, K, mean, rstd);
+#pragma unroll
+  for (int u = 0; u < NC; ++u) xn[u] = normalize8<T>(xn[u], mean, rstd);
+  if (p.h_out && blockIdx.x == 0 && wave == 0)
+#pragma unroll
+    for (int u = 0; u < NC; ++u) *(uint4*)((uint16_t*)p.h_out + (long long)(lane + 64 * u) * 8) = xn[u];
+  auto compute = [&](int j, const uint4 (&w)[NC]) {
+    float acc = 0.f;
+#pragma unroll
+    for (int u = 0; u < NC; ++u) acc = dot8<T>(w[u], xn[u], acc);
+    const float s = wave_sum(acc);
+    if (lane == 0)
+      store_y<T>(p.y, row_begin + wave + j * kWaves, p.y_f32, apply_epi(s + sbias[wave][j], p.epi, sres[wave][j]));
+  };
+  int j = 0;
+  for (; j + 2 < my_rg; j += 2) {
+    load(j + 1, wb);
+    compute(j, wa);
+    load(j + 2, wa);
+    compute(j + 1, wb);
+  }
+  if (j + 1 < my_rg) {
+    load(j + 1, wb);
+    compute(j, wa);
+    compute(j + 1, wb);
+  } else if (j < my_rg) {
+    compute(j, wa);
   }
 }
 
@@ -738,13 +864,17 @@ template <class T, int B>
 hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
   constexpr int R = Tile<B>::R, U = Tile<B>::U;
   const int cap = grid_cap > 0 ? grid_cap : kDefaultGridCap;
-  if (B == 1 && !p.ln) {
-    constexpr int U1 = 4;
+  const bool ln_regs = B == 1 && p.ln && (p.K == 512 || p.K == 1024 || p.K == 2048 || p.K == 4096);
+  if (B == 1 && (!p.ln || ln_regs)) {
     const long long units = (p.rows + kWaves - 1) / kWaves;
     const long long per = std::min<long long>((units + cap - 1) / cap, kX1MaxRows);
     p.rpw = (int)(per * kWaves);
     const int grid = (int)((p.rows + p.rpw - 1) / p.rpw);
-    hipLaunchKernelGGL((gemv_x1_kernel<T, U1>), dim3(grid), dim3(kThreads), 0, s, p);
+    if (!p.ln) hipLaunchKernelGGL((gemv_x1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
+    else if (p.K == 512) hipLaunchKernelGGL((gemv_ln1_kernel<T, 1>), dim3(grid), dim3(kThreads), 0, s, p);
+    else if (p.K == 1024) hipLaunchKernelGGL((gemv_ln1_kernel<T, 2>), dim3(grid), dim3(kThreads), 0, s, p);
+    else if (p.K == 2048) hipLaunchKernelGGL((gemv_ln1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL((gemv_ln1_kernel<T, 8>), dim3(grid), dim3(kThreads), 0, s, p);
     return hipGetLastError();
   }
   // contiguous row blocks of a multiple of R*kWaves rows, at most `cap` blocks
