@@ -847,16 +847,43 @@ __global__ __launch_bounds__(kThreads) void import_kernel(const float* __restric
 
 // Per-batch tiling: rows per wavefront R and 16-byte steps per task U (U*R loads in flight).
 template <int B> struct Tile;
+// (Measured on OPT-6.7B/13B shapes: one row per wavefront up to B = 4, two from B = 5.)
 template <> struct Tile<1> { static constexpr int R = 1, U = 8; };
-template <> struct Tile<2> { static constexpr int R = 2, U = 4; };
-template <> struct Tile<3> { static constexpr int R = 2, U = 4; };
-template <> struct Tile<4> { static constexpr int R = 2, U = 4; };
-template <> struct Tile<5> { static constexpr int R = 4, U = 2; };
-template <> struct Tile<6> { static constexpr int R = 4, U = 2; };
-template <> struct Tile<7> { static constexpr int R = 4, U = 2; };
-template <> struct Tile<8> { static constexpr int R = 4, U = 2; };
+template <> struct Tile<2> { static constexpr int R = 1, U = 8; };
+template <> struct Tile<3> { static constexpr int R = 1, U = 4; };
+template <> struct Tile<4> { static constexpr int R = 1, U = 4; };
+template <> struct Tile<5> { static constexpr int R = 2, U = 2; };
+template <> struct Tile<6> { static constexpr int R = 2, U = 2; };
+template <> struct Tile<7> { static constexpr int R = 2, U = 2; };
+template <> struct Tile<8> { static constexpr int R = 2, U = 2; };
 
-constexpr size_t kLdsMain = 65536 - 1024;  // dynamic LDS of the main kernel (x, bias, residual, outputs)
+constexpr size_t kLdsMain = 65536 - 1024;  // dynamic LDS of the persistent step (x, bias, residual, outputs)
+
+// LDS a workgroup of the per-linear main GEMV may use on this device (gfx950: 160 KiB
+// per CU, all of it addressable by one workgroup), less a margin for the static
+// arrays; and the LDS of one CU, which bounds the co-resident workgroups.
+struct LdsInfo {
+  size_t per_block = 65536, per_cu = 65536;
+  int cus = 1;
+};
+const LdsInfo& lds_info() {
+  static const LdsInfo info = [] {
+    LdsInfo i;
+    int dev = 0, blk = 0, cu = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&blk, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && blk > 0 && cu > 0 &&
+        n > 0) {
+      i.per_block = (size_t)blk;
+      i.per_cu = (size_t)cu;
+      i.cus = n;
+    }
+    (void)hipGetLastError();
+    return i;
+  }();
+  return info;
+}
 constexpr int kTiledLdsBudget = 32768;  // bytes of x per tile in the K-tiled kernel
 constexpr int kDefaultGridCap = 1024;
 
@@ -877,13 +904,31 @@ hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
     else hipLaunchKernelGGL((gemv_ln1_kernel<T, 8>), dim3(grid), dim3(kThreads), 0, s, p);
     return hipGetLastError();
   }
-  // contiguous row blocks of a multiple of R*kWaves rows, at most `cap` blocks
+  // contiguous row blocks of a multiple of R*kWaves rows, at most `cap` blocks; a block
+  // that needs much LDS also caps the grid at the workgroups that fit at once (more
+  // would run in a second round)
   const int unit = R * kWaves;
   const long long units = (p.rows + unit - 1) / unit;
-  const long long per = (units + cap - 1) / cap;
-  const int rpw = (int)(per * unit);
-  const size_t lds = (size_t)B * p.K * 2 + (size_t)(1 + 2 * B) * rpw * 4;  // gemv_lds_bytes
-  if (lds <= kLdsMain) {
+  const LdsInfo& li = lds_info();
+  const size_t lds_max = li.per_block - 1024;
+  auto block_lds = [&](int c) {
+    const long long per = (units + c - 1) / c;
+    return (size_t)B * p.K * 2 + (size_t)(1 + 2 * B) * (size_t)(per * unit) * 4;  // gemv_lds_bytes
+  };
+  int cap_b = cap;
+  const size_t lds0 = block_lds(cap_b);
+  if (lds0 <= lds_max) {
+    const long long fit = (long long)li.cus * (long long)std::max<size_t>(1, li.per_cu / lds0);
+    if (fit < cap_b && block_lds((int)std::max<long long>(1, fit)) <= lds_max)
+      cap_b = (int)std::max<long long>(1, fit);
+    const long long per = (units + cap_b - 1) / cap_b;
+    const int rpw = (int)(per * unit);
+    const size_t lds = block_lds(cap_b);
+    if (lds > 65536) {  // beyond the default dynamic LDS: opt in once per kernel
+      static const hipError_t opt = hipFuncSetAttribute((const void*)gemv_kernel<T, B, R, U>,
+                                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_max);
+      if (opt != hipSuccess) return opt;
+    }
     p.rpw = rpw;
     p.ktile = p.K;
     const int grid = (int)((p.rows + rpw - 1) / rpw);
