@@ -333,20 +333,35 @@ def main():
         log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
             (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
         tname = "BF16" if dt == 1 else "F16"
+        if exec_mode == "persistent":
+            kernel_label = "step_kernel<%s,%d,...>" % (tname, B)
+        elif B == 1:
+            kernel_label = ("gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4> (out, fc2)" % (tname, H // 512, tname)
+                            if H in (512, 1024, 2048, 4096) else
+                            "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4> (out, fc2)" % (tname, tname))
+        else:
+            # from batch 5 on the LayerNorm of qkv and fc1 is its own launch (counted in the
+            # time, not in the GEMV launches)
+            kernel_label = "gemv_kernel<%s,%d,...>%s" % (tname, B, " + layernorm_kernel" if B > 4 else "")
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
         read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
         log("HBM streaming read: %.1f GB/s" % read_gbps)
+        # the same weights read by plain streaming reads in the step's launches: the
+        # step's floor (launch ramp and drain included)
+        read_step_ms = hg.hetegen_model_read_ms(ctx, model, 5, sptr)
+        log("plain read of the step's weights in its %d launches: %.4f ms (%.1f GB/s)" %
+            (4 * L, read_step_ms, wbytes / (read_step_ms * 1e-3) / 1e9))
         result["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                               "frac": round(achieved / HBM_PEAK_GBPS, 4),
                               "traffic": counter_traffic(args.model, dt, B),
-                              "kernel": ("step_kernel<%s,%d,...>" % (tname, B) if exec_mode == "persistent" else
-                                         "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4> (out, fc2)" %
-                                         (tname, tname) if B == 1 else "gemv_kernel<%s,%d,...>" % (tname, B)),
+                              "kernel": kernel_label,
                               "avg_launch_us": round(avg_us, 3), "bytes_per_launch": round(bytes_per_launch),
                               "launches_per_step": launches,
                               "hbm_read_achievable_GBps": round(read_gbps, 1),
-                              "frac_of_achievable": round(achieved / read_gbps, 4)}
+                              "frac_of_achievable": round(achieved / read_gbps, 4),
+                              "read_same_launches_ms": round(read_step_ms, 5),
+                              "frac_of_read_same_launches": round(read_step_ms / ms_step, 4)}
     elif streamed:
         # heterogeneous figures: link and CPU rates, the ideal rate of Eq. 4, busy fractions
         sb = sum(shp[i][0] * shp[i][1] * 2 for i in streamed)

@@ -304,6 +304,17 @@ HETEGEN_API hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, heteg
                                                          int degree, int reps, int objective, void* stream,
                                                          double* delta_out, int* crossed);
 
+/* Read ceiling of the model's resident GPU rows: the rows [0, n_gpu) of every
+ * resident linear (its device copy, n_gpu * K elements) read in step order by the
+ * streaming read kernel of hetegen_probe_hbm, one launch per linear, on `stream`
+ * (a hipStream_t; NULL = the context's own stream).  *ms_out = median wall time of
+ * `reps` (>= 1) such passes after one warm-up pass.  A decode step over the same
+ * resident linears reads at least these bytes in at least these launches, so this
+ * bounds its time from below (launch ramp and drain included).  INVALID_ARG when
+ * the model has no resident GPU rows. */
+HETEGEN_API hetegen_status hetegen_model_read_ms(hetegen_ctx* ctx, const hetegen_model* model, int reps,
+                                                 void* stream, double* ms_out);
+
 /* Current CPU fraction of every linear (4L entries). */
 HETEGEN_API hetegen_status hetegen_model_get_alpha(const hetegen_model* model, double* alpha_out);
 

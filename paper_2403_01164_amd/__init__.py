@@ -80,6 +80,7 @@ _SIGS = {
     "hetegen_alpha_minimize": ([ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d, ctypes.POINTER(_d)], _i),
     "hetegen_model_get_alpha": ([_vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_linear_ms": ([_vp, ctypes.POINTER(_d)], _i),
+    "hetegen_model_read_ms": ([_vp, _vp, _i, _vp, ctypes.POINTER(_d)], _i),
     "hetegen_cpu_linear": ([_vp, _i, _i, _vp, _i, _vp, _i, _i, _vp, _i, _i], _i),
     "hetegen_probe_hbm": ([_vp, _sz, _i, ctypes.POINTER(_d)], _i),
     "hetegen_model_kv_create": ([_vp, _vp, _i, _i], _i),
@@ -263,6 +264,14 @@ def hetegen_model_linear_ms(model, n):
     if rc != OK:
         raise HetegenError(rc, "hetegen_model_linear_ms")
     return [out[i] for i in range(n)]
+
+
+def hetegen_model_read_ms(ctx, model, reps=5, stream=0):
+    """Median ms of one pass of plain streaming reads over the model's resident GPU
+    rows, one launch per resident linear in step order (a lower bound of the step)."""
+    out = _d()
+    _check(_lib.hetegen_model_read_ms(ctx, model, reps, stream, ctypes.byref(out)), ctx)
+    return out.value
 
 
 def hetegen_model_set_exec(model, mode, barrier_spin_limit=0):

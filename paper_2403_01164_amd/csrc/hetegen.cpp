@@ -598,7 +598,7 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
 
 hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   const size_t s = 2;
-  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr;
+  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr && hg::gemv_fuses_ln(j.B);
   const void* xin = j.x;
   long long ldin = j.ldx;
   // 1. input: materialise LayerNorm(x) unless it is fused into one resident GEMV,
@@ -1727,6 +1727,49 @@ hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {
 hetegen_status hetegen_model_get_alpha(const hetegen_model* m, double* alpha_out) {
   if (!m || !alpha_out) return HETEGEN_ERR_INVALID_ARG;
   for (size_t i = 0; i < m->lin.size(); ++i) alpha_out[i] = m->lin[i].alpha;
+  return HETEGEN_OK;
+}
+
+hetegen_status hetegen_model_read_ms(hetegen_ctx* ctx, const hetegen_model* m, int reps, void* stream,
+                                     double* ms_out) {
+  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+  ctx->err.clear();
+  if (!m || !ms_out || reps < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: bad arguments");
+  std::vector<std::pair<const void*, size_t>> bufs;
+  for (const auto& l : m->lin)
+    if (l.resident && l.n_gpu > 0 && l.W_dev) bufs.emplace_back(l.W_dev, (size_t)l.n_gpu * l.K * 2);
+  if (bufs.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: no resident GPU rows");
+  HIPCHK(ctx, hipSetDevice(ctx->device));
+  hipStream_t st = stream ? (hipStream_t)stream : ctx->capture_stream;
+  int ncu = 0;
+  HIPCHK(ctx, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device));
+  uint32_t* sink = nullptr;
+  if (hipMalloc((void**)&sink, 256) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ctx, HETEGEN_ERR_OOM, "hetegen_model_read_ms: sink");
+  }
+  hipEvent_t a = nullptr, b = nullptr;
+  hetegen_status rs = HETEGEN_OK;
+  std::vector<double> t;
+  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess)
+    rs = fail(ctx, HETEGEN_ERR_HIP, "hetegen_model_read_ms: events");
+  for (int r = 0; rs == HETEGEN_OK && r <= reps; ++r) {  // the first pass warms up
+    bool ok = hipEventRecord(a, st) == hipSuccess;
+    for (size_t i = 0; ok && i < bufs.size(); ++i)
+      ok = hg::launch_read(bufs[i].first, bufs[i].second, sink, 4 * std::max(ncu, 1), st) == hipSuccess;
+    float ms = 0;
+    ok = ok && hipEventRecord(b, st) == hipSuccess && hipEventSynchronize(b) == hipSuccess &&
+         hipEventElapsedTime(&ms, a, b) == hipSuccess;
+    if (!ok) rs = fail(ctx, HETEGEN_ERR_HIP, "hetegen_model_read_ms: read pass failed");
+    else if (r > 0) t.push_back(ms);
+  }
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  (void)hipFree(sink);
+  (void)hipGetLastError();
+  if (rs != HETEGEN_OK) return rs;
+  std::sort(t.begin(), t.end());
+  *ms_out = t[t.size() / 2];
   return HETEGEN_OK;
 }
 

@@ -67,6 +67,10 @@ size_t gemv_lds_bytes(int B, int K, int rows_per_block);
 // Largest LDS the main (non-tiled) GEMV and the persistent step accept.
 size_t gemv_lds_limit();
 
+// Whether a resident eager GEMV at batch B normalises its input itself (GemvParams.ln)
+// rather than after a separate LayerNorm launch; both give the same bits.
+bool gemv_fuses_ln(int B);
+
 // Co-resident workgroups of the persistent step kernel per CU (0 if unsupported).
 int step_blocks_per_cu(int dtype, int B, size_t lds);
 

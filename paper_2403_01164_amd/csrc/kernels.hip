@@ -139,27 +139,43 @@ template <class T, int B, class Get>
 __device__ __forceinline__ void ln_stats(Get get, int K, float* mean, float* rstd, float (*red)[8][kWaves]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n8 = K >> 3;
+  // the B rows are read side by side (B loads in flight per chunk); each row's
+  // partial still adds its chunks in increasing c
   float s[B];
 #pragma unroll
-  for (int b = 0; b < B; ++b) {
-    s[b] = 0.f;
-    for (int c = tid; c < n8; c += kThreads) {
+  for (int b = 0; b < B; ++b) s[b] = 0.f;
+#pragma unroll 2
+  for (int c = tid; c < n8; c += kThreads) {
+    uint4 v[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) v[b] = get(b, c);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
       float f[8];
-      unpack8<T>(get(b, c), f);
+      unpack8<T>(v[b], f);
       s[b] += ((f[0] + f[1]) + (f[2] + f[3])) + ((f[4] + f[5]) + (f[6] + f[7]));
     }
-    s[b] = wave_sum(s[b]);
-    if (lane == 0) red[0][b][wave] = s[b];
   }
+#pragma unroll
+  for (int b = 0; b < B; ++b) s[b] = wave_sum(s[b]);
+  if (lane == 0)
+#pragma unroll
+    for (int b = 0; b < B; ++b) red[0][b][wave] = s[b];
   __syncthreads();
 #pragma unroll
-  for (int b = 0; b < B; ++b) mean[b] = ((red[0][b][0] + red[0][b][1]) + (red[0][b][2] + red[0][b][3])) / (float)K;
-#pragma unroll
   for (int b = 0; b < B; ++b) {
+    mean[b] = ((red[0][b][0] + red[0][b][1]) + (red[0][b][2] + red[0][b][3])) / (float)K;
     s[b] = 0.f;
-    for (int c = tid; c < n8; c += kThreads) {
+  }
+#pragma unroll 2
+  for (int c = tid; c < n8; c += kThreads) {
+    uint4 v[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) v[b] = get(b, c);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
       float f[8];
-      unpack8<T>(get(b, c), f);
+      unpack8<T>(v[b], f);
       float acc = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -168,9 +184,12 @@ __device__ __forceinline__ void ln_stats(Get get, int K, float* mean, float* rst
       }
       s[b] += acc;
     }
-    s[b] = wave_sum(s[b]);
-    if (lane == 0) red[1][b][wave] = s[b];
   }
+#pragma unroll
+  for (int b = 0; b < B; ++b) s[b] = wave_sum(s[b]);
+  if (lane == 0)
+#pragma unroll
+    for (int b = 0; b < B; ++b) red[1][b][wave] = s[b];
   __syncthreads();
 #pragma unroll
   for (int b = 0; b < B; ++b) {
@@ -352,10 +371,13 @@ __device__ __forceinline__ void gemv_block(const GemvParams& p, int blk, uint4* 
   // prologue: x, bias and residual of the block into LDS
   {
     const uint16_t* x = (const uint16_t*)p.x;
+#pragma unroll 2
+    for (int c = tid; c < k8; c += kThreads) {
+      uint4 v[B];
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const uint16_t* xrow = x + b * p.ldx;
-      for (int c = tid; c < k8; c += kThreads) xs[b * k8 + c] = load_act16<COH_LOAD>(xrow, (uint32_t)K * 2, (uint32_t)c * 16);
+      for (int b = 0; b < B; ++b) v[b] = load_act16<COH_LOAD>(x + b * p.ldx, (uint32_t)K * 2, (uint32_t)c * 16);
+#pragma unroll
+      for (int b = 0; b < B; ++b) xs[b * k8 + c] = v[b];
     }
     const uint16_t* bias = (const uint16_t*)p.bias;
     for (int i = tid; i < nrows; i += kThreads) sb[i] = bias ? T::to_f32(gmem(bias)[row_begin + i]) : 0.f;
@@ -373,9 +395,9 @@ __device__ __forceinline__ void gemv_block(const GemvParams& p, int blk, uint4* 
       float mean[B], rstd[B];
       ln_stats<T, B>([&](int b, int c) { return xs[b * k8 + c]; }, K, mean, rstd, red);
       const bool write_h = p.h_out != nullptr && blk == 0;
+      for (int c = tid; c < k8; c += kThreads) {  // each thread rewrites only the chunks it summed
 #pragma unroll
-      for (int b = 0; b < B; ++b) {
-        for (int c = tid; c < k8; c += kThreads) {  // each thread rewrites only the chunks it summed
+        for (int b = 0; b < B; ++b) {
           const uint4 v = normalize8<T>(xs[b * k8 + c], mean[b], rstd[b]);
           xs[b * k8 + c] = v;
           if (write_h) *(uint4*)((uint16_t*)p.h_out + b * p.ldh + (long long)c * 8) = v;
@@ -695,15 +717,17 @@ __device__ __forceinline__ void stage_x_tile(const GemvParams& p, uint4* xs, int
                                              const float* rstd, bool write_h) {
   const uint16_t* x = (const uint16_t*)p.x;
   const int n8 = kn >> 3, kt8 = p.ktile >> 3;
+  for (int c = threadIdx.x; c < n8; c += kThreads) {
+    uint4 v[B];
 #pragma unroll
-  for (int b = 0; b < B; ++b) {
-    for (int c = threadIdx.x; c < n8; c += kThreads) {
-      uint4 v = *(const uint4*)(x + b * p.ldx + k0 + (long long)c * 8);
+    for (int b = 0; b < B; ++b) v[b] = *(const uint4*)(x + b * p.ldx + k0 + (long long)c * 8);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
       if (p.ln) {
-        v = normalize8<T>(v, mean[b], rstd[b]);
-        if (write_h) *(uint4*)((uint16_t*)p.h_out + b * p.ldh + k0 + (long long)c * 8) = v;
+        v[b] = normalize8<T>(v[b], mean[b], rstd[b]);
+        if (write_h) *(uint4*)((uint16_t*)p.h_out + b * p.ldh + k0 + (long long)c * 8) = v[b];
       }
-      xs[b * kt8 + c] = v;
+      xs[b * kt8 + c] = v[b];
     }
   }
 }
@@ -794,26 +818,27 @@ __global__ __launch_bounds__(kThreads) void gemv_tiled_kernel(GemvParams p) {
   }
 }
 
-template <class T, int B>
+// One batch row per blockIdx.y: the statistics of a row are the same bits whatever
+// the batch (ln_stats treats rows independently), and the B rows run in parallel.
+template <class T>
 __global__ __launch_bounds__(kThreads) void layernorm_kernel(const uint16_t* __restrict__ x, long long ldx, int K,
                                                              uint16_t* __restrict__ h, long long ldh,
                                                              float* __restrict__ h_host) {
   __shared__ float red[2][8][kWaves];
-  float mean[B], rstd[B];
-  ln_stats<T, B>([&](int b, int c) { return *(const uint4*)(x + b * ldx + (long long)c * 8); }, K, mean, rstd, red);
+  const int b = blockIdx.y;
+  const uint16_t* xr = x + b * ldx;
+  float mean, rstd;
+  ln_stats<T, 1>([&](int, int c) { return *(const uint4*)(xr + (long long)c * 8); }, K, &mean, &rstd, red);
   const int n8 = K >> 3;
-#pragma unroll
-  for (int b = 0; b < B; ++b) {
-    for (int c = blockIdx.x * kThreads + threadIdx.x; c < n8; c += gridDim.x * kThreads) {
-      uint4 v = normalize8<T>(*(const uint4*)(x + b * ldx + (long long)c * 8), mean[b], rstd[b]);
-      *(uint4*)(h + b * ldh + (long long)c * 8) = v;
-      if (h_host) {
-        float f[8];
-        unpack8<T>(v, f);
-        float4* dst = (float4*)(h_host + (long long)b * K + (long long)c * 8);
-        dst[0] = make_float4(f[0], f[1], f[2], f[3]);
-        dst[1] = make_float4(f[4], f[5], f[6], f[7]);
-      }
+  for (int c = blockIdx.x * kThreads + threadIdx.x; c < n8; c += gridDim.x * kThreads) {
+    uint4 v = normalize8<T>(*(const uint4*)(xr + (long long)c * 8), mean, rstd);
+    *(uint4*)(h + b * ldh + (long long)c * 8) = v;
+    if (h_host) {
+      float f[8];
+      unpack8<T>(v, f);
+      float4* dst = (float4*)(h_host + (long long)b * K + (long long)c * 8);
+      dst[0] = make_float4(f[0], f[1], f[2], f[3]);
+      dst[1] = make_float4(f[4], f[5], f[6], f[7]);
     }
   }
 }
@@ -960,30 +985,16 @@ hipError_t launch_gemv_t(const GemvParams& p, int B, hipStream_t s, int cap) {
   return hipErrorInvalidValue;
 }
 
-template <class T, int B>
-hipError_t launch_ln_b(const void* x, long long ldx, int K, void* h, long long ldh, float* hh, hipStream_t s) {
+template <class T>
+hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long long ldh, float* hh, hipStream_t s) {
+  if (B < 1 || B > 8) return hipErrorInvalidValue;
   const int n8 = K >> 3;
   int grid = (n8 + kThreads * 4 - 1) / (kThreads * 4);
   if (grid < 1) grid = 1;
   if (grid > 16) grid = 16;
-  hipLaunchKernelGGL((layernorm_kernel<T, B>), dim3(grid), dim3(kThreads), 0, s, (const uint16_t*)x, ldx, K,
+  hipLaunchKernelGGL((layernorm_kernel<T>), dim3(grid, B), dim3(kThreads), 0, s, (const uint16_t*)x, ldx, K,
                      (uint16_t*)h, ldh, hh);
   return hipGetLastError();
-}
-
-template <class T>
-hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long long ldh, float* hh, hipStream_t s) {
-  switch (B) {
-    case 1: return launch_ln_b<T, 1>(x, ldx, K, h, ldh, hh, s);
-    case 2: return launch_ln_b<T, 2>(x, ldx, K, h, ldh, hh, s);
-    case 3: return launch_ln_b<T, 3>(x, ldx, K, h, ldh, hh, s);
-    case 4: return launch_ln_b<T, 4>(x, ldx, K, h, ldh, hh, s);
-    case 5: return launch_ln_b<T, 5>(x, ldx, K, h, ldh, hh, s);
-    case 6: return launch_ln_b<T, 6>(x, ldx, K, h, ldh, hh, s);
-    case 7: return launch_ln_b<T, 7>(x, ldx, K, h, ldh, hh, s);
-    case 8: return launch_ln_b<T, 8>(x, ldx, K, h, ldh, hh, s);
-  }
-  return hipErrorInvalidValue;
 }
 
 template <class T>
@@ -1021,6 +1032,10 @@ size_t gemv_lds_bytes(int B, int K, int rows_per_block) {
 }
 
 size_t gemv_lds_limit() { return kLdsMain; }
+
+// Measured on OPT-6.7B shapes: from B = 5 on, normalising x once per workgroup in the
+// prologue costs more than a separate LayerNorm launch.
+bool gemv_fuses_ln(int B) { return B <= 4; }
 
 int step_blocks_per_cu(int dtype, int B, size_t lds) {
   const void* f = dtype == 1 ? step_fn<BF16>(B) : step_fn<F16>(B);

@@ -344,6 +344,23 @@ def test_linear_times_reported_for_heterogeneous_steps(ctx):
         m.free()
 
 
+def test_read_floor_of_resident_rows(ctx):
+    dtype, L, H, F = synth.F16, 2, 512, 2048
+    m = Model(ctx, L, H, F, dtype, [0.0, 0.3, 0.0, 0.0] * L, [1, 1, 0, 1] * L)
+    try:
+        ms = hg.hetegen_model_read_ms(ctx, m.m, 3)
+        assert np.isfinite(ms) and 0 < ms < 100
+    finally:
+        m.free()
+    m = Model(ctx, 1, H, F, dtype, 0.5, 0)  # nothing resident
+    try:
+        with pytest.raises(hg.HetegenError):
+            hg.hetegen_model_read_ms(ctx, m.m, 3)
+        with pytest.raises(hg.HetegenError):
+            hg.hetegen_model_read_ms(ctx, m.m, 0)
+    finally:
+        m.free()
+
 
 # ---- full decode steps with a KV cache (Sec. 2.1, Eq. 1) ----
 def _fill_cache(m, B, P, seed=0):
