@@ -399,6 +399,10 @@ def main():
             "busy_frac": {"cpu": round(prof["cpu_ms"] / wall_ms, 4), "io": round(prof["h2d_ms"] / wall_ms, 4),
                           "gpu": round(prof["gpu_ms"] / wall_ms, 4), "pin": round(prof["pin_ms"] / wall_ms, 4)},
             "profiled_ms_per_step": round(wall_ms / nprof, 3),
+            # where the calling thread waits around the CPU shares (per step of the profiled pass)
+            "wait_ms_per_step": {"input_before_cpu_share": round(prof["xwait_ms"] / nprof, 3),
+                                 "link_after_cpu_share": round(prof["tailwait_ms"] / nprof, 3),
+                                 "cpu_shares": int(prof["cpu_shares"] // nprof)},
         }
         log("hetero: %s" % json.dumps(result["hetero"]))
 

@@ -380,6 +380,11 @@ typedef struct {
   int64_t gemv_launches;
   double pin_ms;       /* host time the pin team spent staging pageable chunks */
   double pin_bytes;    /* bytes staged */
+  double xwait_ms;     /* host time waiting, before a CPU share, for its input to reach host memory
+                          (the GPU work ahead of it in stream order, then the hand-off) */
+  double tailwait_ms;  /* host time waiting, after a CPU share, to enqueue the GEMVs of the linear's
+                          remaining chunks (their copies not yet issued: the link is behind) */
+  int64_t cpu_shares;  /* linears computed with CPU rows */
 } hetegen_profile;
 
 /* on != 0: bracket every chunk copy and GEMV launch with events and synchronise at

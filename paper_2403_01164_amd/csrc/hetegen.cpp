@@ -670,7 +670,10 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
     if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
     ctx->y_pending = false;
     TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)j.B * j.n_cpu * 4));
+    const auto tw = Clock::now();
     HIPCHK(ctx, hipEventSynchronize(ctx->ev_x));
+    ctx->prof.xwait_ms += ms_since(tw);
+    ctx->prof.cpu_shares++;
     auto t0 = Clock::now();
     hg::cpu_share(ctx->x_host, j.B, j.K, (const uint16_t*)j.W_host, j.dtype, (const uint16_t*)j.bias_host, j.n_gpu, j.N,
                   ctx->y_host, j.n_cpu, ctx->cpu_threads);
@@ -684,10 +687,12 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
     HIPCHK(ctx, hipEventRecord(ctx->ev_y, st));
     ctx->y_pending = true;
   }
+  const auto tt = Clock::now();
   while (streamed && r0 < j.n_gpu) {
     bool did = false;
     TRY(next_chunk(true, &did));
   }
+  if (j.n_cpu > 0) ctx->prof.tailwait_ms += ms_since(tt);
   if (j.trace_out)
     HIPCHK(ctx, hipMemcpy2DAsync(j.trace_out, (size_t)j.N * s, j.y, (size_t)j.ldy * s, (size_t)j.N * s, j.B,
                                  hipMemcpyDeviceToDevice, st));
