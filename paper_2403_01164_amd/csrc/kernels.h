@@ -64,7 +64,9 @@ int gemv_rows_unit(int B);
 // Dynamic LDS of the main GEMV for batch B, reduction K and rows_per_block rows.
 size_t gemv_lds_bytes(int B, int K, int rows_per_block);
 
-// Largest LDS the main (non-tiled) GEMV and the persistent step accept.
+// Largest LDS the persistent step accepts per workgroup (the per-linear main GEMV may
+// use up to the device's LDS per workgroup, less 1 KiB, before it switches to the
+// K-tiled kernel).
 size_t gemv_lds_limit();
 
 // Whether a resident eager GEMV at batch B normalises its input itself (GemvParams.ln)

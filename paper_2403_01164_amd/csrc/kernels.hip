@@ -25,7 +25,9 @@
 //    gathered in LDS and stored per block with contiguous stores; the epilogue adds
 //    the bias, applies ReLU or a residual sum and rounds to the activation type (or
 //    stores binary32), so the decode step needs no elementwise kernels.
-// When x does not fit in LDS (large B*K), a K-tiled variant restages x per tile.
+// x may use the device's whole LDS per workgroup (160 KiB on gfx950, opted in above the
+// default 64 KiB, with the grid capped at the workgroups that fit at once); when it
+// does not fit even so (large B*K), a K-tiled variant restages x per tile.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
