@@ -83,6 +83,84 @@ def counter_traffic(model, dt, B):
     return float(fields["traffic_bytes_per_launch"])
 
 
+
+def single_linear(args, torch, synth, hg):
+    """Latency of hetegen_linear on one shape (the single-linear configuration): for each
+    CPU fraction and placement, host wall time from the call to the end of the GPU work
+    (stream synchronised), median and p10/p90 over the reps; each rep uses the next of
+    enough distinct weight copies that they cannot stay in the 256 MB memory-side cache."""
+    N, K = (int(v) for v in args.linear.lower().split("x"))
+    B, dt = args.batch, 0
+    ctx = hg.hetegen_create(0, cpu_threads=args.threads, chunk_bytes=args.chunk_mb << 20, ring_depth=args.ring)
+    sptr = torch.cuda.current_stream().cuda_stream
+    wb = N * K * 2
+    ncopy = max(3, (512 << 20) // wb + 1)
+    Wh, Wd = [], []
+    bh = hg.hetegen_host_alloc(ctx, N * 2)
+    synth.fill_normal_ptr(bh, N, dt, 0, synth.bias_id(0, "qkv"), 0.0, 0.02)
+    bd = torch.empty(N, dtype=torch.int16, device="cuda")
+    bd.copy_(torch.from_numpy(np.ctypeslib.as_array((ctypes.c_int16 * N).from_address(bh)).copy()))
+    for c in range(ncopy):
+        w = hg.hetegen_host_alloc(ctx, wb)
+        synth.fill_normal_ptr(w, N * K, dt, 0, synth.weight_id(c, "qkv"), 0.0, 0.02)
+        Wh.append(w)
+        d = torch.empty(N * K, dtype=torch.int16, device="cuda")
+        d.copy_(torch.from_numpy(np.ctypeslib.as_array((ctypes.c_int16 * (N * K)).from_address(w)).copy()))
+        Wd.append(d)
+    x = torch.from_numpy(synth.normal((B, K), dt, 0, synth.act_id(0)).view(np.int16)).cuda()
+    y = torch.empty((B, N), dtype=torch.float32, device="cuda")
+    probe = hg.hetegen_probe(ctx, Wh[0], N, K, dt, B, 5)
+    log("single linear [%d,%d] B=%d: %d weight copies (%.0f MB); probe %s" %
+        (N, K, B, ncopy, ncopy * wb / 1e6, {k: round(v / 1e9, 1) for k, v in probe.items()}))
+    rows = []
+    for resident in (True, False):
+        for alpha in (0.0, 0.25, 0.5, 1.0):
+            def call(c):
+                hg.hetegen_linear(ctx, x.data_ptr(), B, K, Wh[c], Wd[c].data_ptr() if resident else 0, N, dt, bh,
+                                  bd.data_ptr(), alpha, y.data_ptr(), hg.F32, sptr)
+            for c in range(10):
+                call(c % ncopy)
+            torch.cuda.synchronize()
+            ts = []
+            for r in range(args.linear_reps):
+                t0 = time.perf_counter()
+                call((r + 10) % ncopy)
+                torch.cuda.synchronize()
+                ts.append((time.perf_counter() - t0) * 1e6)
+            ts.sort()
+            q = lambda f: ts[min(len(ts) - 1, int(f * (len(ts) - 1) + 0.5))]
+            n_cpu = min(N, int(np.floor(alpha * N + 0.5)))
+            # roofline of the configuration: HBM for resident GPU rows, the link for streamed
+            # ones, host reads for CPU rows (Eq. 4 balance when split)
+            v_g = HBM_PEAK_GBPS * 1e9 if resident else 1.0 / (1.0 / probe["h2d_Bps"] + 1.0 / probe["hbm_gemv_Bps"])
+            if n_cpu == 0:
+                floor_us, bound = wb / v_g * 1e6, ("hbm" if resident else "h2d")
+            elif n_cpu == N:
+                floor_us, bound = wb / probe["cpu_Bps"] * 1e6, "cpu"
+            else:
+                floor_us = max(n_cpu * K * 2 / probe["cpu_Bps"], (N - n_cpu) * K * 2 / v_g) * 1e6
+                bound = "cpu+" + ("hbm" if resident else "h2d")
+            rows.append({"alpha_cpu": alpha, "resident": resident, "median_us": round(q(0.5), 2),
+                         "p10_us": round(q(0.1), 2), "p90_us": round(q(0.9), 2),
+                         "GBps": round(wb / (q(0.5) * 1e-6) / 1e9, 2), "bound": bound,
+                         "floor_us": round(floor_us, 2), "frac_of_floor": round(floor_us / q(0.5), 4)})
+            log("alpha %.2f %s: median %.1f us (p10 %.1f, p90 %.1f), floor %.1f us (%s)" %
+                (alpha, "resident" if resident else "streamed", q(0.5), q(0.1), q(0.9), floor_us, bound))
+    head = rows[0]
+    print(json.dumps({
+        "metric": "single-linear latency (us per call, host wall to end of GPU work)",
+        "value": head["median_us"], "unit": "us", "n_gpus": 1, "steps": args.linear_reps, "warmup": 10,
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic: seeded N(0,0.02) weights and bias, N(0,1) x",
+        "config": {"workload": "single Linear [%d,%d] fp16, batch %d, CPU fractions 0/.25/.5/1, resident and "
+                               "streamed; %d weight copies rotated (%.0f MB)" % (N, K, B, ncopy, ncopy * wb / 1e6)},
+        "probe_GBps": {k: round(v / 1e9, 2) for k, v in probe.items()},
+        "results": rows}))
+    for w in Wh:
+        hg.hetegen_host_free(ctx, w)
+    hg.hetegen_host_free(ctx, bh)
+    hg.hetegen_destroy(ctx)
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,6 +202,11 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="end with one plain 256 MiB device-to-device copy, the reference dispatch for "
                          "scaling HBM byte counters")
+    ap.add_argument("--linear", default=None, metavar="NxK",
+                    help="instead of a decode step: latency of one heterogeneous linear [N,K] (fp16, --batch) at "
+                         "CPU fractions 0, .25, .5, 1, resident and streamed, over --linear-reps calls that rotate "
+                         "weight copies totalling > 512 MB (prints its own JSON line)")
+    ap.add_argument("--linear-reps", type=int, default=200)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the heterogeneous "
@@ -137,6 +220,9 @@ def main():
     import paper_2403_01164_amd as hg
 
     torch.cuda.set_device(0)
+    if args.linear:
+        single_linear(args, torch, synth, hg)
+        return
     L, H, F, dt, placement = OPT[args.model]
     L_full = L
     if args.layers:
@@ -262,6 +348,7 @@ def main():
         step(t)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hg.hetegen_get_profile(ctx, reset=True)  # host-side counters of the timed steps (no events added)
     wall0 = time.perf_counter()
     e0.record(stream)
     for t in range(args.warmup, nstep):
@@ -269,10 +356,22 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    tprof = hg.hetegen_get_profile(ctx, reset=True)
     ms_step = e0.elapsed_time(e1) / args.steps
     gbps = wbytes / (ms_step * 1e-3) / 1e9
     log("decode step %.4f ms/token, %.1f GB/s effective (wall %.4f ms/step)" %
         (ms_step, gbps, wall * 1e3 / args.steps))
+    # distribution over steps: a second pass with events between consecutive steps
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for t in range(args.warmup, nstep):
+        step(t)
+        evs[t - args.warmup + 1].record(stream)
+    torch.cuda.synchronize()
+    per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    step_pct = [round(per_step[min(len(per_step) - 1, int(q * (len(per_step) - 1) + 0.5))], 5)
+                for q in (0.1, 0.5, 0.9)]
+    log("per-step ms p10 / p50 / p90: %s" % step_pct)
 
     if placement == "all":
         desc = "all linears HBM-resident (alpha=0), GEMV-only"
@@ -297,6 +396,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
         "ms_per_token": round(ms_step, 5),
+        "step_ms_p10_p50_p90": step_pct,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -399,10 +499,17 @@ def main():
             "busy_frac": {"cpu": round(prof["cpu_ms"] / wall_ms, 4), "io": round(prof["h2d_ms"] / wall_ms, 4),
                           "gpu": round(prof["gpu_ms"] / wall_ms, 4), "pin": round(prof["pin_ms"] / wall_ms, 4)},
             "profiled_ms_per_step": round(wall_ms / nprof, 3),
-            # where the calling thread waits around the CPU shares (per step of the profiled pass)
-            "wait_ms_per_step": {"input_before_cpu_share": round(prof["xwait_ms"] / nprof, 3),
-                                 "link_after_cpu_share": round(prof["tailwait_ms"] / nprof, 3),
-                                 "cpu_shares": int(prof["cpu_shares"] // nprof)},
+            # the calling thread's time per timed step: CPU shares, waits for their inputs (the
+            # GPU work ahead of them, then the hand-off), waits for the link after them, and the
+            # rest (enqueueing kernels and copies, the glue between linears)
+            "host_ms_per_step": {"cpu_shares": round(tprof["cpu_ms"] / args.steps, 3),
+                                 "input_wait": round(tprof["xwait_ms"] / args.steps, 3),
+                                 "link_wait": round(tprof["tailwait_ms"] / args.steps, 3),
+                                 "enqueue_in_linears": round((tprof["hetlin_ms"] - tprof["cpu_ms"] -
+                                                              tprof["xwait_ms"] - tprof["tailwait_ms"]) /
+                                                             args.steps, 3),
+                                 "outside_linears": round(ms_step - tprof["hetlin_ms"] / args.steps, 3),
+                                 "n_cpu_shares": int(tprof["cpu_shares"] // args.steps)},
         }
         log("hetero: %s" % json.dumps(result["hetero"]))
 

@@ -385,6 +385,8 @@ typedef struct {
   double tailwait_ms;  /* host time waiting, after a CPU share, to enqueue the GEMVs of the linear's
                           remaining chunks (their copies not yet issued: the link is behind) */
   int64_t cpu_shares;  /* linears computed with CPU rows */
+  double hetlin_ms;    /* host time inside those linears (CPU share, the waits above, and enqueueing
+                          their kernels and chunk GEMVs) */
 } hetegen_profile;
 
 /* on != 0: bracket every chunk copy and GEMV launch with events and synchronise at

@@ -436,6 +436,7 @@ bool copy_chunk(hetegen_ctx* ctx, long long s, const hetegen_ctx::Chunk& c, std:
   const hipError_t q = hipEventQuery(ctx->ev_free[slot]);
   if (q != hipSuccess) {
     if (q != hipErrorNotReady) MGR_HIP(q);
+    (void)hipGetLastError();  // not an error
     if (c.host_wait) MGR_HIP(hipEventSynchronize(ctx->ev_free[slot]));
     else MGR_HIP(hipStreamWaitEvent(ctx->copy_stream, ctx->ev_free[slot], 0));
   }
@@ -611,6 +612,7 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
 }
 
 hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
+  const auto tl = Clock::now();
   const size_t s = 2;
   const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr && hg::gemv_fuses_ln(j.B);
   const void* xin = j.x;
@@ -649,7 +651,16 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
     const int nr = std::min(cr, j.n_gpu - r0);
     if (bytes != (size_t)nr * j.K * s) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: chunk plan out of step");
     const int slot = (int)(seq % ctx->ring);
-    HIPCHK(ctx, hipStreamWaitEvent(st, ctx->ev_ready[slot], 0));
+    // a copy that has already completed needs no wait; queuing a wait on the copy
+    // stream costs the calling thread ~20 us per chunk, on the path between two CPU
+    // shares (the event's last record is this chunk's copy: front_chunk saw it issued)
+    const hipError_t q = hipEventQuery(ctx->ev_ready[slot]);
+    if (q == hipErrorNotReady) {
+      (void)hipGetLastError();  // not an error: keep it from surfacing at the next launch check
+      HIPCHK(ctx, hipStreamWaitEvent(st, ctx->ev_ready[slot], 0));
+    } else {
+      HIPCHK(ctx, q);
+    }
     TRY(run_gemv(ctx, j, xin, ldin, 0, ctx->slot[slot], r0, nr, st, nullptr));
     HIPCHK(ctx, hipEventRecord(ctx->ev_free[slot], st));
     pop_chunk(ctx);
@@ -666,11 +677,12 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   }
   // 3. CPU rows on the calling thread's OpenMP team
   if (j.n_cpu > 0) {
-    // the previous import kernel may still read y_host
+    // the previous import kernel may still read y_host (it precedes ev_x in stream
+    // order, so this wait is part of the wait for the input)
+    const auto tw = Clock::now();
     if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
     ctx->y_pending = false;
     TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)j.B * j.n_cpu * 4));
-    const auto tw = Clock::now();
     HIPCHK(ctx, hipEventSynchronize(ctx->ev_x));
     ctx->prof.xwait_ms += ms_since(tw);
     ctx->prof.cpu_shares++;
@@ -696,6 +708,7 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   if (j.trace_out)
     HIPCHK(ctx, hipMemcpy2DAsync(j.trace_out, (size_t)j.N * s, j.y, (size_t)j.ldy * s, (size_t)j.N * s, j.B,
                                  hipMemcpyDeviceToDevice, st));
+  if (j.n_cpu > 0) ctx->prof.hetlin_ms += ms_since(tl);
   return HETEGEN_OK;
 }
 
