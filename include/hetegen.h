@@ -59,6 +59,10 @@ typedef struct {
                          (Sec. 4.2 hybrid pin || transfer), in [1, 64]; 0: 4;
                          < 0: pageable weights are refused with HETEGEN_ERR_NOT_PINNED */
   int pin_ring;       /* pinned staging buffers of chunk_bytes each, in [2, 64]; 0: 4 */
+  int numa_node;      /* NUMA placement of the pinned host memory the context allocates
+                         (hetegen_host_alloc, hand-off and staging buffers): n > 0 binds it to
+                         node n - 1 (INVALID_ARG if that node does not exist); 0: the
+                         allocating thread's own memory policy */
 } hetegen_config;
 
 /* Create a context on cfg->device: a copy stream, the staging ring

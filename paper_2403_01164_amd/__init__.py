@@ -34,7 +34,8 @@ if not os.path.exists(LIB_PATH):
 
 class Config(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int), ("cpu_threads", ctypes.c_int), ("chunk_bytes", ctypes.c_size_t),
-                ("ring_depth", ctypes.c_int), ("pin_threads", ctypes.c_int), ("pin_ring", ctypes.c_int)]
+                ("ring_depth", ctypes.c_int), ("pin_threads", ctypes.c_int), ("pin_ring", ctypes.c_int),
+                ("numa_node", ctypes.c_int)]
 
 
 class Shape(ctypes.Structure):
@@ -118,8 +119,11 @@ def _check(rc, ctx=None):
         raise HetegenError(rc, msg.decode() if msg else "")
 
 
-def hetegen_create(device=0, cpu_threads=0, chunk_bytes=0, ring_depth=0, pin_threads=0, pin_ring=0):
-    cfg = Config(device, cpu_threads, chunk_bytes, ring_depth, pin_threads, pin_ring)
+def hetegen_create(device=0, cpu_threads=0, chunk_bytes=0, ring_depth=0, pin_threads=0, pin_ring=0,
+                   numa_node=None):
+    """numa_node: None leaves pinned host memory to the calling thread's policy; n binds it to node n."""
+    cfg = Config(device, cpu_threads, chunk_bytes, ring_depth, pin_threads, pin_ring,
+                 0 if numa_node is None else int(numa_node) + 1)
     out = _vp()
     _check(_lib.hetegen_create(ctypes.byref(cfg), ctypes.byref(out)))
     return out.value

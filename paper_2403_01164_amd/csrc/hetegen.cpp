@@ -24,6 +24,8 @@
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
+#include <sys/syscall.h>
+#include <unistd.h>
 
 #include <algorithm>
 #include <chrono>
@@ -178,6 +180,7 @@ struct hetegen_ctx {
   // pageable weights: pinned staging buffers and the team that fills them
   int pin_threads = kDefaultPinThreads;  // < 0: pageable weights refused
   int pin_ring = kDefaultPinRing;
+  int numa_node = -1;                     // node of pinned allocations; < 0: thread policy
   std::vector<void*> bounce;
   std::vector<hipEvent_t> ev_bounce;
   long long bounce_seq = 0;  // manager thread only
@@ -283,6 +286,23 @@ int split_cpu_rows(int N, double alpha) {
   return (int)c;
 }
 
+// hipHostMalloc on the context's NUMA node: the calling thread's memory policy is set
+// to bind to that node around the allocation (which then follows it) and restored.
+hipError_t host_malloc(const hetegen_ctx* ctx, void** p, size_t bytes, unsigned flags) {
+  if (ctx->numa_node < 0) return hipHostMalloc(p, bytes, flags);
+  constexpr int kMpolBind = 2;
+  int old_mode = 0;
+  unsigned long old_mask[16] = {0};
+  const bool saved = syscall(SYS_get_mempolicy, &old_mode, old_mask, 16 * 8 * sizeof(unsigned long), nullptr, 0) == 0;
+  unsigned long mask[16] = {0};
+  mask[ctx->numa_node / 64] = 1ul << (ctx->numa_node % 64);
+  if (syscall(SYS_set_mempolicy, kMpolBind, mask, 16 * 8 * sizeof(unsigned long)) != 0) return hipErrorInvalidValue;
+  const hipError_t e = hipHostMalloc(p, bytes, flags | hipHostMallocNumaUser);
+  if (saved) (void)syscall(SYS_set_mempolicy, old_mode, old_mask, 16 * 8 * sizeof(unsigned long));
+  else (void)syscall(SYS_set_mempolicy, 0, nullptr, 0);
+  return e;
+}
+
 hetegen_status ensure_host(hetegen_ctx* ctx, float** buf, size_t* have, size_t need) {
   if (*have >= need) return HETEGEN_OK;
   if (*buf) {
@@ -293,7 +313,7 @@ hetegen_status ensure_host(hetegen_ctx* ctx, float** buf, size_t* have, size_t n
   }
   size_t bytes = std::max(need, (size_t)1 << 20);
   // coherent: written by kernels and read by the host (and the reverse) around events
-  if (hipHostMalloc((void**)buf, bytes, hipHostMallocCoherent) != hipSuccess) {
+  if (host_malloc(ctx, (void**)buf, bytes, hipHostMallocCoherent) != hipSuccess) {
     (void)hipGetLastError();
     *buf = nullptr;
     return fail(ctx, HETEGEN_ERR_OOM, "pinned hand-off buffer of %zu bytes", bytes);
@@ -493,7 +513,7 @@ hetegen_status ensure_pin_resources(hetegen_ctx* ctx) {
   ctx->bounce.resize(ctx->pin_ring, nullptr);
   ctx->ev_bounce.resize(ctx->pin_ring, nullptr);
   for (int i = 0; i < ctx->pin_ring; ++i) {
-    if (!ctx->bounce[i] && hipHostMalloc(&ctx->bounce[i], ctx->chunk_bytes, hipHostMallocDefault) != hipSuccess) {
+    if (!ctx->bounce[i] && host_malloc(ctx, &ctx->bounce[i], ctx->chunk_bytes, hipHostMallocDefault) != hipSuccess) {
       (void)hipGetLastError();
       ctx->bounce[i] = nullptr;
       return fail(ctx, HETEGEN_ERR_OOM, "pinned staging buffer of %zu bytes", ctx->chunk_bytes);
@@ -747,6 +767,14 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
   }
   if (c.device < 0 || c.device >= ndev)
     return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "device %d outside [0, %d)", c.device, ndev);
+  if (c.numa_node < 0 || c.numa_node > 1024)
+    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "numa_node %d outside [0, 1024]", c.numa_node);
+  if (c.numa_node > 0) {
+    char path[64];
+    snprintf(path, sizeof path, "/sys/devices/system/node/node%d", c.numa_node - 1);
+    if (access(path, F_OK) != 0)
+      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "NUMA node %d does not exist", c.numa_node - 1);
+  }
   hetegen_ctx* ctx = new hetegen_ctx();
   ctx->device = c.device;
   ctx->cpu_threads = c.cpu_threads;
@@ -754,6 +782,7 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
   ctx->ring = c.ring_depth;
   ctx->pin_threads = c.pin_threads < 0 ? -1 : c.pin_threads;
   ctx->pin_ring = c.pin_ring;
+  ctx->numa_node = c.numa_node - 1;
   auto bail = [&](hetegen_status st) {
     g_create_error = ctx->err;
     hetegen_destroy(ctx);
@@ -835,10 +864,10 @@ hetegen_status hetegen_host_alloc(hetegen_ctx* ctx, size_t bytes, void** p) {
   if (!ctx || !p || bytes == 0) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_host_alloc: bad arguments");
   *p = nullptr;
   HIPCHK(ctx, hipSetDevice(ctx->device));
-  if (hipHostMalloc(p, bytes, hipHostMallocDefault) != hipSuccess) {
+  if (host_malloc(ctx, p, bytes, hipHostMallocDefault) != hipSuccess) {
     (void)hipGetLastError();
     *p = nullptr;
-    return fail(ctx, HETEGEN_ERR_OOM, "hipHostMalloc of %zu bytes failed", bytes);
+    return fail(ctx, HETEGEN_ERR_OOM, "pinned allocation of %zu bytes failed", bytes);
   }
   return HETEGEN_OK;
 }

@@ -282,3 +282,36 @@ def test_probe_hbm_read_bandwidth(ctx):
     assert 5e11 < bps < 9e12  # between a slow link and above the nominal 8 TB/s peak
     with pytest.raises(hg.HetegenError):
         hg.hetegen_probe_hbm(ctx, 1000, 3)
+
+
+def _page_node(addr):
+    """NUMA node of the page at `addr` (get_mempolicy with MPOL_F_NODE | MPOL_F_ADDR)."""
+    import ctypes
+    libc = ctypes.CDLL(None, use_errno=True)
+    node = ctypes.c_int(-1)
+    sys_get_mempolicy = 239  # x86-64
+    rc = libc.syscall(sys_get_mempolicy, ctypes.byref(node), None, ctypes.c_ulong(0), ctypes.c_void_p(addr),
+                      ctypes.c_ulong(1 | 2))
+    return node.value if rc == 0 else None
+
+
+def test_numa_node_placement_of_pinned_memory():
+    import os
+    nodes = sorted(int(d[4:]) for d in os.listdir("/sys/devices/system/node") if d.startswith("node") and d[4:].isdigit())
+    c = hg.hetegen_create(0, numa_node=nodes[-1], chunk_bytes=65536, ring_depth=2)
+    try:
+        p = Problem(c, 2, 520, 1001, synth.F16, seed=3)
+        try:
+            got = _page_node(p.W.ptr)
+            if got is not None:
+                assert got == nodes[-1]
+            for alpha, resident in ((0.0, False), (0.4, False), (0.4, True), (1.0, False)):
+                assert rel_err(p.run(alpha, resident), p.ref()) <= TOL, (alpha, resident)
+        finally:
+            p.free()
+    finally:
+        hg.hetegen_destroy(c)
+    with pytest.raises(hg.HetegenError):
+        hg.hetegen_create(0, numa_node=nodes[-1] + 1)
+    with pytest.raises(hg.HetegenError):
+        hg.hetegen_create(0, numa_node=5000)
