@@ -73,3 +73,20 @@ def test_bad_arguments():
         hg.hetegen_cpu_linear(x, W.ctypes.data, 0, synth.F16, 0, 4)
     with pytest.raises(hg.HetegenError):  # rows reversed
         hg.hetegen_cpu_linear(np.zeros((1, 8), np.float32), W.ctypes.data, 0, synth.F16, 3, 2)
+
+
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+@pytest.mark.parametrize("K", [264, 520, 4104])
+def test_batch_rows_independent(dtype, K):
+    # every batch row gets the bits it gets alone (batches of 5-8 run in two groups over
+    # L1-resident chunks; the order of each row's products does not change)
+    B, N = 8, 37
+    x, W, b = _problem(B, K, N, dtype, "normal", seed=K)
+    xf = oracle.decode(x, dtype)
+    full = hg.hetegen_cpu_linear(xf, W.ctypes.data, b.ctypes.data, dtype, 0, N)
+    for nb in (5, 6, 7):
+        part = hg.hetegen_cpu_linear(np.ascontiguousarray(xf[:nb]), W.ctypes.data, b.ctypes.data, dtype, 0, N)
+        assert np.array_equal(part, full[:nb]), nb
+    for bb in range(B):
+        one = hg.hetegen_cpu_linear(np.ascontiguousarray(xf[bb:bb + 1]), W.ctypes.data, b.ctypes.data, dtype, 0, N)
+        assert np.array_equal(one[0], full[bb]), bb
