@@ -52,7 +52,8 @@ typedef struct hetegen_model hetegen_model;
 
 typedef struct {
   int device;         /* HIP device ordinal */
-  int cpu_threads;    /* host threads for the CPU share; <= 0: the OpenMP default */
+  int cpu_threads;    /* host threads for the CPU share (the calling thread and a worker team);
+                         <= 0: the OpenMP default thread count (OMP_NUM_THREADS) */
   size_t chunk_bytes; /* weight bytes per streamed chunk; 0: 32 MiB */
   int ring_depth;     /* device staging slots for streamed chunks, in [2, 64]; 0: 8 */
   int pin_threads;    /* host threads that stage pageable weights into pinned memory
@@ -174,12 +175,13 @@ HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, i
 HETEGEN_API hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out);
 
 /* The CPU share alone (Sec. 3.2: the host cores compute the rows whose parameters
- * stay in host memory), on the calling thread's OpenMP team, no device involved:
+ * stay in host memory), on the calling thread and the library's CPU worker team (one
+ * job at a time; calls from several threads are serialised), no device involved:
  *   y[b * ldy + (j - r0)] = sum_k x[b * K + k] * W[j * K + k] + bias[j],
  *   j in [r0, r1), b < B,
  * x binary32 [B, K] host, W [N, K] host (pinned or pageable), bias host [N] or NULL,
  * y binary32 host.  Binary32 accumulation, 16-bit weights widened exactly.
- * threads <= 0: the OpenMP default.  B in [1, 8], K % 8 == 0, 0 <= r0 <= r1. */
+ * threads <= 0: the OpenMP default thread count.  B in [1, 8], K % 8 == 0, 0 <= r0 <= r1. */
 HETEGEN_API hetegen_status hetegen_cpu_linear(const float* x, int B, int K, const void* W_host, hetegen_dtype dtype,
                                               const void* bias_host, int r0, int r1, float* y, int ldy, int threads);
 

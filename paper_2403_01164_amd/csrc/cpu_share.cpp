@@ -12,11 +12,107 @@
 #include "cpu_share.h"
 
 #include <immintrin.h>
+#include <linux/futex.h>
 #include <omp.h>
+#include <stdlib.h>
 #include <string.h>
+#include <sys/syscall.h>
+#include <unistd.h>
+
+#include <atomic>
+#include <chrono>
+#include <climits>
+#include <mutex>
+#include <thread>
+#include <vector>
 
 namespace hg {
 namespace {
+
+// ---------------- worker team ----------------
+// The CPU shares of a decode step come ~1 ms apart, with the calling thread's kernel
+// and copy enqueues (and the parameter manager thread) in between.  An OpenMP team
+// keeps its workers spinning through such gaps (libgomp's default spin count), on
+// every core, and the calling thread's and the manager's work then waits for the
+// scheduler.  This team spins only briefly (kSpinUs) and then sleeps on a futex; the
+// caller takes part in every job.  One job runs at a time (jobs from several host
+// threads are serialised).
+class Team {
+ public:
+  static Team& get() {
+    static Team* t = new Team();  // never destroyed: its workers sleep until the process ends
+    return *t;
+  }
+  // fn(arg, g) for every g in [0, ngrains), on `threads` threads including the caller;
+  // grains are handed out in increasing order from a shared counter.
+  void run(int threads, int ngrains, void (*fn)(void*, int), void* arg) {
+    if (ngrains <= 0) return;
+    const int nw = std::min(threads, ngrains) - 1;
+    if (nw <= 0) {
+      for (int g = 0; g < ngrains; ++g) fn(arg, g);
+      return;
+    }
+    std::lock_guard<std::mutex> lk(run_mu_);
+    grow(nw);
+    fn_ = fn;
+    arg_ = arg;
+    ngrains_ = ngrains;
+    nw_ = nw;
+    next_.store(0, std::memory_order_relaxed);
+    left_.store((int)workers_.size(), std::memory_order_relaxed);  // every worker acknowledges the job
+    gen_.fetch_add(1, std::memory_order_seq_cst);
+    if (sleepers_.load(std::memory_order_seq_cst) > 0) syscall(SYS_futex, &gen_, FUTEX_WAKE_PRIVATE, INT_MAX, nullptr, nullptr, 0);
+    grains();
+    while (left_.load(std::memory_order_acquire) > 0) _mm_pause();
+  }
+
+ private:
+  Team() {
+    const char* e = getenv("HETEGEN_SPIN_US");
+    spin_us_ = e ? atoi(e) : kSpinUs;
+  }
+  static constexpr int kSpinUs = 20;
+  void grains() {
+    for (int g; (g = next_.fetch_add(1, std::memory_order_relaxed)) < ngrains_;) fn_(arg_, g);
+  }
+  void grow(int n) {
+    while ((int)workers_.size() < n) {
+      const int i = (int)workers_.size();
+      const uint32_t g0 = gen_.load(std::memory_order_relaxed);
+      workers_.emplace_back([this, i, g0] { work(i, g0); });
+      workers_.back().detach();
+    }
+  }
+  void work(int i, uint32_t seen) {
+    for (;;) {
+      uint32_t g = gen_.load(std::memory_order_acquire);
+      if (g == seen) {
+        const auto t0 = std::chrono::steady_clock::now();
+        while (g == seen && std::chrono::steady_clock::now() - t0 < std::chrono::microseconds(spin_us_)) {
+          for (int k = 0; k < 32; ++k) _mm_pause();
+          g = gen_.load(std::memory_order_acquire);
+        }
+      }
+      while (g == seen) {
+        sleepers_.fetch_add(1, std::memory_order_seq_cst);
+        if (gen_.load(std::memory_order_seq_cst) == seen)
+          syscall(SYS_futex, &gen_, FUTEX_WAIT_PRIVATE, seen, nullptr, nullptr, 0);
+        sleepers_.fetch_sub(1, std::memory_order_seq_cst);
+        g = gen_.load(std::memory_order_acquire);
+      }
+      seen = g;  // the next job: every worker acknowledged the previous one before it was published
+      if (i < nw_) grains();
+      left_.fetch_sub(1, std::memory_order_release);
+    }
+  }
+  std::mutex run_mu_;
+  std::vector<std::thread> workers_;
+  std::atomic<uint32_t> gen_{0};
+  std::atomic<int> sleepers_{0}, next_{0}, left_{0};
+  void (*fn_)(void*, int) = nullptr;
+  void* arg_ = nullptr;
+  int ngrains_ = 0, nw_ = 0, spin_us_ = kSpinUs;
+};
 
 // ---------------- portable fallback ----------------
 float f16_to_f32(uint16_t h) {
@@ -285,24 +381,35 @@ void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const
   int nt = (n + 7) / 8;
   if (nt > nt_max) nt = nt_max;
   if (nt < 1) nt = 1;
+  struct Job {
+    const float* x;
+    int B, K;
+    const uint16_t* W;
+    int dtype;
+    const uint16_t* bias;
+    int r0, r1, blocks;
+    float* y;
+    int ldy;
+  } job{x, B, K, W, dtype, bias, r0, r1, (n + 3) / 4, y, ldy};
   if (g_isa == ISA_SCALAR) {
-#pragma omp parallel for schedule(static) num_threads(nt)
-    for (int r = r0; r < r1; ++r) rows_scalar(x, B, K, W, dtype, bias, r0, r, r + 1, y, ldy);
+    Team::get().run(nt, n, [](void* a, int g) {
+      const Job& j = *(const Job*)a;
+      rows_scalar(j.x, j.B, j.K, j.W, j.dtype, j.bias, j.r0, j.r0 + g, j.r0 + g + 1, j.y, j.ldy);
+    }, &job);
     return;
   }
   // blocks of 4 rows handed out 8 at a time (32 rows, long sequential streams): a
   // core slowed by other work hands its remaining blocks to the others, which a
   // static split cannot (measured +5-38 % at batch 1 on the 16-core host).  Every
   // row is computed by one thread in the same order whatever the schedule.
-  const int blocks = (n + 3) / 4;
   constexpr int kGrain = 8;
-  const int grains = (blocks + kGrain - 1) / kGrain;
-#pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
-  for (int g = 0; g < grains; ++g) {
-    const int ba = g * kGrain, bb = ba + kGrain < blocks ? ba + kGrain : blocks;
-    if (dtype == 1) run_blocks_b<true>(g_isa, x, B, K, W, bias, r0, r1, ba, bb, y, ldy);
-    else run_blocks_b<false>(g_isa, x, B, K, W, bias, r0, r1, ba, bb, y, ldy);
-  }
+  const int grains = (job.blocks + kGrain - 1) / kGrain;
+  Team::get().run(nt, grains, [](void* a, int g) {
+    const Job& j = *(const Job*)a;
+    const int ba = g * kGrain, bb = ba + kGrain < j.blocks ? ba + kGrain : j.blocks;
+    if (j.dtype == 1) run_blocks_b<true>(g_isa, j.x, j.B, j.K, j.W, j.bias, j.r0, j.r1, ba, bb, j.y, j.ldy);
+    else run_blocks_b<false>(g_isa, j.x, j.B, j.K, j.W, j.bias, j.r0, j.r1, ba, bb, j.y, j.ldy);
+  }, &job);
 }
 
 }  // namespace hg

@@ -6,7 +6,8 @@ namespace hg {
 
 // y[b * ldy + (r - r0)] = sum_k x[b * K + k] * W[r * K + k] + bias[r]   for r in [r0, r1), b < B.
 // x: binary32 [B][K]; W: 16-bit rows (dtype 0 = fp16, 1 = bf16) with row stride K;
-// bias: 16-bit [N] or nullptr; y: binary32.  nthreads <= 0 uses the OpenMP default.
+// bias: 16-bit [N] or nullptr; y: binary32.  Runs on the calling thread and a worker team;
+// nthreads <= 0 uses the OpenMP default thread count.
 void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const uint16_t* bias, int r0, int r1,
                float* y, int ldy, int nthreads);
 
