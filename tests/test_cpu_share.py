@@ -90,3 +90,27 @@ def test_batch_rows_independent(dtype, K):
     for bb in range(B):
         one = hg.hetegen_cpu_linear(np.ascontiguousarray(xf[bb:bb + 1]), W.ctypes.data, b.ctypes.data, dtype, 0, N)
         assert np.array_equal(one[0], full[bb]), bb
+
+
+def test_calls_from_several_threads():
+    # the worker team runs one job at a time; concurrent callers get their own results
+    import threading
+    dtype, B, K, N = synth.BF16, 5, 520, 2051
+    x, W, b = _problem(B, K, N, dtype, "normal", seed=11)
+    xf = oracle.decode(x, dtype)
+    ref = hg.hetegen_cpu_linear(xf, W.ctypes.data, b.ctypes.data, dtype, 0, N)
+    bad = []
+
+    def worker(k):
+        for it in range(60):
+            r0, r1 = (k * 13 + it) % 40, N - (it * 7) % 50
+            y = hg.hetegen_cpu_linear(xf, W.ctypes.data, b.ctypes.data, dtype, r0, r1, threads=1 + (it + k) % 8)
+            if not np.array_equal(y, ref[:, r0:r1]):
+                bad.append((k, it))
+
+    ts = [threading.Thread(target=worker, args=(k,)) for k in range(4)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert not bad
