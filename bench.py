@@ -436,9 +436,11 @@ def main():
         if exec_mode == "persistent":
             kernel_label = "step_kernel<%s,%d,...>" % (tname, B)
         elif B == 1:
-            kernel_label = ("gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4> (out, fc2)" % (tname, H // 512, tname)
+            kernel_label = ("gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (tname, H // 512, tname)
                             if H in (512, 1024, 2048, 4096) else
-                            "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4> (out, fc2)" % (tname, tname))
+                            "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (tname, tname))
+        elif B == 2:
+            kernel_label = "gemv_kernel<%s,2,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,2> (out, fc2)" % (tname, tname)
         else:
             # from batch 5 on the LayerNorm of qkv and fc1 is its own launch (counted in the
             # time, not in the GEMV launches)

@@ -446,18 +446,18 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Batch-1 GEMV without a fused LayerNorm: x is read straight from L1/L2 inside
-// the task loop (it is the same 2*K bytes for every wavefront, so it stays
-// cached), which removes the LDS prologue and its barrier; the bias and residual
+// GEMV of NB <= 2 batch rows without a fused LayerNorm: x is read straight from
+// L1/L2 inside the task loop (it is the same NB*2*K bytes for every wavefront, so
+// it stays cached), which removes the LDS prologue and its barrier; the bias and residual
 // of a wavefront's rows are loaded once, ahead of its weight stream, into that
 // wavefront's slice of LDS, and lane 0 stores each finished row.  Each
 // lane accumulates its chunks in the same order as gemv_block, so both kernels
 // give bit-identical results.
 // ---------------------------------------------------------------------------
-template <class T, int U>
+template <class T, int U, int NB>
 __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
   // per wavefront: bias and residual of its rows (row j of the wave: local row wave + j*kWaves)
-  __shared__ float sbias[kWaves][kX1MaxRows], sres[kWaves][kX1MaxRows];
+  __shared__ float sbias[kWaves][kX1MaxRows], sres[kWaves][NB][kX1MaxRows];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int K = p.K, k8 = K >> 3, rpw = p.rpw;
   const int row_begin = blockIdx.x * rpw;
@@ -467,18 +467,21 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
   const int my_rg = nrows > wave ? (nrows - wave + kWaves - 1) / kWaves : 0;  // <= kX1MaxRows (launcher)
   const int ntask = my_rg * nseg;
   const uint16_t* W = (const uint16_t*)p.W;
-  const uint4* x = (const uint4*)p.x;
   const uint16_t* bias = (const uint16_t*)p.bias;
   const uint16_t* res = (const uint16_t*)p.resid;
   // bias and residual first: waiting for them later does not wait for the weights
-  float bj = 0.f, rj = 0.f;
+  float bj = 0.f, rj[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) rj[b] = 0.f;
   if (lane < my_rg) {
     const int row = row_begin + wave + lane * kWaves;
     if (bias) bj = T::to_f32(gmem(bias)[row]);
-    if (p.epi == EPI_RESID) rj = T::to_f32(gmem(res)[row]);
+    if (p.epi == EPI_RESID)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) rj[b] = T::to_f32(gmem(res)[(long long)b * p.ldr + row]);
   }
   struct Buf {
-    uint4 w[U], x[U];
+    uint4 w[U], x[NB][U];
   };
   auto load = [&](int t, Buf& f) {
     const int j = t / nseg, seg = t - j * nseg;
@@ -488,27 +491,38 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
 #pragma unroll
     for (int u = 0; u < U; ++u) f.w[u] = load_stream(wr + min(c0 + 64 * u, k8 - 1));
 #pragma unroll
-    for (int u = 0; u < U; ++u) f.x[u] = load_g16(x + min(c0 + 64 * u, k8 - 1));
+    for (int b = 0; b < NB; ++b) {
+      const uint4* xb = (const uint4*)((const uint16_t*)p.x + (long long)b * p.ldx);
+#pragma unroll
+      for (int u = 0; u < U; ++u) f.x[b][u] = load_g16(xb + min(c0 + 64 * u, k8 - 1));
+    }
   };
   Buf fa, fb;
   if (ntask > 0) load(0, fa);
   if (lane < my_rg) {
     sbias[wave][lane] = bj;
-    sres[wave][lane] = rj;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) sres[wave][b][lane] = rj[b];
   }
-  float acc = 0.f;
+  float acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = 0.f;
   auto compute = [&](int t, const Buf& f) {
     const int j = t / nseg, seg = t - j * nseg;
     const int c0 = seg * SEG + lane;
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (c0 + 64 * u < k8) acc = dot8<T>(f.w[u], f.x[u], acc);
+      if (c0 + 64 * u < k8)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) acc[b] = dot8<T>(f.w[u], f.x[b][u], acc[b]);
     if (seg == nseg - 1) {
-      const float s = wave_sum(acc);
-      acc = 0.f;
-      if (lane == 0) {
-        const int row = row_begin + wave + j * kWaves;
-        store_y<T>(p.y, row, p.y_f32, apply_epi(s + sbias[wave][j], p.epi, sres[wave][j]));
+      const int row = row_begin + wave + j * kWaves;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const float s = wave_sum(acc[b]);
+        acc[b] = 0.f;
+        if (lane == 0)
+          store_y<T>(p.y, (long long)b * p.ldy + row, p.y_f32, apply_epi(s + sbias[wave][j], p.epi, sres[wave][b][j]));
       }
     }
   };
@@ -914,22 +928,30 @@ const LdsInfo& lds_info() {
 constexpr int kTiledLdsBudget = 32768;  // bytes of x per tile in the K-tiled kernel
 constexpr int kDefaultGridCap = 1024;
 
+// Batches up to this size run linears without a fused LayerNorm on gemv_x1_kernel (x
+// read per wavefront from L1/L2) rather than staging x in LDS per workgroup (OPT-6.7B
+// shapes at B = 2: out 9.3 -> 8.6 us, fc2 25.9 -> 25.3 us; slower from B = 3 on, and
+// the register LayerNorm kernel only pays at B = 1).
+constexpr int kX1MaxB = 2;
+
 template <class T, int B>
 hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
   constexpr int R = Tile<B>::R, U = Tile<B>::U;
   const int cap = grid_cap > 0 ? grid_cap : kDefaultGridCap;
-  const bool ln_regs = B == 1 && p.ln && (p.K == 512 || p.K == 1024 || p.K == 2048 || p.K == 4096);
-  if (B == 1 && (!p.ln || ln_regs)) {
-    const long long units = (p.rows + kWaves - 1) / kWaves;
-    const long long per = std::min<long long>((units + cap - 1) / cap, kX1MaxRows);
-    p.rpw = (int)(per * kWaves);
-    const int grid = (int)((p.rows + p.rpw - 1) / p.rpw);
-    if (!p.ln) hipLaunchKernelGGL((gemv_x1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
-    else if (p.K == 512) hipLaunchKernelGGL((gemv_ln1_kernel<T, 1>), dim3(grid), dim3(kThreads), 0, s, p);
-    else if (p.K == 1024) hipLaunchKernelGGL((gemv_ln1_kernel<T, 2>), dim3(grid), dim3(kThreads), 0, s, p);
-    else if (p.K == 2048) hipLaunchKernelGGL((gemv_ln1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL((gemv_ln1_kernel<T, 8>), dim3(grid), dim3(kThreads), 0, s, p);
-    return hipGetLastError();
+  if constexpr (B <= kX1MaxB) {
+    const bool ln_regs = B == 1 && p.ln && (p.K == 512 || p.K == 1024 || p.K == 2048 || p.K == 4096);
+    if (!p.ln || ln_regs) {
+      const long long units = (p.rows + kWaves - 1) / kWaves;
+      const long long per = std::min<long long>((units + cap - 1) / cap, kX1MaxRows);
+      p.rpw = (int)(per * kWaves);
+      const int grid = (int)((p.rows + p.rpw - 1) / p.rpw);
+      if (!p.ln) hipLaunchKernelGGL((gemv_x1_kernel<T, 4, B>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (p.K == 512) hipLaunchKernelGGL((gemv_ln1_kernel<T, 1>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (p.K == 1024) hipLaunchKernelGGL((gemv_ln1_kernel<T, 2>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (p.K == 2048) hipLaunchKernelGGL((gemv_ln1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
+      else hipLaunchKernelGGL((gemv_ln1_kernel<T, 8>), dim3(grid), dim3(kThreads), 0, s, p);
+      return hipGetLastError();
+    }
   }
   // contiguous row blocks of a multiple of R*kWaves rows, at most `cap` blocks; a block
   // that needs much LDS also caps the grid at the workgroups that fit at once (more
