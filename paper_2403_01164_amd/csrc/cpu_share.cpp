@@ -372,6 +372,10 @@ const char* cpu_share_isa() {
   return g_isa == ISA_AVX512 ? "avx512" : g_isa == ISA_AVX2 ? "avx2" : "scalar";
 }
 
+void team_for(int threads, int ngrains, void (*fn)(void*, int), void* arg) {
+  Team::get().run(threads > 0 ? threads : omp_get_max_threads(), ngrains, fn, arg);
+}
+
 void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const uint16_t* bias, int r0, int r1,
                float* y, int ldy, int nthreads) {
   const int n = r1 - r0;

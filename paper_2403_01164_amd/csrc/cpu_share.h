@@ -11,6 +11,12 @@ namespace hg {
 void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const uint16_t* bias, int r0, int r1,
                float* y, int ldy, int nthreads);
 
+// fn(arg, g) for g in [0, ngrains) on the CPU share's worker team (`threads` threads
+// including the caller; <= 0: the OpenMP default count), grains handed out in
+// increasing order.  For other host-side work that must not leave a second team of
+// threads spinning beside the CPU share's.
+void team_for(int threads, int ngrains, void (*fn)(void*, int), void* arg);
+
 // Instruction set the CPU share dispatches to on this host ("avx512", "avx2", "scalar").
 const char* cpu_share_isa();
 

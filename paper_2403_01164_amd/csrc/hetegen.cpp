@@ -1248,12 +1248,24 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
     return fail(ctx, HETEGEN_ERR_OOM, "probe cache-flush buffer");
   }
   uint64_t flush_sink = 0;
+  // read on the CPU share's own worker team (a second team would still be spinning
+  // when the timed pass starts)
+  struct Flush {
+    const uint64_t* p;
+    long long n;
+    uint64_t part[64];
+  } fl{flush.data(), (long long)flush.size(), {}};
+  enum { kFlushGrains = 64 };
   auto flush_caches = [&](int) {
-    const long long n = (long long)flush.size();
-    uint64_t acc = 0;
-#pragma omp parallel for schedule(static) reduction(^ : acc)
-    for (long long i = 0; i < n; i += 8) acc ^= flush[i];  // one word per 64-byte line
-    flush_sink ^= acc;
+    hg::team_for(ctx->cpu_threads, kFlushGrains, [](void* a, int g) {
+      Flush& f = *(Flush*)a;
+      const long long per = (f.n / kFlushGrains + 7) & ~7LL;
+      const long long b = per * g, e = std::min(f.n, b + per);
+      uint64_t acc = 0;
+      for (long long i = b; i < e; i += 8) acc ^= f.p[i];  // one word per 64-byte line
+      f.part[g] = acc;
+    }, &fl);
+    for (int g = 0; g < kFlushGrains; ++g) flush_sink ^= fl.part[g];
   };
   std::vector<double> tc;
   for (int r = -1; r < reps; ++r) {  // one untimed pass first: threads up, TLBs warm
