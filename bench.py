@@ -184,7 +184,7 @@ def main():
     ap.add_argument("--no-alpha-bench", dest="alpha_bench", action="store_false",
                     help="keep the closed-form CPU fractions (default for streamed linears: refine them with the "
                          "step-level alpha benchmark, Sec. 4.4, and also time the closed-form fractions)")
-    ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: OpenMP default)")
+    ap.add_argument("--threads", type=int, default=0, help="CPU-share threads (0: the OpenMP default count, OMP_NUM_THREADS)")
     ap.add_argument("--pageable", action="store_true",
                     help="weights in plain pageable host memory (transparent huge pages), streamed through the "
                          "hybrid pin || transfer path (Sec. 4.2); biases stay pinned")
