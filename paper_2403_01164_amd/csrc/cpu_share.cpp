@@ -57,9 +57,9 @@ class Team {
     fn_ = fn;
     arg_ = arg;
     ngrains_ = ngrains;
-    nw_ = nw;
+    nw_ = std::min(nw, nworkers_);  // fewer if threads could not be created
     next_.store(0, std::memory_order_relaxed);
-    left_.store((int)workers_.size(), std::memory_order_relaxed);  // every worker acknowledges the job
+    left_.store(nworkers_, std::memory_order_relaxed);  // every worker acknowledges the job
     gen_.fetch_add(1, std::memory_order_seq_cst);
     if (sleepers_.load(std::memory_order_seq_cst) > 0) syscall(SYS_futex, &gen_, FUTEX_WAKE_PRIVATE, INT_MAX, nullptr, nullptr, 0);
     grains();
@@ -76,11 +76,16 @@ class Team {
     for (int g; (g = next_.fetch_add(1, std::memory_order_relaxed)) < ngrains_;) fn_(arg_, g);
   }
   void grow(int n) {
-    while ((int)workers_.size() < n) {
-      const int i = (int)workers_.size();
+    while (nworkers_ < n) {
+      const int i = nworkers_;
       const uint32_t g0 = gen_.load(std::memory_order_relaxed);
-      workers_.emplace_back([this, i, g0] { work(i, g0); });
-      workers_.back().detach();
+      try {
+        std::thread t([this, i, g0] { work(i, g0); });
+        t.detach();
+      } catch (...) {
+        return;  // no more threads: the job runs on those there are
+      }
+      ++nworkers_;
     }
   }
   void work(int i, uint32_t seen) {
@@ -106,7 +111,7 @@ class Team {
     }
   }
   std::mutex run_mu_;
-  std::vector<std::thread> workers_;
+  int nworkers_ = 0;  // detached worker threads
   std::atomic<uint32_t> gen_{0};
   std::atomic<int> sleepers_{0}, next_{0}, left_{0};
   void (*fn_)(void*, int) = nullptr;
