@@ -237,7 +237,7 @@ def test_argument_errors(ctx):
     (7168, 28672, synth.F16, 0.6, False),    # OPT-30B fc2, streamed + CPU
     (36864, 9216, synth.BF16, 0.3, False),   # OPT-66B fc1 bf16, streamed + CPU
 ])
-@pytest.mark.parametrize("B", [1, 4, 8])
+@pytest.mark.parametrize("B", [1, 2, 4, 8])
 def test_full_size_opt_linears(ctx, N, K, dtype, alpha, resident, B):
     p = Problem(ctx, B, K, N, dtype, seed=N + K)
     try:
