@@ -695,7 +695,7 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
     TRY(next_chunk(j.n_cpu == 0, &did));
     if (!did) break;
   }
-  // 3. CPU rows on the calling thread's OpenMP team
+  // 3. CPU rows on the calling thread and the CPU share's worker team
   if (j.n_cpu > 0) {
     // the previous import kernel may still read y_host (it precedes ev_x in stream
     // order, so this wait is part of the wait for the input)
