@@ -437,7 +437,7 @@ def main():
             kernel_label = "step_kernel<%s,%d,...>" % (tname, B)
         elif B == 1:
             kernel_label = ("gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (tname, H // 512, tname)
-                            if H in (512, 1024, 2048, 4096) else
+                            if H % 512 == 0 and H // 512 in (1, 2, 4, 5, 8, 10, 14) else
                             "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (tname, tname))
         elif B == 2:
             kernel_label = "gemv_kernel<%s,2,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,2> (out, fc2)" % (tname, tname)

@@ -543,7 +543,7 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Batch-1 GEMV with a fused LayerNorm for K = 512 * NC (NC <= 8): every wavefront
+// Batch-1 GEMV with a fused LayerNorm for K = 512 * NC (NC <= 14): every wavefront
 // loads the whole input row into registers (lane l holds the 16-byte chunks
 // l + 64u, exactly the chunks it multiplies in every row), normalises it there and
 // keeps it for all its rows: no LDS staging and no workgroup barrier.  The
@@ -939,17 +939,23 @@ hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
   constexpr int R = Tile<B>::R, U = Tile<B>::U;
   const int cap = grid_cap > 0 ? grid_cap : kDefaultGridCap;
   if constexpr (B <= kX1MaxB) {
-    const bool ln_regs = B == 1 && p.ln && (p.K == 512 || p.K == 1024 || p.K == 2048 || p.K == 4096);
+    // K = 512 * NC for the NC instantiated below (hidden sizes of OPT-350M .. OPT-30B); at
+    // NC = 18 (9216) the row no longer fits the registers well and the LDS kernel is as fast
+    const int nc = p.K % 512 == 0 ? p.K / 512 : 0;
+    const bool ln_regs = B == 1 && p.ln && (nc == 1 || nc == 2 || nc == 4 || nc == 5 || nc == 8 || nc == 10 || nc == 14);
     if (!p.ln || ln_regs) {
       const long long units = (p.rows + kWaves - 1) / kWaves;
       const long long per = std::min<long long>((units + cap - 1) / cap, kX1MaxRows);
       p.rpw = (int)(per * kWaves);
       const int grid = (int)((p.rows + p.rpw - 1) / p.rpw);
       if (!p.ln) hipLaunchKernelGGL((gemv_x1_kernel<T, 4, B>), dim3(grid), dim3(kThreads), 0, s, p);
-      else if (p.K == 512) hipLaunchKernelGGL((gemv_ln1_kernel<T, 1>), dim3(grid), dim3(kThreads), 0, s, p);
-      else if (p.K == 1024) hipLaunchKernelGGL((gemv_ln1_kernel<T, 2>), dim3(grid), dim3(kThreads), 0, s, p);
-      else if (p.K == 2048) hipLaunchKernelGGL((gemv_ln1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
-      else hipLaunchKernelGGL((gemv_ln1_kernel<T, 8>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (nc == 1) hipLaunchKernelGGL((gemv_ln1_kernel<T, 1>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (nc == 2) hipLaunchKernelGGL((gemv_ln1_kernel<T, 2>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (nc == 4) hipLaunchKernelGGL((gemv_ln1_kernel<T, 4>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (nc == 5) hipLaunchKernelGGL((gemv_ln1_kernel<T, 5>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (nc == 8) hipLaunchKernelGGL((gemv_ln1_kernel<T, 8>), dim3(grid), dim3(kThreads), 0, s, p);
+      else if (nc == 10) hipLaunchKernelGGL((gemv_ln1_kernel<T, 10>), dim3(grid), dim3(kThreads), 0, s, p);
+      else hipLaunchKernelGGL((gemv_ln1_kernel<T, 14>), dim3(grid), dim3(kThreads), 0, s, p);
       return hipGetLastError();
     }
   }

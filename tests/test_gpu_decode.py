@@ -280,6 +280,25 @@ def test_persistent_opt67b_shapes_two_layers(ctx):
         m.free()
 
 
+@pytest.mark.parametrize("H", [2560, 5120, 7168])
+def test_register_layernorm_hidden_sizes_bit_identical_to_persistent(ctx, H):
+    # the register-LayerNorm GEMV at K = 512 * NC for NC = 5, 10, 14 (OPT-2.7B/13B/30B hidden
+    # sizes) gives the workgroup kernel's bits, and matches the oracle teacher-forced
+    dtype, L = synth.F16, 1
+    m = Model(ctx, L, H, 4 * H, dtype, 0.0, 1, max_batch=1)
+    try:
+        x = synth.normal((1, H), dtype, 0, synth.act_id(0))
+        hg.hetegen_model_set_exec(m.m, hg.EXEC_EAGER)
+        eager, tr = m.step(x, trace=True)
+        last, _ = m.check_teacher_forced(x, tr)
+        assert np.array_equal(eager, last)
+        hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT)
+        assert np.array_equal(m.step(x), eager)
+        assert hg.hetegen_model_last_exec(m.m) == hg.EXEC_PERSISTENT
+    finally:
+        m.free()
+
+
 def test_barrier_wait_that_gives_up_is_reported(ctx):
     # a spin limit of one poll makes waits give up (outputs undefined, kernel still
     # drains); the next step on the model must report the failure
