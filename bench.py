@@ -84,6 +84,46 @@ def counter_traffic(model, dt, B):
 
 
 
+def host_info(torch):
+    """Machine the line was measured on: CPU model, cores, NUMA nodes and the GPU's node,
+    GPU name and compute units, ROCm / HIP / torch versions (None where unreadable)."""
+    def read(path):
+        try:
+            with open(path) as f:
+                return f.read().strip()
+        except OSError:
+            return None
+    cpu, phys = None, set()
+    txt = read("/proc/cpuinfo") or ""
+    pid = cid = None
+    for line in txt.splitlines():
+        k, _, v = line.partition(":")
+        k, v = k.strip(), v.strip()
+        if k == "model name" and cpu is None:
+            cpu = v
+        elif k == "physical id":
+            pid = v
+        elif k == "core id":
+            cid = v
+            phys.add((pid, cid))
+    nodes = sorted(int(d[4:]) for d in os.listdir("/sys/devices/system/node")
+                   if d.startswith("node") and d[4:].isdigit()) if os.path.isdir("/sys/devices/system/node") else []
+    info = {"cpu": cpu, "physical_cores": len(phys) or None, "logical_cpus": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0)), "numa_nodes": len(nodes) or None,
+            "rocm": read("/opt/rocm/.info/version"), "hip": torch.version.hip, "torch": torch.__version__,
+            "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
+    try:
+        pr = torch.cuda.get_device_properties(0)
+        info["gpu"] = "%s (%s, %d CUs)" % (pr.name, pr.gcnArchName, pr.multi_processor_count)
+        bdf = "%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)
+        node = read("/sys/bus/pci/devices/%s/numa_node" % bdf)
+        info["gpu_pci"] = bdf
+        info["gpu_numa_node"] = int(node) if node is not None and node.lstrip("-").isdigit() else None
+    except Exception:
+        pass
+    return info
+
+
 def single_linear(args, torch, synth, hg):
     """Latency of hetegen_linear on one shape (the single-linear configuration): for each
     CPU fraction and placement, host wall time from the call to the end of the GPU work
@@ -155,7 +195,7 @@ def single_linear(args, torch, synth, hg):
         "config": {"workload": "single Linear [%d,%d] fp16, batch %d, CPU fractions 0/.25/.5/1, resident and "
                                "streamed; %d weight copies rotated (%.0f MB)" % (N, K, B, ncopy, ncopy * wb / 1e6)},
         "probe_GBps": {k: round(v / 1e9, 2) for k, v in probe.items()},
-        "results": rows}))
+        "results": rows, "host": host_info(torch)}))
     for w in Wh:
         hg.hetegen_host_free(ctx, w)
     hg.hetegen_host_free(ctx, bh)
@@ -411,6 +451,7 @@ def main():
     }
     if schedule:
         result["config"]["schedule"] = schedule
+    result["host"] = host_info(torch)
 
     exec_mode = {1: "persistent", 2: "graph", 3: "eager"}.get(hg.hetegen_model_last_exec(model), "?")
     result["config"]["exec"] = exec_mode
