@@ -537,6 +537,11 @@ def main():
             "h2d_GBps_over_step": round(h2d_b / (ms_step * 1e-3) / 1e9, 2),
             "h2d_frac_of_probe_link": round(h2d_b / (ms_step * 1e-3) / v_com, 4),
             "cpu_GBps_over_step": round(cpu_b / (ms_step * 1e-3) / 1e9, 2),
+            # host-memory bytes of the step: the CPU share reads its rows once; a streamed row is
+            # read once by the DMA from pinned memory, or, from pageable memory, read and written
+            # by the pin team first (three passes)
+            "host_memory_GBps_over_step": round((cpu_b + h2d_b * (3 if args.pageable else 1)) /
+                                                (ms_step * 1e-3) / 1e9, 2),
             "ideal_ms_per_step": round(ideal_s * 1e3, 3),
             "frac_of_ideal": round(ideal_s * 1e3 / ms_step, 4),
             "busy_frac": {"cpu": round(prof["cpu_ms"] / wall_ms, 4), "io": round(prof["h2d_ms"] / wall_ms, 4),
