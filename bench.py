@@ -113,6 +113,16 @@ def host_info(torch):
             "rocm": read("/opt/rocm/.info/version"), "hip": torch.version.hip, "torch": torch.__version__,
             "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
     try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        v = ctypes.c_int(0)
+        if hip.hipDriverGetVersion(ctypes.byref(v)) == 0:
+            info["hip_driver_version"] = v.value
+        if hip.hipRuntimeGetVersion(ctypes.byref(v)) == 0:
+            info["hip_runtime_version"] = v.value
+    except OSError:
+        pass
+    info["amdgpu_module"] = read("/sys/module/amdgpu/version")
+    try:
         pr = torch.cuda.get_device_properties(0)
         info["gpu"] = "%s (%s, %d CUs)" % (pr.name, pr.gcnArchName, pr.multi_processor_count)
         bdf = "%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)
@@ -187,6 +197,34 @@ def single_linear(args, torch, synth, hg):
             log("alpha %.2f %s: median %.1f us (p10 %.1f, p90 %.1f), floor %.1f us (%s)" %
                 (alpha, "resident" if resident else "streamed", q(0.5), q(0.1), q(0.9), floor_us, bound))
     head = rows[0]
+    cpu_base = None
+    if not args.no_cpu_baseline:
+        # the oracle on the same linear and weight copies, with the default OpenMP team and
+        # single-threaded, about 3 s each
+        import oracle
+        xh = synth.normal((B, K), dt, 0, synth.act_id(0))
+        yh = np.empty((B, N), np.float32)
+
+        def oracle_rate():
+            n, t = 0, 0.0
+            while t < 3.0:
+                c0 = time.perf_counter()
+                oracle.linear_ptr(xh.ctypes.data, K, B, K, Wh[n % ncopy], N, dt, bh, yh)
+                t += time.perf_counter() - c0
+                n += 1
+            return n, t, n * wb / t / 1e9
+        gomp = ctypes.CDLL("libgomp.so.1")
+        threads = gomp.omp_get_max_threads()
+        n_all, t_all, v_all = oracle_rate()
+        gomp.omp_set_num_threads(1)
+        n_one, t_one, v_one = oracle_rate()
+        gomp.omp_set_num_threads(threads)
+        cpu_base = {"value": round(wb / (t_all / n_all) / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+                    "sample": "%d calls on the %d weight copies, %.1f s" % (n_all, ncopy, t_all),
+                    "us_per_call": round(t_all / n_all * 1e6, 1),
+                    "single_thread": {"value": round(v_one, 3), "unit": "GB/s", "us_per_call": round(t_one / n_one * 1e6, 1),
+                                      "sample": "%d calls, %.1f s" % (n_one, t_one)}}
+        log("oracle: %.2f GB/s on %d threads, %.2f GB/s single-threaded" % (v_all, threads, v_one))
     print(json.dumps({
         "metric": "single-linear latency (us per call, host wall to end of GPU work)",
         "value": head["median_us"], "unit": "us", "n_gpus": 1, "steps": args.linear_reps, "warmup": 10,
@@ -195,7 +233,7 @@ def single_linear(args, torch, synth, hg):
         "config": {"workload": "single Linear [%d,%d] fp16, batch %d, CPU fractions 0/.25/.5/1, resident and "
                                "streamed; %d weight copies rotated (%.0f MB)" % (N, K, B, ncopy, ncopy * wb / 1e6)},
         "probe_GBps": {k: round(v / 1e9, 2) for k, v in probe.items()},
-        "results": rows, "host": host_info(torch)}))
+        "results": rows, "cpu_baseline": cpu_base, "host": host_info(torch)}))
     for w in Wh:
         hg.hetegen_host_free(ctx, w)
     hg.hetegen_host_free(ctx, bh)
