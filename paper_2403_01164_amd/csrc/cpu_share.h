@@ -17,6 +17,10 @@ void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const
 // threads spinning beside the CPU share's.
 void team_for(int threads, int ngrains, void (*fn)(void*, int), void* arg);
 
+// Streamed chunks queued by the library's contexts (+n when planned, -1 when consumed or
+// dropped): while none is queued, the worker team spins longer between jobs.
+void team_streamed_chunks(long long delta);
+
 // Instruction set the CPU share dispatches to on this host ("avx512", "avx2", "scalar").
 const char* cpu_share_isa();
 

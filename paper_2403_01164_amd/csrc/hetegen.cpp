@@ -534,10 +534,12 @@ void plan_chunks(hetegen_ctx* ctx, const void* W_host, int n_gpu, int K, int dty
   const int cr = chunk_rows_for(ctx, K, dtype);
   {
     std::lock_guard<std::mutex> lk(ctx->mu);
-    for (int r0 = 0; r0 < n_gpu; r0 += cr) {
+    long long n = 0;
+    for (int r0 = 0; r0 < n_gpu; r0 += cr, ++n) {
       int nr = std::min(cr, n_gpu - r0);
       ctx->jobs.push_back({(const char*)W_host + (size_t)r0 * row, (size_t)nr * row, pageable, host_wait});
     }
+    hg::team_streamed_chunks(n);
   }
   ctx->cv.notify_all();
 }
@@ -569,6 +571,7 @@ void pop_chunk(hetegen_ctx* ctx) {
     std::lock_guard<std::mutex> lk(ctx->mu);
     ctx->jobs.pop_front();
     ctx->head++;
+    hg::team_streamed_chunks(-1);
   }
   ctx->cv.notify_all();
 }
@@ -578,6 +581,7 @@ void pop_chunk(hetegen_ctx* ctx) {
 void reset_pipeline(hetegen_ctx* ctx) {
   std::unique_lock<std::mutex> lk(ctx->mu);
   ctx->cv.wait(lk, [&] { return !ctx->busy; });
+  hg::team_streamed_chunks(-(long long)ctx->jobs.size());
   ctx->jobs.clear();
   ctx->head = ctx->copy_enq;
   ctx->failed = false;
@@ -830,6 +834,8 @@ hetegen_status hetegen_destroy(hetegen_ctx* ctx) {
     ctx->cv.notify_all();
     ctx->mgr.join();
   }
+  hg::team_streamed_chunks(-(long long)ctx->jobs.size());  // chunks a failed call left queued
+  ctx->jobs.clear();
   ctx->team.shutdown();
   (void)hipSetDevice(ctx->device);
   (void)hipDeviceSynchronize();
