@@ -228,6 +228,24 @@ def test_opt67b_shape_two_layers_resident(ctx, B):
         m.free()
 
 
+def test_opt67b_full_model_resident_as_benchmarked(ctx):
+    # the benchmark's workload itself: all 32 OPT-6.7B-shaped layers resident, batch 1, the
+    # default execution mode; every one of the 128 linears checked against the oracle on the
+    # input it was given, and the untraced step gives the same bits
+    dtype, L, H, F = synth.F16, 32, 4096, 16384
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
+    try:
+        x = synth.normal((1, H), dtype, 0, synth.act_id(0))
+        out, tr = m.step(x, trace=True)
+        assert hg.hetegen_model_last_exec(m.m) == 3  # eager per-linear launches
+        last, worst = m.check_teacher_forced(x, tr)
+        assert np.array_equal(out, last)
+        assert np.array_equal(m.step(x), out)
+        print("32 layers: worst per-linear relative error %.3g" % worst)
+    finally:
+        m.free()
+
+
 def test_opt13b_shape_one_layer_hetero(ctx):
     dtype, L, H, F = synth.F16, 1, 5120, 20480
     m = Model(ctx, L, H, F, dtype, [0.62, 0.6, 0.63, 0.61], 0, max_batch=1)
