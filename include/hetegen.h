@@ -41,8 +41,10 @@ typedef enum {
   HETEGEN_ERR_INVALID_ARG = 1, /* null pointer, bad size, alpha outside [0,1] or not finite */
   HETEGEN_ERR_NOT_PINNED = 2,  /* a host weight buffer is not page-locked host memory */
   HETEGEN_ERR_UNSUPPORTED = 3, /* K % 8 != 0, B outside [1, 8], misaligned pointer, dtype mix */
-  HETEGEN_ERR_OOM = 4,         /* device or pinned host allocation failed */
-  HETEGEN_ERR_HIP = 5          /* a HIP runtime call failed (code in the message) */
+  HETEGEN_ERR_OOM = 4,         /* device, pinned or host allocation failed */
+  HETEGEN_ERR_HIP = 5,         /* a HIP runtime call failed (code in the message) */
+  HETEGEN_ERR_INTERNAL = 6     /* any other host-side failure (message says what); no call
+                                  lets an exception cross this interface */
 } hetegen_status;
 
 typedef enum { HETEGEN_F16 = 0, HETEGEN_BF16 = 1, HETEGEN_F32 = 2 } hetegen_dtype;

@@ -21,11 +21,11 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhetegen.so")
 
 F16, BF16, F32 = 0, 1, 2
-OK, ERR_INVALID_ARG, ERR_NOT_PINNED, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP = range(6)
+OK, ERR_INVALID_ARG, ERR_NOT_PINNED, ERR_UNSUPPORTED, ERR_OOM, ERR_HIP, ERR_INTERNAL = range(7)
 PLAN_APPROX = 1
 EXEC_AUTO, EXEC_PERSISTENT, EXEC_GRAPH, EXEC_EAGER = 0, 1, 2, 3
 BENCH_CROSSING, BENCH_WALL = 0, 1
-STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "NOT_PINNED", 3: "UNSUPPORTED", 4: "OOM", 5: "HIP"}
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "NOT_PINNED", 3: "UNSUPPORTED", 4: "OOM", 5: "HIP", 6: "INTERNAL"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError("libhetegen.so is not built: run `python paper_2403_01164_amd/build.py` "

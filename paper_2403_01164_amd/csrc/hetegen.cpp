@@ -31,8 +31,10 @@
 #include <chrono>
 #include <condition_variable>
 #include <deque>
+#include <exception>
 #include <map>
 #include <mutex>
+#include <new>
 #include <string>
 #include <thread>
 #include <vector>
@@ -260,6 +262,34 @@ hetegen_status fail(hetegen_ctx* ctx, hetegen_status code, const char* fmt, ...)
   if (ctx) ctx->err = buf;
   else g_create_error = buf;
   return code;
+}
+
+// Every exported call returns a status and lets no exception cross the C ABI: host
+// allocation failures (vectors, queues, messages) become HETEGEN_ERR_OOM, anything else
+// HETEGEN_ERR_INTERNAL; building the message may itself fail, so it is best-effort.
+template <class F>
+hetegen_status api_guard(hetegen_ctx* ctx, F&& f) noexcept {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    try {
+      fail(ctx, HETEGEN_ERR_OOM, "host memory exhausted");
+    } catch (...) {
+    }
+    return HETEGEN_ERR_OOM;
+  } catch (const std::exception& e) {
+    try {
+      fail(ctx, HETEGEN_ERR_INTERNAL, "internal error: %s", e.what());
+    } catch (...) {
+    }
+    return HETEGEN_ERR_INTERNAL;
+  } catch (...) {
+    try {
+      fail(ctx, HETEGEN_ERR_INTERNAL, "internal error");
+    } catch (...) {
+    }
+    return HETEGEN_ERR_INTERNAL;
+  }
 }
 
 #define HIPCHK(ctx, expr)                                                                           \
@@ -747,228 +777,240 @@ hetegen_status finish_call(hetegen_ctx* ctx, Clock::time_point t0) {
 extern "C" {
 
 hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
-  if (!out) return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "out is NULL");
-  *out = nullptr;
-  hetegen_config c{};
-  if (cfg) c = *cfg;
-  if (c.ring_depth == 0) c.ring_depth = kDefaultRing;
-  if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunk;
-  if (c.ring_depth < 2 || c.ring_depth > 64)
-    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "ring_depth %d outside [2, 64]", c.ring_depth);
-  if (c.chunk_bytes < 4096 || (c.chunk_bytes & 15u))
-    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "chunk_bytes %zu must be >= 4096 and a multiple of 16",
-                c.chunk_bytes);
-  if (c.pin_threads == 0) c.pin_threads = kDefaultPinThreads;
-  if (c.pin_ring == 0) c.pin_ring = kDefaultPinRing;
-  if (c.pin_threads > 64 || c.pin_ring < 2 || c.pin_ring > 64)
-    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "pin_threads %d must be <= 64 and pin_ring %d in [2, 64]",
-                c.pin_threads, c.pin_ring);
-  int ndev = 0;
-  hipError_t e = hipGetDeviceCount(&ndev);
-  if (e != hipSuccess || ndev <= 0) {
-    (void)hipGetLastError();
-    return fail(nullptr, HETEGEN_ERR_HIP, "no HIP device (%s)", hipGetErrorString(e));
-  }
-  if (c.device < 0 || c.device >= ndev)
-    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "device %d outside [0, %d)", c.device, ndev);
-  if (c.numa_node < 0 || c.numa_node > 1024)
-    return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "numa_node %d outside [0, 1024]", c.numa_node);
-  if (c.numa_node > 0) {
-    char path[64];
-    snprintf(path, sizeof path, "/sys/devices/system/node/node%d", c.numa_node - 1);
-    if (access(path, F_OK) != 0)
-      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "NUMA node %d does not exist", c.numa_node - 1);
-  }
-  hetegen_ctx* ctx = new hetegen_ctx();
-  ctx->device = c.device;
-  ctx->cpu_threads = c.cpu_threads;
-  ctx->chunk_bytes = c.chunk_bytes;
-  ctx->ring = c.ring_depth;
-  ctx->pin_threads = c.pin_threads < 0 ? -1 : c.pin_threads;
-  ctx->pin_ring = c.pin_ring;
-  ctx->numa_node = c.numa_node - 1;
-  auto bail = [&](hetegen_status st) {
-    g_create_error = ctx->err;
-    hetegen_destroy(ctx);
-    return st;
-  };
-  if (hipSetDevice(c.device) != hipSuccess) return bail(fail(ctx, HETEGEN_ERR_HIP, "hipSetDevice(%d)", c.device));
-  if (hipStreamCreateWithFlags(&ctx->copy_stream, hipStreamNonBlocking) != hipSuccess ||
-      hipStreamCreateWithFlags(&ctx->capture_stream, hipStreamNonBlocking) != hipSuccess)
-    return bail(fail(ctx, HETEGEN_ERR_HIP, "stream creation failed"));
-  if (hipEventCreateWithFlags(&ctx->ev_x, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->ev_y, hipEventDisableTiming) != hipSuccess)
-    return bail(fail(ctx, HETEGEN_ERR_HIP, "event creation failed"));
-  ctx->slot.assign(c.ring_depth, nullptr);
-  ctx->ev_ready.assign(c.ring_depth, nullptr);
-  ctx->ev_free.assign(c.ring_depth, nullptr);
-  for (int i = 0; i < c.ring_depth; ++i) {
-    if (hipMalloc(&ctx->slot[i], c.chunk_bytes) != hipSuccess) {
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!out) return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    hetegen_config c{};
+    if (cfg) c = *cfg;
+    if (c.ring_depth == 0) c.ring_depth = kDefaultRing;
+    if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunk;
+    if (c.ring_depth < 2 || c.ring_depth > 64)
+      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "ring_depth %d outside [2, 64]", c.ring_depth);
+    if (c.chunk_bytes < 4096 || (c.chunk_bytes & 15u))
+      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "chunk_bytes %zu must be >= 4096 and a multiple of 16",
+                  c.chunk_bytes);
+    if (c.pin_threads == 0) c.pin_threads = kDefaultPinThreads;
+    if (c.pin_ring == 0) c.pin_ring = kDefaultPinRing;
+    if (c.pin_threads > 64 || c.pin_ring < 2 || c.pin_ring > 64)
+      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "pin_threads %d must be <= 64 and pin_ring %d in [2, 64]",
+                  c.pin_threads, c.pin_ring);
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess || ndev <= 0) {
       (void)hipGetLastError();
-      ctx->slot[i] = nullptr;
-      return bail(fail(ctx, HETEGEN_ERR_OOM, "staging slot of %zu bytes", c.chunk_bytes));
+      return fail(nullptr, HETEGEN_ERR_HIP, "no HIP device (%s)", hipGetErrorString(e));
     }
-    if (hipEventCreateWithFlags(&ctx->ev_ready[i], hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&ctx->ev_free[i], hipEventDisableTiming | hipEventBlockingSync) != hipSuccess)
+    if (c.device < 0 || c.device >= ndev)
+      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "device %d outside [0, %d)", c.device, ndev);
+    if (c.numa_node < 0 || c.numa_node > 1024)
+      return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "numa_node %d outside [0, 1024]", c.numa_node);
+    if (c.numa_node > 0) {
+      char path[64];
+      snprintf(path, sizeof path, "/sys/devices/system/node/node%d", c.numa_node - 1);
+      if (access(path, F_OK) != 0)
+        return fail(nullptr, HETEGEN_ERR_INVALID_ARG, "NUMA node %d does not exist", c.numa_node - 1);
+    }
+    hetegen_ctx* ctx = new hetegen_ctx();
+    ctx->device = c.device;
+    ctx->cpu_threads = c.cpu_threads;
+    ctx->chunk_bytes = c.chunk_bytes;
+    ctx->ring = c.ring_depth;
+    ctx->pin_threads = c.pin_threads < 0 ? -1 : c.pin_threads;
+    ctx->pin_ring = c.pin_ring;
+    ctx->numa_node = c.numa_node - 1;
+    auto bail = [&](hetegen_status st) {
+      g_create_error = ctx->err;
+      hetegen_destroy(ctx);
+      return st;
+    };
+    if (hipSetDevice(c.device) != hipSuccess) return bail(fail(ctx, HETEGEN_ERR_HIP, "hipSetDevice(%d)", c.device));
+    if (hipStreamCreateWithFlags(&ctx->copy_stream, hipStreamNonBlocking) != hipSuccess ||
+        hipStreamCreateWithFlags(&ctx->capture_stream, hipStreamNonBlocking) != hipSuccess)
+      return bail(fail(ctx, HETEGEN_ERR_HIP, "stream creation failed"));
+    if (hipEventCreateWithFlags(&ctx->ev_x, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ctx->ev_y, hipEventDisableTiming) != hipSuccess)
       return bail(fail(ctx, HETEGEN_ERR_HIP, "event creation failed"));
-    // every slot starts free
-    if (hipEventRecord(ctx->ev_free[i], ctx->copy_stream) != hipSuccess)
-      return bail(fail(ctx, HETEGEN_ERR_HIP, "hipEventRecord failed"));
-  }
-  try {
-    ctx->mgr = std::thread(manager_main, ctx);
-  } catch (...) {
-    return bail(fail(ctx, HETEGEN_ERR_OOM, "parameter manager thread"));
-  }
-  *out = ctx;
-  return HETEGEN_OK;
+    ctx->slot.assign(c.ring_depth, nullptr);
+    ctx->ev_ready.assign(c.ring_depth, nullptr);
+    ctx->ev_free.assign(c.ring_depth, nullptr);
+    for (int i = 0; i < c.ring_depth; ++i) {
+      if (hipMalloc(&ctx->slot[i], c.chunk_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->slot[i] = nullptr;
+        return bail(fail(ctx, HETEGEN_ERR_OOM, "staging slot of %zu bytes", c.chunk_bytes));
+      }
+      if (hipEventCreateWithFlags(&ctx->ev_ready[i], hipEventDisableTiming) != hipSuccess ||
+          hipEventCreateWithFlags(&ctx->ev_free[i], hipEventDisableTiming | hipEventBlockingSync) != hipSuccess)
+        return bail(fail(ctx, HETEGEN_ERR_HIP, "event creation failed"));
+      // every slot starts free
+      if (hipEventRecord(ctx->ev_free[i], ctx->copy_stream) != hipSuccess)
+        return bail(fail(ctx, HETEGEN_ERR_HIP, "hipEventRecord failed"));
+    }
+    try {
+      ctx->mgr = std::thread(manager_main, ctx);
+    } catch (...) {
+      return bail(fail(ctx, HETEGEN_ERR_OOM, "parameter manager thread"));
+    }
+    *out = ctx;
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_destroy(hetegen_ctx* ctx) {
-  if (!ctx) return HETEGEN_OK;
-  if (ctx->mgr.joinable()) {
-    {
-      std::lock_guard<std::mutex> lk(ctx->mu);
-      ctx->stop = true;
+  return api_guard(nullptr, [&]() -> hetegen_status {  // ctx is gone by the end
+    if (!ctx) return HETEGEN_OK;
+    if (ctx->mgr.joinable()) {
+      {
+        std::lock_guard<std::mutex> lk(ctx->mu);
+        ctx->stop = true;
+      }
+      ctx->cv.notify_all();
+      ctx->mgr.join();
     }
-    ctx->cv.notify_all();
-    ctx->mgr.join();
-  }
-  hg::team_streamed_chunks(-(long long)ctx->jobs.size());  // chunks a failed call left queued
-  ctx->jobs.clear();
-  ctx->team.shutdown();
-  (void)hipSetDevice(ctx->device);
-  (void)hipDeviceSynchronize();
-  for (size_t i = 0; i < ctx->bounce.size(); ++i) {
-    if (ctx->bounce[i]) (void)hipHostFree(ctx->bounce[i]);
-    if (ctx->ev_bounce[i]) (void)hipEventDestroy(ctx->ev_bounce[i]);
-  }
-  for (auto& t : ctx->timed) {
-    (void)hipEventDestroy(t.a);
-    (void)hipEventDestroy(t.b);
-  }
-  for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
-  for (size_t i = 0; i < ctx->slot.size(); ++i) {
-    if (ctx->slot[i]) (void)hipFree(ctx->slot[i]);
-    if (ctx->ev_ready[i]) (void)hipEventDestroy(ctx->ev_ready[i]);
-    if (ctx->ev_free[i]) (void)hipEventDestroy(ctx->ev_free[i]);
-  }
-  if (ctx->ev_x) (void)hipEventDestroy(ctx->ev_x);
-  if (ctx->ev_y) (void)hipEventDestroy(ctx->ev_y);
-  if (ctx->x_host) (void)hipHostFree(ctx->x_host);
-  if (ctx->y_host) (void)hipHostFree(ctx->y_host);
-  if (ctx->copy_stream) (void)hipStreamDestroy(ctx->copy_stream);
-  if (ctx->capture_stream) (void)hipStreamDestroy(ctx->capture_stream);
-  (void)hipGetLastError();
-  delete ctx;
-  return HETEGEN_OK;
+    hg::team_streamed_chunks(-(long long)ctx->jobs.size());  // chunks a failed call left queued
+    ctx->jobs.clear();
+    ctx->team.shutdown();
+    (void)hipSetDevice(ctx->device);
+    (void)hipDeviceSynchronize();
+    for (size_t i = 0; i < ctx->bounce.size(); ++i) {
+      if (ctx->bounce[i]) (void)hipHostFree(ctx->bounce[i]);
+      if (ctx->ev_bounce[i]) (void)hipEventDestroy(ctx->ev_bounce[i]);
+    }
+    for (auto& t : ctx->timed) {
+      (void)hipEventDestroy(t.a);
+      (void)hipEventDestroy(t.b);
+    }
+    for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
+    for (size_t i = 0; i < ctx->slot.size(); ++i) {
+      if (ctx->slot[i]) (void)hipFree(ctx->slot[i]);
+      if (ctx->ev_ready[i]) (void)hipEventDestroy(ctx->ev_ready[i]);
+      if (ctx->ev_free[i]) (void)hipEventDestroy(ctx->ev_free[i]);
+    }
+    if (ctx->ev_x) (void)hipEventDestroy(ctx->ev_x);
+    if (ctx->ev_y) (void)hipEventDestroy(ctx->ev_y);
+    if (ctx->x_host) (void)hipHostFree(ctx->x_host);
+    if (ctx->y_host) (void)hipHostFree(ctx->y_host);
+    if (ctx->copy_stream) (void)hipStreamDestroy(ctx->copy_stream);
+    if (ctx->capture_stream) (void)hipStreamDestroy(ctx->capture_stream);
+    (void)hipGetLastError();
+    delete ctx;
+    return HETEGEN_OK;
+  });
 }
 
 const char* hetegen_last_error(const hetegen_ctx* ctx) { return ctx ? ctx->err.c_str() : g_create_error.c_str(); }
 
 hetegen_status hetegen_host_alloc(hetegen_ctx* ctx, size_t bytes, void** p) {
-  if (!ctx || !p || bytes == 0) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_host_alloc: bad arguments");
-  *p = nullptr;
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  if (host_malloc(ctx, p, bytes, hipHostMallocDefault) != hipSuccess) {
-    (void)hipGetLastError();
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx || !p || bytes == 0) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_host_alloc: bad arguments");
     *p = nullptr;
-    return fail(ctx, HETEGEN_ERR_OOM, "pinned allocation of %zu bytes failed", bytes);
-  }
-  return HETEGEN_OK;
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    if (host_malloc(ctx, p, bytes, hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      *p = nullptr;
+      return fail(ctx, HETEGEN_ERR_OOM, "pinned allocation of %zu bytes failed", bytes);
+    }
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_host_free(hetegen_ctx* ctx, void* p) {
-  if (!ctx) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "ctx is NULL");
-  if (!p) return HETEGEN_OK;
-  HIPCHK(ctx, hipHostFree(p));
-  return HETEGEN_OK;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "ctx is NULL");
+    if (!p) return HETEGEN_OK;
+    HIPCHK(ctx, hipHostFree(p));
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K, const void* W_host,
                               const void* W_dev_resident, int N, hetegen_dtype w_dtype, const void* bias_host,
                               const void* bias_dev, double alpha, void* y_dev, hetegen_dtype y_dtype, void* stream) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  auto t0 = Clock::now();
-  ctx->err.clear();
-  if (!x_dev || !W_host || !y_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "x_dev, W_host and y_dev are required");
-  if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "alpha %g outside [0, 1]", alpha);
-  if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
-  if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
-  if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
-  if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
-    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
-  if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)
-    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "y dtype must be the weight dtype or fp32");
-  if (!aligned16(x_dev) || !aligned16(W_host) || (W_dev_resident && !aligned16(W_dev_resident)))
-    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x, W and the resident copy must be 16-byte aligned");
-  const int n_cpu = split_cpu_rows(N, alpha), n_gpu = N - n_cpu;
-  if ((n_cpu > 0 && !bias_host && bias_dev) || (n_gpu > 0 && !bias_dev && bias_host))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bias: pass bias_host and bias_dev, or neither");
-  bool pageable = false;
-  TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
-  const size_t row = (size_t)K * 2;
-  if (!W_dev_resident && n_gpu > 0 && row > ctx->chunk_bytes)
-    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "a weight row (%zu bytes) exceeds chunk_bytes", row);
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  hipStream_t st = (hipStream_t)stream;
-  Job j{};
-  j.x = x_dev;
-  j.ldx = K;
-  j.B = B;
-  j.K = K;
-  j.N = N;
-  j.dtype = w_dtype;
-  j.W_host = W_host;
-  j.W_dev = W_dev_resident;
-  j.bias_host = bias_host;
-  j.bias_dev = bias_dev;
-  j.n_gpu = n_gpu;
-  j.n_cpu = n_cpu;
-  j.y = y_dev;
-  j.ldy = N;
-  j.y_f32 = y_dtype == HETEGEN_F32;
-  j.epi = hg::EPI_NONE;
-  if (!W_dev_resident && n_gpu > 0) {
-    if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
-    if (pageable) TRY(ensure_pin_resources(ctx));
-    plan_chunks(ctx, W_host, n_gpu, K, w_dtype, pageable, n_cpu == 0);
-  }
-  hetegen_status stt = run_linear(ctx, j, st);
-  if (stt != HETEGEN_OK) {
-    reset_pipeline(ctx);
-    return stt;
-  }
-  return finish_call(ctx, t0);
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    auto t0 = Clock::now();
+    ctx->err.clear();
+    if (!x_dev || !W_host || !y_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "x_dev, W_host and y_dev are required");
+    if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "alpha %g outside [0, 1]", alpha);
+    if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
+    if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
+    if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+    if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
+    if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "y dtype must be the weight dtype or fp32");
+    if (!aligned16(x_dev) || !aligned16(W_host) || (W_dev_resident && !aligned16(W_dev_resident)))
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x, W and the resident copy must be 16-byte aligned");
+    const int n_cpu = split_cpu_rows(N, alpha), n_gpu = N - n_cpu;
+    if ((n_cpu > 0 && !bias_host && bias_dev) || (n_gpu > 0 && !bias_dev && bias_host))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bias: pass bias_host and bias_dev, or neither");
+    bool pageable = false;
+    TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
+    const size_t row = (size_t)K * 2;
+    if (!W_dev_resident && n_gpu > 0 && row > ctx->chunk_bytes)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "a weight row (%zu bytes) exceeds chunk_bytes", row);
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    hipStream_t st = (hipStream_t)stream;
+    Job j{};
+    j.x = x_dev;
+    j.ldx = K;
+    j.B = B;
+    j.K = K;
+    j.N = N;
+    j.dtype = w_dtype;
+    j.W_host = W_host;
+    j.W_dev = W_dev_resident;
+    j.bias_host = bias_host;
+    j.bias_dev = bias_dev;
+    j.n_gpu = n_gpu;
+    j.n_cpu = n_cpu;
+    j.y = y_dev;
+    j.ldy = N;
+    j.y_f32 = y_dtype == HETEGEN_F32;
+    j.epi = hg::EPI_NONE;
+    if (!W_dev_resident && n_gpu > 0) {
+      if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+      if (pageable) TRY(ensure_pin_resources(ctx));
+      plan_chunks(ctx, W_host, n_gpu, K, w_dtype, pageable, n_cpu == 0);
+    }
+    hetegen_status stt = run_linear(ctx, j, st);
+    if (stt != HETEGEN_OK) {
+      reset_pipeline(ctx);
+      return stt;
+    }
+    return finish_call(ctx, t0);
+  });
 }
 
 // ---- planner (pure host arithmetic) ----
 hetegen_status hetegen_layer_plan(const hetegen_shape* shapes, int n, const hetegen_bw* bw, int n_bw, int flags,
                                   double* alpha_out) {
-  if (!shapes || !bw || !alpha_out || n < 0 || !(n_bw == 1 || n_bw == n)) return HETEGEN_ERR_INVALID_ARG;
-  for (int i = 0; i < n; ++i) {
-    const hetegen_bw& b = bw[n_bw == 1 ? 0 : i];
-    if (shapes[i].N < 1 || shapes[i].K < 1) return HETEGEN_ERR_INVALID_ARG;
-    if (shapes[i].resident) {
-      alpha_out[i] = 0.0;
-      continue;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!shapes || !bw || !alpha_out || n < 0 || !(n_bw == 1 || n_bw == n)) return HETEGEN_ERR_INVALID_ARG;
+    for (int i = 0; i < n; ++i) {
+      const hetegen_bw& b = bw[n_bw == 1 ? 0 : i];
+      if (shapes[i].N < 1 || shapes[i].K < 1) return HETEGEN_ERR_INVALID_ARG;
+      if (shapes[i].resident) {
+        alpha_out[i] = 0.0;
+        continue;
+      }
+      const double vc = b.cpu_Bps, vg = b.hbm_gemv_Bps;
+      double vm = b.h2d_Bps;
+      if (!(vc > 0 && std::isfinite(vc) && vg > 0 && std::isfinite(vg) && vm > 0 && std::isfinite(vm)))
+        return HETEGEN_ERR_INVALID_ARG;
+      if (b.pin_Bps > 0) {
+        if (!std::isfinite(b.pin_Bps)) return HETEGEN_ERR_INVALID_ARG;
+        vm = std::min(vm, b.pin_Bps);  // T_COM = max(T_PIN, T_TRANS)
+      }
+      // CPU fraction = 1 - alpha_gpu; written as the balance of per-byte times so that
+      // large speed ratios do not overflow: (1/Vcom + 1/Vgpu) / (1/Vcpu + 1/Vcom + 1/Vgpu).
+      double c;
+      if (flags & HETEGEN_PLAN_APPROX) c = (1.0 / vm) / (1.0 / vc + 1.0 / vm);
+      else c = (1.0 / vm + 1.0 / vg) / (1.0 / vc + 1.0 / vm + 1.0 / vg);
+      alpha_out[i] = std::min(1.0, std::max(0.0, c));
     }
-    const double vc = b.cpu_Bps, vg = b.hbm_gemv_Bps;
-    double vm = b.h2d_Bps;
-    if (!(vc > 0 && std::isfinite(vc) && vg > 0 && std::isfinite(vg) && vm > 0 && std::isfinite(vm)))
-      return HETEGEN_ERR_INVALID_ARG;
-    if (b.pin_Bps > 0) {
-      if (!std::isfinite(b.pin_Bps)) return HETEGEN_ERR_INVALID_ARG;
-      vm = std::min(vm, b.pin_Bps);  // T_COM = max(T_PIN, T_TRANS)
-    }
-    // CPU fraction = 1 - alpha_gpu; written as the balance of per-byte times so that
-    // large speed ratios do not overflow: (1/Vcom + 1/Vgpu) / (1/Vcpu + 1/Vcom + 1/Vgpu).
-    double c;
-    if (flags & HETEGEN_PLAN_APPROX) c = (1.0 / vm) / (1.0 / vc + 1.0 / vm);
-    else c = (1.0 / vm + 1.0 / vg) / (1.0 / vc + 1.0 / vm + 1.0 / vg);
-    alpha_out[i] = std::min(1.0, std::max(0.0, c));
-  }
-  return HETEGEN_OK;
+    return HETEGEN_OK;
+  });
 }
 
 }  // extern "C"
@@ -1017,94 +1059,98 @@ double poly(const double* c, int d, double s) {
 
 extern "C" hetegen_status hetegen_alpha_fit(const double* alphas, const double* t_cpu, const double* t_com, int n,
                                             int degree, double lo, double hi, double* alpha_out, int* crossed) {
-  if (!alphas || !t_cpu || !t_com || !alpha_out || degree < 1 || degree > 3 || n < degree + 1 || !(lo < hi))
-    return HETEGEN_ERR_INVALID_ARG;
-  double amin = alphas[0], amax = alphas[0];
-  for (int i = 0; i < n; ++i) {
-    if (!std::isfinite(alphas[i]) || !std::isfinite(t_cpu[i]) || !std::isfinite(t_com[i]))
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!alphas || !t_cpu || !t_com || !alpha_out || degree < 1 || degree > 3 || n < degree + 1 || !(lo < hi))
       return HETEGEN_ERR_INVALID_ARG;
-    amin = std::min(amin, alphas[i]);
-    amax = std::max(amax, alphas[i]);
-  }
-  const double ctr = 0.5 * (amin + amax), half = amax > amin ? 0.5 * (amax - amin) : 1.0;
-  std::vector<double> sv(n);
-  for (int i = 0; i < n; ++i) sv[i] = (alphas[i] - ctr) / half;
-  double cc[4], cg[4];
-  if (!lsq_poly(sv, t_cpu, degree, cc) || !lsq_poly(sv, t_com, degree, cg)) return HETEGEN_ERR_INVALID_ARG;
-  auto fc = [&](double a) { return poly(cc, degree, (a - ctr) / half); };
-  auto fg = [&](double a) { return poly(cg, degree, (a - ctr) / half); };
-  auto g = [&](double a) { return fc(a) - fg(a); };
-  // sign changes of F_CPU - F_COM on a fine grid, each refined by bisection
-  const int M = 2000;
-  double best = 0, best_t = INFINITY;
-  bool found = false;
-  double a0 = lo, g0 = g(lo);
-  for (int i = 1; i <= M; ++i) {
-    const double a1 = lo + (hi - lo) * i / M, g1 = g(a1);
-    if (g0 == 0 || (g0 < 0) != (g1 < 0)) {
-      double l = a0, r = a1, gl = g0;
-      if (g0 == 0) r = a0;
-      for (int it = 0; it < 200 && r - l > 0; ++it) {
-        const double mid = 0.5 * (l + r), gm = g(mid);
-        if (mid <= l || mid >= r) break;
-        if ((gm < 0) == (gl < 0)) {
-          l = mid;
-          gl = gm;
-        } else {
-          r = mid;
+    double amin = alphas[0], amax = alphas[0];
+    for (int i = 0; i < n; ++i) {
+      if (!std::isfinite(alphas[i]) || !std::isfinite(t_cpu[i]) || !std::isfinite(t_com[i]))
+        return HETEGEN_ERR_INVALID_ARG;
+      amin = std::min(amin, alphas[i]);
+      amax = std::max(amax, alphas[i]);
+    }
+    const double ctr = 0.5 * (amin + amax), half = amax > amin ? 0.5 * (amax - amin) : 1.0;
+    std::vector<double> sv(n);
+    for (int i = 0; i < n; ++i) sv[i] = (alphas[i] - ctr) / half;
+    double cc[4], cg[4];
+    if (!lsq_poly(sv, t_cpu, degree, cc) || !lsq_poly(sv, t_com, degree, cg)) return HETEGEN_ERR_INVALID_ARG;
+    auto fc = [&](double a) { return poly(cc, degree, (a - ctr) / half); };
+    auto fg = [&](double a) { return poly(cg, degree, (a - ctr) / half); };
+    auto g = [&](double a) { return fc(a) - fg(a); };
+    // sign changes of F_CPU - F_COM on a fine grid, each refined by bisection
+    const int M = 2000;
+    double best = 0, best_t = INFINITY;
+    bool found = false;
+    double a0 = lo, g0 = g(lo);
+    for (int i = 1; i <= M; ++i) {
+      const double a1 = lo + (hi - lo) * i / M, g1 = g(a1);
+      if (g0 == 0 || (g0 < 0) != (g1 < 0)) {
+        double l = a0, r = a1, gl = g0;
+        if (g0 == 0) r = a0;
+        for (int it = 0; it < 200 && r - l > 0; ++it) {
+          const double mid = 0.5 * (l + r), gm = g(mid);
+          if (mid <= l || mid >= r) break;
+          if ((gm < 0) == (gl < 0)) {
+            l = mid;
+            gl = gm;
+          } else {
+            r = mid;
+          }
+        }
+        const double root = 0.5 * (l + r);
+        if (fc(root) < best_t) {
+          best_t = fc(root);
+          best = root;
+          found = true;
         }
       }
-      const double root = 0.5 * (l + r);
-      if (fc(root) < best_t) {
-        best_t = fc(root);
-        best = root;
-        found = true;
+      a0 = a1;
+      g0 = g1;
+    }
+    if (!found) {  // no crossing: bracket point with the smallest max(F_CPU, F_COM)
+      const int G = 10000;
+      for (int i = 0; i <= G; ++i) {
+        const double a = lo + (hi - lo) * i / G, m = std::max(fc(a), fg(a));
+        if (m < best_t) {
+          best_t = m;
+          best = a;
+        }
       }
     }
-    a0 = a1;
-    g0 = g1;
-  }
-  if (!found) {  // no crossing: bracket point with the smallest max(F_CPU, F_COM)
-    const int G = 10000;
-    for (int i = 0; i <= G; ++i) {
-      const double a = lo + (hi - lo) * i / G, m = std::max(fc(a), fg(a));
-      if (m < best_t) {
-        best_t = m;
-        best = a;
-      }
-    }
-  }
-  *alpha_out = std::min(hi, std::max(lo, best));
-  if (crossed) *crossed = found ? 1 : 0;
-  return HETEGEN_OK;
+    *alpha_out = std::min(hi, std::max(lo, best));
+    if (crossed) *crossed = found ? 1 : 0;
+    return HETEGEN_OK;
+  });
 }
 
 extern "C" hetegen_status hetegen_alpha_minimize(const double* alphas, const double* t, int n, int degree, double lo,
                                                  double hi, double* alpha_out) {
-  if (!alphas || !t || !alpha_out || degree < 1 || degree > 3 || n < degree + 1 || !(lo < hi))
-    return HETEGEN_ERR_INVALID_ARG;
-  double amin = alphas[0], amax = alphas[0];
-  for (int i = 0; i < n; ++i) {
-    if (!std::isfinite(alphas[i]) || !std::isfinite(t[i])) return HETEGEN_ERR_INVALID_ARG;
-    amin = std::min(amin, alphas[i]);
-    amax = std::max(amax, alphas[i]);
-  }
-  const double ctr = 0.5 * (amin + amax), half = amax > amin ? 0.5 * (amax - amin) : 1.0;
-  std::vector<double> sv(n);
-  for (int i = 0; i < n; ++i) sv[i] = (alphas[i] - ctr) / half;
-  double c[4];
-  if (!lsq_poly(sv, t, degree, c)) return HETEGEN_ERR_INVALID_ARG;
-  const int G = 10000;
-  double best = lo, best_t = INFINITY;
-  for (int i = 0; i <= G; ++i) {
-    const double a = lo + (hi - lo) * i / G, v = poly(c, degree, (a - ctr) / half);
-    if (v < best_t) {
-      best_t = v;
-      best = a;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!alphas || !t || !alpha_out || degree < 1 || degree > 3 || n < degree + 1 || !(lo < hi))
+      return HETEGEN_ERR_INVALID_ARG;
+    double amin = alphas[0], amax = alphas[0];
+    for (int i = 0; i < n; ++i) {
+      if (!std::isfinite(alphas[i]) || !std::isfinite(t[i])) return HETEGEN_ERR_INVALID_ARG;
+      amin = std::min(amin, alphas[i]);
+      amax = std::max(amax, alphas[i]);
     }
-  }
-  *alpha_out = best;
-  return HETEGEN_OK;
+    const double ctr = 0.5 * (amin + amax), half = amax > amin ? 0.5 * (amax - amin) : 1.0;
+    std::vector<double> sv(n);
+    for (int i = 0; i < n; ++i) sv[i] = (alphas[i] - ctr) / half;
+    double c[4];
+    if (!lsq_poly(sv, t, degree, c)) return HETEGEN_ERR_INVALID_ARG;
+    const int G = 10000;
+    double best = lo, best_t = INFINITY;
+    for (int i = 0; i <= G; ++i) {
+      const double a = lo + (hi - lo) * i / G, v = poly(c, degree, (a - ctr) / half);
+      if (v < best_t) {
+        best_t = v;
+        best = a;
+      }
+    }
+    *alpha_out = best;
+    return HETEGEN_OK;
+  });
 }
 
 extern "C" hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void* x_dev, int B, int K,
@@ -1112,110 +1158,120 @@ extern "C" hetegen_status hetegen_alpha_benchmark(hetegen_ctx* ctx, const void* 
                                                   const void* bias_host, const void* bias_dev, void* y_dev,
                                                   double alpha0, double gamma, double lambda, int degree, int reps,
                                                   void* stream, double* alpha_out, int* crossed) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  if (!alpha_out || !(gamma >= 0) || !(lambda > 0) || reps < 1 || !(alpha0 >= 0 && alpha0 <= 1) || degree < 1 ||
-      degree > 3)
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_alpha_benchmark: bad arguments");
-  const double lo = std::max(0.0, alpha0 - gamma), hi = std::min(1.0, alpha0 + gamma);
-  std::vector<double> as, tc, tg;
-  for (int i = 0;; ++i) {
-    const double a = lo + i * lambda;
-    if (a > hi + 1e-9) break;
-    as.push_back(std::min(a, hi));
-  }
-  if ((int)as.size() < degree + 1 || !(lo < hi))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bracket holds %zu points; degree %d needs %d", as.size(), degree,
-                degree + 1);
-  const bool was = ctx->profiling;
-  ctx->profiling = true;
-  TRY(flush_profile(ctx));
-  const hetegen_profile saved = ctx->prof;
-  hetegen_status st = HETEGEN_OK;
-  for (double a : as) {
-    std::vector<double> c, g;
-    for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
-      ctx->prof = hetegen_profile{};
-      st = hetegen_linear(ctx, x_dev, B, K, W_host, nullptr, N, dtype, bias_host, bias_dev, a, y_dev, HETEGEN_F32,
-                          stream);
-      if (st == HETEGEN_OK && r > 0) {  // the first run of each point warms it up
-        c.push_back(ctx->prof.cpu_ms);
-        g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
-      }
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    if (!alpha_out || !(gamma >= 0) || !(lambda > 0) || reps < 1 || !(alpha0 >= 0 && alpha0 <= 1) || degree < 1 ||
+        degree > 3)
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_alpha_benchmark: bad arguments");
+    const double lo = std::max(0.0, alpha0 - gamma), hi = std::min(1.0, alpha0 + gamma);
+    std::vector<double> as, tc, tg;
+    for (int i = 0;; ++i) {
+      const double a = lo + i * lambda;
+      if (a > hi + 1e-9) break;
+      as.push_back(std::min(a, hi));
     }
-    if (st != HETEGEN_OK) break;
-    std::sort(c.begin(), c.end());
-    std::sort(g.begin(), g.end());
-    tc.push_back(c[c.size() / 2]);
-    tg.push_back(g[g.size() / 2]);
-  }
-  ctx->prof = saved;
-  ctx->profiling = was;
-  if (st != HETEGEN_OK) return st;
-  hetegen_status fs = hetegen_alpha_fit(as.data(), tc.data(), tg.data(), (int)as.size(), degree, lo, hi, alpha_out,
-                                        crossed);
-  if (fs != HETEGEN_OK) return fail(ctx, fs, "alpha fit failed");
-  return HETEGEN_OK;
+    if ((int)as.size() < degree + 1 || !(lo < hi))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bracket holds %zu points; degree %d needs %d", as.size(), degree,
+                  degree + 1);
+    const bool was = ctx->profiling;
+    ctx->profiling = true;
+    TRY(flush_profile(ctx));
+    const hetegen_profile saved = ctx->prof;
+    hetegen_status st = HETEGEN_OK;
+    for (double a : as) {
+      std::vector<double> c, g;
+      for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
+        ctx->prof = hetegen_profile{};
+        st = hetegen_linear(ctx, x_dev, B, K, W_host, nullptr, N, dtype, bias_host, bias_dev, a, y_dev, HETEGEN_F32,
+                            stream);
+        if (st == HETEGEN_OK && r > 0) {  // the first run of each point warms it up
+          c.push_back(ctx->prof.cpu_ms);
+          g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
+        }
+      }
+      if (st != HETEGEN_OK) break;
+      std::sort(c.begin(), c.end());
+      std::sort(g.begin(), g.end());
+      tc.push_back(c[c.size() / 2]);
+      tg.push_back(g[g.size() / 2]);
+    }
+    ctx->prof = saved;
+    ctx->profiling = was;
+    if (st != HETEGEN_OK) return st;
+    hetegen_status fs = hetegen_alpha_fit(as.data(), tc.data(), tg.data(), (int)as.size(), degree, lo, hi, alpha_out,
+                                          crossed);
+    if (fs != HETEGEN_OK) return fail(ctx, fs, "alpha fit failed");
+    return HETEGEN_OK;
+  });
 }
 
 extern "C" hetegen_status hetegen_cpu_linear(const float* x, int B, int K, const void* W_host, hetegen_dtype dtype,
                                              const void* bias_host, int r0, int r1, float* y, int ldy, int threads) {
-  if (!x || !W_host || !y || B < 1 || B > kMaxBatch || K < 8 || K % 8 || r0 < 0 || r1 < r0 || ldy < r1 - r0 ||
-      (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
-    return HETEGEN_ERR_INVALID_ARG;
-  hg::cpu_share(x, B, K, (const uint16_t*)W_host, dtype, (const uint16_t*)bias_host, r0, r1, y, ldy, threads);
-  return HETEGEN_OK;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!x || !W_host || !y || B < 1 || B > kMaxBatch || K < 8 || K % 8 || r0 < 0 || r1 < r0 || ldy < r1 - r0 ||
+        (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
+      return HETEGEN_ERR_INVALID_ARG;
+    hg::cpu_share(x, B, K, (const uint16_t*)W_host, dtype, (const uint16_t*)bias_host, r0, r1, y, ldy, threads);
+    return HETEGEN_OK;
+  });
 }
 
 // ---- heterogeneous module scheduler (Sec. 4.5, Eq. 13) ----
 extern "C" hetegen_status hetegen_module_schedule(const double* t_cpu, const double* mem, const int* layer, int n,
                                                   double budget_bytes, int* resident_out, double* used_out) {
-  if (n < 0 || (n > 0 && (!t_cpu || !mem || !layer || !resident_out)) || !(budget_bytes >= 0))
-    return HETEGEN_ERR_INVALID_ARG;
-  std::vector<double> g(n);
-  std::map<int, std::vector<int>> by_layer;  // layers in increasing order
-  for (int i = 0; i < n; ++i) {
-    if (!std::isfinite(t_cpu[i]) || t_cpu[i] < 0 || !std::isfinite(mem[i]) || !(mem[i] > 0) || layer[i] < 0)
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (n < 0 || (n > 0 && (!t_cpu || !mem || !layer || !resident_out)) || !(budget_bytes >= 0))
       return HETEGEN_ERR_INVALID_ARG;
-    g[i] = t_cpu[i] / mem[i];
-    by_layer[layer[i]].push_back(i);
-  }
-  // modules of each layer by decreasing gain (stable: index order among equal gains)
-  size_t depth = 0;
-  for (auto& kv : by_layer) {
-    std::stable_sort(kv.second.begin(), kv.second.end(), [&](int a, int b) { return g[a] > g[b]; });
-    depth = std::max(depth, kv.second.size());
-  }
-  double used = 0.0;
-  for (int i = 0; i < n; ++i) resident_out[i] = 0;
-  for (size_t r = 0; r < depth; ++r) {
-    for (const auto& kv : by_layer) {
-      const auto& v = kv.second;
-      if (r >= v.size()) continue;
-      const int i = v[r];
-      if (used + mem[i] <= budget_bytes) {
-        resident_out[i] = 1;
-        used += mem[i];
+    std::vector<double> g(n);
+    std::map<int, std::vector<int>> by_layer;  // layers in increasing order
+    for (int i = 0; i < n; ++i) {
+      if (!std::isfinite(t_cpu[i]) || t_cpu[i] < 0 || !std::isfinite(mem[i]) || !(mem[i] > 0) || layer[i] < 0)
+        return HETEGEN_ERR_INVALID_ARG;
+      g[i] = t_cpu[i] / mem[i];
+      by_layer[layer[i]].push_back(i);
+    }
+    // modules of each layer by decreasing gain (stable: index order among equal gains)
+    size_t depth = 0;
+    for (auto& kv : by_layer) {
+      std::stable_sort(kv.second.begin(), kv.second.end(), [&](int a, int b) { return g[a] > g[b]; });
+      depth = std::max(depth, kv.second.size());
+    }
+    double used = 0.0;
+    for (int i = 0; i < n; ++i) resident_out[i] = 0;
+    for (size_t r = 0; r < depth; ++r) {
+      for (const auto& kv : by_layer) {
+        const auto& v = kv.second;
+        if (r >= v.size()) continue;
+        const int i = v[r];
+        if (used + mem[i] <= budget_bytes) {
+          resident_out[i] = 1;
+          used += mem[i];
+        }
       }
     }
-  }
-  if (used_out) *used_out = used;
-  return HETEGEN_OK;
+    if (used_out) *used_out = used;
+    return HETEGEN_OK;
+  });
 }
 
 extern "C" {
 
 hetegen_status hetegen_set_profiling(hetegen_ctx* ctx, int on) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->profiling = on != 0;
-  return HETEGEN_OK;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->profiling = on != 0;
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_get_profile(hetegen_ctx* ctx, hetegen_profile* out, int reset) {
-  if (!ctx || !out) return HETEGEN_ERR_INVALID_ARG;
-  TRY(flush_profile(ctx));
-  *out = ctx->prof;
-  if (reset) ctx->prof = hetegen_profile{};
-  return HETEGEN_OK;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx || !out) return HETEGEN_ERR_INVALID_ARG;
+    TRY(flush_profile(ctx));
+    *out = ctx->prof;
+    if (reset) ctx->prof = hetegen_profile{};
+    return HETEGEN_OK;
+  });
 }
 
 }  // extern "C"
@@ -1223,220 +1279,226 @@ hetegen_status hetegen_get_profile(hetegen_ctx* ctx, hetegen_profile* out, int r
 // ---- bandwidth probe ----
 extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, int N, int K, hetegen_dtype dtype, int B,
                                         int reps, int flags, hetegen_bw* out) {
-  if (!ctx || !W_host || !out || N < 1 || K < 8 || K % 8 || B < 1 || B > kMaxBatch || reps < 1 ||
-      (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe: bad arguments");
-  bool pageable = false;
-  TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
-  HIPCHK(ctx, hipDeviceSynchronize());  // earlier GEMVs may still read the staging slots
-  if (pageable) TRY(ensure_pin_resources(ctx));
-  const size_t wbytes = (size_t)N * K * 2;
-  auto median = [](std::vector<double> v) {
-    std::sort(v.begin(), v.end());
-    return v[v.size() / 2];
-  };
-  // V_CPU: the CPU share over all rows
-  if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
-  ctx->y_pending = false;
-  TRY(ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, (size_t)B * K * 4));
-  TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)B * N * 4));
-  memset(ctx->x_host, 0, (size_t)B * K * 4);
-  // In a step every weight comes from DRAM (a step's weights dwarf the host caches);
-  // a single linear re-read by the probe can sit in a large L3, so the caches are
-  // flushed before every pass by reading a 1 GiB buffer (reading, not writing: dirty
-  // lines written back during the timed pass would slow it).
-  std::vector<uint64_t> flush;
-  try {
-    flush.assign(((size_t)1 << 30) / sizeof(uint64_t), 1);
-  } catch (...) {
-    return fail(ctx, HETEGEN_ERR_OOM, "probe cache-flush buffer");
-  }
-  uint64_t flush_sink = 0;
-  // read on the CPU share's own worker team (a second team would still be spinning
-  // when the timed pass starts)
-  struct Flush {
-    const uint64_t* p;
-    long long n;
-    uint64_t part[64];
-  } fl{flush.data(), (long long)flush.size(), {}};
-  enum { kFlushGrains = 64 };
-  auto flush_caches = [&](int) {
-    hg::team_for(ctx->cpu_threads, kFlushGrains, [](void* a, int g) {
-      Flush& f = *(Flush*)a;
-      const long long per = (f.n / kFlushGrains + 7) & ~7LL;
-      const long long b = per * g, e = std::min(f.n, b + per);
-      uint64_t acc = 0;
-      for (long long i = b; i < e; i += 8) acc ^= f.p[i];  // one word per 64-byte line
-      f.part[g] = acc;
-    }, &fl);
-    for (int g = 0; g < kFlushGrains; ++g) flush_sink ^= fl.part[g];
-  };
-  std::vector<double> tc;
-  for (int r = -1; r < reps; ++r) {  // one untimed pass first: threads up, TLBs warm
-    flush_caches(r & 0xff);
-    auto t0 = Clock::now();
-    hg::cpu_share(ctx->x_host, B, K, (const uint16_t*)W_host, dtype, nullptr, 0, N, ctx->y_host, N, ctx->cpu_threads);
-    if (r >= 0) tc.push_back(ms_since(t0) * 1e-3);
-  }
-  // V_PIN (pageable weights): the pin team staging W_host chunk by chunk
-  const size_t row = (size_t)K * 2;
-  const size_t cbytes = (size_t)chunk_rows_for(ctx, K, dtype) * row;
-  std::vector<double> tp;
-  for (int r = 0; pageable && r < reps; ++r) {
-    HIPCHK(ctx, hipStreamSynchronize(ctx->copy_stream));  // no copy reads the staging buffers
-    flush_caches(r & 0xff);
-    auto t0 = Clock::now();
-    int i = 0;
-    for (size_t off = 0; off < wbytes; off += cbytes, ++i)
-      ctx->team.copy((char*)ctx->bounce[i % ctx->pin_ring], (const char*)W_host + off, std::min(cbytes, wbytes - off));
-    tp.push_back(ms_since(t0) * 1e-3);
-  }
-  // V_COM: chunked copies through the ring on the copy stream, from W_host or (pageable)
-  // from the pinned staging buffers
-  hipEvent_t a, b;
-  HIPCHK(ctx, hipEventCreate(&a));
-  HIPCHK(ctx, hipEventCreate(&b));
-  std::vector<double> tm;
-  for (int r = 0; r < reps; ++r) {
-    HIPCHK(ctx, hipEventRecord(a, ctx->copy_stream));
-    int i = 0;
-    for (size_t off = 0; off < wbytes; off += cbytes, ++i) {
-      const size_t nb = std::min(cbytes, wbytes - off);
-      const void* src = pageable ? ctx->bounce[i % ctx->pin_ring] : (const char*)W_host + off;
-      HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], src, nb, hipMemcpyHostToDevice, ctx->copy_stream));
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx || !W_host || !out || N < 1 || K < 8 || K % 8 || B < 1 || B > kMaxBatch || reps < 1 ||
+        (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe: bad arguments");
+    bool pageable = false;
+    TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
+    HIPCHK(ctx, hipDeviceSynchronize());  // earlier GEMVs may still read the staging slots
+    if (pageable) TRY(ensure_pin_resources(ctx));
+    const size_t wbytes = (size_t)N * K * 2;
+    auto median = [](std::vector<double> v) {
+      std::sort(v.begin(), v.end());
+      return v[v.size() / 2];
+    };
+    // V_CPU: the CPU share over all rows
+    if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
+    ctx->y_pending = false;
+    TRY(ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, (size_t)B * K * 4));
+    TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)B * N * 4));
+    memset(ctx->x_host, 0, (size_t)B * K * 4);
+    // In a step every weight comes from DRAM (a step's weights dwarf the host caches);
+    // a single linear re-read by the probe can sit in a large L3, so the caches are
+    // flushed before every pass by reading a 1 GiB buffer (reading, not writing: dirty
+    // lines written back during the timed pass would slow it).
+    std::vector<uint64_t> flush;
+    try {
+      flush.assign(((size_t)1 << 30) / sizeof(uint64_t), 1);
+    } catch (...) {
+      return fail(ctx, HETEGEN_ERR_OOM, "probe cache-flush buffer");
     }
-    HIPCHK(ctx, hipEventRecord(b, ctx->copy_stream));
-    HIPCHK(ctx, hipEventSynchronize(b));
-    float ms = 0;
-    HIPCHK(ctx, hipEventElapsedTime(&ms, a, b));
-    tm.push_back(ms * 1e-3);
-  }
-  // concurrent rates: the copies of W once, the CPU share over W back to back until they end
-  std::vector<double> cc, cm;
-  for (int r = 0; (flags & HETEGEN_PROBE_CONCURRENT) && !pageable && r < reps; ++r) {
-    flush_caches(r & 0xff);
-    HIPCHK(ctx, hipEventRecord(a, ctx->copy_stream));
-    for (size_t off = 0, i = 0; off < wbytes; off += cbytes, ++i)
-      HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], (const char*)W_host + off, std::min(cbytes, wbytes - off),
-                                 hipMemcpyHostToDevice, ctx->copy_stream));
-    HIPCHK(ctx, hipEventRecord(b, ctx->copy_stream));
-    double t_sum = 0;  // CPU passes that ended before the copies did (each on cold caches)
-    int n_done = 0;
-    for (int pass = 0;; ++pass) {
-      if (pass > 0) flush_caches((r + pass) & 0xff);
-      const auto t0 = Clock::now();
+    uint64_t flush_sink = 0;
+    // read on the CPU share's own worker team (a second team would still be spinning
+    // when the timed pass starts)
+    struct Flush {
+      const uint64_t* p;
+      long long n;
+      uint64_t part[64];
+    } fl{flush.data(), (long long)flush.size(), {}};
+    enum { kFlushGrains = 64 };
+    auto flush_caches = [&](int) {
+      hg::team_for(ctx->cpu_threads, kFlushGrains, [](void* a, int g) {
+        Flush& f = *(Flush*)a;
+        const long long per = (f.n / kFlushGrains + 7) & ~7LL;
+        const long long b = per * g, e = std::min(f.n, b + per);
+        uint64_t acc = 0;
+        for (long long i = b; i < e; i += 8) acc ^= f.p[i];  // one word per 64-byte line
+        f.part[g] = acc;
+      }, &fl);
+      for (int g = 0; g < kFlushGrains; ++g) flush_sink ^= fl.part[g];
+    };
+    std::vector<double> tc;
+    for (int r = -1; r < reps; ++r) {  // one untimed pass first: threads up, TLBs warm
+      flush_caches(r & 0xff);
+      auto t0 = Clock::now();
       hg::cpu_share(ctx->x_host, B, K, (const uint16_t*)W_host, dtype, nullptr, 0, N, ctx->y_host, N, ctx->cpu_threads);
-      const double t = ms_since(t0) * 1e-3;
-      const hipError_t q = hipEventQuery(b);
-      if (q == hipErrorNotReady) {
-        (void)hipGetLastError();
-        t_sum += t;
-        ++n_done;
-        continue;
-      }
-      HIPCHK(ctx, q);
-      if (n_done == 0) {  // the copies ended within the first pass: count that pass
-        t_sum = t;
-        n_done = 1;
-      }
-      break;
+      if (r >= 0) tc.push_back(ms_since(t0) * 1e-3);
     }
-    float ms = 0;
-    HIPCHK(ctx, hipEventElapsedTime(&ms, a, b));
-    cc.push_back(t_sum / n_done);
-    cm.push_back(ms * 1e-3);
-  }
-  // V_GPU: the GEMV over a device copy of W
-  void *Wd = nullptr, *xd = nullptr, *yd = nullptr;
-  hetegen_status st = HETEGEN_OK;
-  std::vector<double> tg;
-  if (hipMalloc(&Wd, wbytes) != hipSuccess || hipMalloc(&xd, (size_t)B * K * 2) != hipSuccess ||
-      hipMalloc(&yd, (size_t)B * N * 4) != hipSuccess) {
+    // V_PIN (pageable weights): the pin team staging W_host chunk by chunk
+    const size_t row = (size_t)K * 2;
+    const size_t cbytes = (size_t)chunk_rows_for(ctx, K, dtype) * row;
+    std::vector<double> tp;
+    for (int r = 0; pageable && r < reps; ++r) {
+      HIPCHK(ctx, hipStreamSynchronize(ctx->copy_stream));  // no copy reads the staging buffers
+      flush_caches(r & 0xff);
+      auto t0 = Clock::now();
+      int i = 0;
+      for (size_t off = 0; off < wbytes; off += cbytes, ++i)
+        ctx->team.copy((char*)ctx->bounce[i % ctx->pin_ring], (const char*)W_host + off,
+                       std::min(cbytes, wbytes - off));
+      tp.push_back(ms_since(t0) * 1e-3);
+    }
+    // V_COM: chunked copies through the ring on the copy stream, from W_host or (pageable)
+    // from the pinned staging buffers
+    hipEvent_t a, b;
+    HIPCHK(ctx, hipEventCreate(&a));
+    HIPCHK(ctx, hipEventCreate(&b));
+    std::vector<double> tm;
+    for (int r = 0; r < reps; ++r) {
+      HIPCHK(ctx, hipEventRecord(a, ctx->copy_stream));
+      int i = 0;
+      for (size_t off = 0; off < wbytes; off += cbytes, ++i) {
+        const size_t nb = std::min(cbytes, wbytes - off);
+        const void* src = pageable ? ctx->bounce[i % ctx->pin_ring] : (const char*)W_host + off;
+        HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], src, nb, hipMemcpyHostToDevice, ctx->copy_stream));
+      }
+      HIPCHK(ctx, hipEventRecord(b, ctx->copy_stream));
+      HIPCHK(ctx, hipEventSynchronize(b));
+      float ms = 0;
+      HIPCHK(ctx, hipEventElapsedTime(&ms, a, b));
+      tm.push_back(ms * 1e-3);
+    }
+    // concurrent rates: the copies of W once, the CPU share over W back to back until they end
+    std::vector<double> cc, cm;
+    for (int r = 0; (flags & HETEGEN_PROBE_CONCURRENT) && !pageable && r < reps; ++r) {
+      flush_caches(r & 0xff);
+      HIPCHK(ctx, hipEventRecord(a, ctx->copy_stream));
+      for (size_t off = 0, i = 0; off < wbytes; off += cbytes, ++i)
+        HIPCHK(ctx, hipMemcpyAsync(ctx->slot[i % ctx->ring], (const char*)W_host + off, std::min(cbytes, wbytes - off),
+                                   hipMemcpyHostToDevice, ctx->copy_stream));
+      HIPCHK(ctx, hipEventRecord(b, ctx->copy_stream));
+      double t_sum = 0;  // CPU passes that ended before the copies did (each on cold caches)
+      int n_done = 0;
+      for (int pass = 0;; ++pass) {
+        if (pass > 0) flush_caches((r + pass) & 0xff);
+        const auto t0 = Clock::now();
+        hg::cpu_share(ctx->x_host, B, K, (const uint16_t*)W_host, dtype, nullptr, 0, N, ctx->y_host, N,
+                      ctx->cpu_threads);
+        const double t = ms_since(t0) * 1e-3;
+        const hipError_t q = hipEventQuery(b);
+        if (q == hipErrorNotReady) {
+          (void)hipGetLastError();
+          t_sum += t;
+          ++n_done;
+          continue;
+        }
+        HIPCHK(ctx, q);
+        if (n_done == 0) {  // the copies ended within the first pass: count that pass
+          t_sum = t;
+          n_done = 1;
+        }
+        break;
+      }
+      float ms = 0;
+      HIPCHK(ctx, hipEventElapsedTime(&ms, a, b));
+      cc.push_back(t_sum / n_done);
+      cm.push_back(ms * 1e-3);
+    }
+    // V_GPU: the GEMV over a device copy of W
+    void *Wd = nullptr, *xd = nullptr, *yd = nullptr;
+    hetegen_status st = HETEGEN_OK;
+    std::vector<double> tg;
+    if (hipMalloc(&Wd, wbytes) != hipSuccess || hipMalloc(&xd, (size_t)B * K * 2) != hipSuccess ||
+        hipMalloc(&yd, (size_t)B * N * 4) != hipSuccess) {
+      (void)hipGetLastError();
+      st = fail(ctx, HETEGEN_ERR_OOM, "probe buffers");
+    }
+    if (st == HETEGEN_OK && (hipMemcpy(Wd, W_host, wbytes, hipMemcpyHostToDevice) != hipSuccess ||
+                             hipMemset(xd, 0, (size_t)B * K * 2) != hipSuccess))
+      st = fail(ctx, HETEGEN_ERR_HIP, "probe upload failed");
+    for (int r = 0; st == HETEGEN_OK && r < reps + 1; ++r) {
+      hg::GemvParams p{};
+      p.x = xd;
+      p.ldx = K;
+      p.W = Wd;
+      p.y = yd;
+      p.ldy = N;
+      p.rows = N;
+      p.K = K;
+      p.y_f32 = 1;
+      if (hipEventRecord(a, ctx->capture_stream) != hipSuccess ||
+          hg::launch_gemv(p, dtype, B, ctx->capture_stream, 0) != hipSuccess ||
+          hipEventRecord(b, ctx->capture_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess) {
+        st = fail(ctx, HETEGEN_ERR_HIP, "probe GEMV failed");
+        break;
+      }
+      float ms = 0;
+      (void)hipEventElapsedTime(&ms, a, b);
+      if (r > 0) tg.push_back(ms * 1e-3);
+    }
+    if (Wd) (void)hipFree(Wd);
+    if (xd) (void)hipFree(xd);
+    if (yd) (void)hipFree(yd);
+    (void)hipEventDestroy(a);
+    (void)hipEventDestroy(b);
     (void)hipGetLastError();
-    st = fail(ctx, HETEGEN_ERR_OOM, "probe buffers");
-  }
-  if (st == HETEGEN_OK && (hipMemcpy(Wd, W_host, wbytes, hipMemcpyHostToDevice) != hipSuccess ||
-                           hipMemset(xd, 0, (size_t)B * K * 2) != hipSuccess))
-    st = fail(ctx, HETEGEN_ERR_HIP, "probe upload failed");
-  for (int r = 0; st == HETEGEN_OK && r < reps + 1; ++r) {
-    hg::GemvParams p{};
-    p.x = xd;
-    p.ldx = K;
-    p.W = Wd;
-    p.y = yd;
-    p.ldy = N;
-    p.rows = N;
-    p.K = K;
-    p.y_f32 = 1;
-    if (hipEventRecord(a, ctx->capture_stream) != hipSuccess ||
-        hg::launch_gemv(p, dtype, B, ctx->capture_stream, 0) != hipSuccess ||
-        hipEventRecord(b, ctx->capture_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess) {
-      st = fail(ctx, HETEGEN_ERR_HIP, "probe GEMV failed");
-      break;
-    }
-    float ms = 0;
-    (void)hipEventElapsedTime(&ms, a, b);
-    if (r > 0) tg.push_back(ms * 1e-3);
-  }
-  if (Wd) (void)hipFree(Wd);
-  if (xd) (void)hipFree(xd);
-  if (yd) (void)hipFree(yd);
-  (void)hipEventDestroy(a);
-  (void)hipEventDestroy(b);
-  (void)hipGetLastError();
-  if (st != HETEGEN_OK) return st;
-  if (flush_sink == 0x5a5a5a5a5a5a5a5aull) ctx->err = "";  // keeps the flush reads
-  out->cpu_Bps = wbytes / median(cc.empty() ? tc : cc);
-  out->h2d_Bps = wbytes / median(cm.empty() ? tm : cm);
-  out->hbm_gemv_Bps = wbytes / median(tg);
-  out->pin_Bps = pageable ? wbytes / median(tp) : 0;
-  return HETEGEN_OK;
+    if (st != HETEGEN_OK) return st;
+    if (flush_sink == 0x5a5a5a5a5a5a5a5aull) ctx->err = "";  // keeps the flush reads
+    out->cpu_Bps = wbytes / median(cc.empty() ? tc : cc);
+    out->h2d_Bps = wbytes / median(cm.empty() ? tm : cm);
+    out->hbm_gemv_Bps = wbytes / median(tg);
+    out->pin_Bps = pageable ? wbytes / median(tp) : 0;
+    return HETEGEN_OK;
+  });
 }
 
 // ---- achievable HBM read bandwidth ----
 extern "C" hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->err.clear();
-  if (!Bps_out || reps < 1 || bytes < ((size_t)1 << 20) || (bytes & 15))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe_hbm: bad arguments");
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  void* buf = nullptr;
-  uint32_t* sink = nullptr;
-  if (hipMalloc(&buf, bytes) != hipSuccess || hipMalloc((void**)&sink, 256) != hipSuccess) {
-    (void)hipGetLastError();
-    if (buf) (void)hipFree(buf);
-    return fail(ctx, HETEGEN_ERR_OOM, "probe buffer of %zu bytes", bytes);
-  }
-  hipEvent_t a = nullptr, b = nullptr;
-  hetegen_status st = HETEGEN_OK;
-  std::vector<double> t;
-  int ncu = 0;
-  if (hipMemset(buf, 0x11, bytes) != hipSuccess || hipEventCreate(&a) != hipSuccess ||
-      hipEventCreate(&b) != hipSuccess ||
-      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess)
-    st = fail(ctx, HETEGEN_ERR_HIP, "probe setup failed");
-  for (int r = 0; st == HETEGEN_OK && r <= reps; ++r) {  // the first run warms up
-    float ms = 0;
-    if (hipEventRecord(a, ctx->capture_stream) != hipSuccess ||
-        hg::launch_read(buf, bytes, sink, 4 * std::max(ncu, 1), ctx->capture_stream) != hipSuccess ||
-        hipEventRecord(b, ctx->capture_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess ||
-        hipEventElapsedTime(&ms, a, b) != hipSuccess) {
-      st = fail(ctx, HETEGEN_ERR_HIP, "probe read kernel failed");
-      break;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!Bps_out || reps < 1 || bytes < ((size_t)1 << 20) || (bytes & 15))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe_hbm: bad arguments");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    void* buf = nullptr;
+    uint32_t* sink = nullptr;
+    if (hipMalloc(&buf, bytes) != hipSuccess || hipMalloc((void**)&sink, 256) != hipSuccess) {
+      (void)hipGetLastError();
+      if (buf) (void)hipFree(buf);
+      return fail(ctx, HETEGEN_ERR_OOM, "probe buffer of %zu bytes", bytes);
     }
-    if (r > 0) t.push_back(ms * 1e-3);
-  }
-  if (a) (void)hipEventDestroy(a);
-  if (b) (void)hipEventDestroy(b);
-  (void)hipFree(buf);
-  (void)hipFree(sink);
-  (void)hipGetLastError();
-  if (st != HETEGEN_OK) return st;
-  std::sort(t.begin(), t.end());
-  *Bps_out = (double)bytes / t[t.size() / 2];
-  return HETEGEN_OK;
+    hipEvent_t a = nullptr, b = nullptr;
+    hetegen_status st = HETEGEN_OK;
+    std::vector<double> t;
+    int ncu = 0;
+    if (hipMemset(buf, 0x11, bytes) != hipSuccess || hipEventCreate(&a) != hipSuccess ||
+        hipEventCreate(&b) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess)
+      st = fail(ctx, HETEGEN_ERR_HIP, "probe setup failed");
+    for (int r = 0; st == HETEGEN_OK && r <= reps; ++r) {  // the first run warms up
+      float ms = 0;
+      if (hipEventRecord(a, ctx->capture_stream) != hipSuccess ||
+          hg::launch_read(buf, bytes, sink, 4 * std::max(ncu, 1), ctx->capture_stream) != hipSuccess ||
+          hipEventRecord(b, ctx->capture_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess ||
+          hipEventElapsedTime(&ms, a, b) != hipSuccess) {
+        st = fail(ctx, HETEGEN_ERR_HIP, "probe read kernel failed");
+        break;
+      }
+      if (r > 0) t.push_back(ms * 1e-3);
+    }
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    (void)hipFree(buf);
+    (void)hipFree(sink);
+    (void)hipGetLastError();
+    if (st != HETEGEN_OK) return st;
+    std::sort(t.begin(), t.end());
+    *Bps_out = (double)bytes / t[t.size() / 2];
+    return HETEGEN_OK;
+  });
 }
 
 // ---- decode step over decoder-layer linears ----
@@ -1665,292 +1727,307 @@ extern "C" {
 hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype, void* const* W_host,
                                     void* const* bias_host, const double* alpha, const int* resident, int max_batch,
                                     hetegen_model** out) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->err.clear();
-  if (!out || !W_host || !alpha || L < 1 || H < 8 || F < 8 || H % 8 || F % 8 || max_batch < 1 ||
-      max_batch > kMaxBatch)
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_create: bad arguments");
-  if (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16)
-    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "model dtype: fp16 or bf16");
-  *out = nullptr;
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  hetegen_model* m = new hetegen_model();
-  m->L = L;
-  m->H = H;
-  m->F = F;
-  m->dtype = dtype;
-  m->max_batch = max_batch;
-  m->lin.resize((size_t)4 * L);
-  m->lin_ms.assign((size_t)4 * L, 0.0);
-  size_t dev_bytes = 0;
-  for (int i = 0; i < 4 * L; ++i) {
-    auto& l = m->lin[i];
-    const int which = i % 4;
-    l.N = which == 0 ? 3 * H : which == 2 ? F : H;
-    l.K = which == 3 ? F : H;
-    l.W_host = W_host[i];
-    l.bias_host = bias_host ? bias_host[i] : nullptr;
-    l.alpha = alpha[i];
-    l.resident = resident ? resident[i] != 0 : 0;
-    if (!l.W_host || !(l.alpha >= 0 && l.alpha <= 1) || !aligned16(l.W_host)) {
-      model_free(m);
-      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "linear %d: weight pointer or alpha invalid", i);
-    }
-    hetegen_status st = check_weight(ctx, l.W_host, (size_t)l.N * l.K * 2, &l.pageable);
-    if (st != HETEGEN_OK) {
-      model_free(m);
-      return st;
-    }
-    if ((size_t)l.K * 2 > ctx->chunk_bytes && !l.resident) {
-      model_free(m);
-      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "linear %d: a row exceeds chunk_bytes", i);
-    }
-    l.n_cpu = split_cpu_rows(l.N, l.alpha);
-    l.n_gpu = l.N - l.n_cpu;
-    if (l.resident) dev_bytes += align256((size_t)l.n_gpu * l.K * 2);
-    if (l.bias_host) dev_bytes += align256((size_t)l.N * 2);
-  }
-  if (dev_bytes && hipMalloc(&m->arena, dev_bytes) != hipSuccess) {
-    (void)hipGetLastError();
-    model_free(m);
-    return fail(ctx, HETEGEN_ERR_OOM, "%zu bytes of HBM for resident weights", dev_bytes);
-  }
-  char* p = (char*)m->arena;
-  for (auto& l : m->lin) {
-    if (l.resident) {
-      l.W_dev = p;
-      if (l.n_gpu > 0 && hipMemcpy(p, l.W_host, (size_t)l.n_gpu * l.K * 2, hipMemcpyHostToDevice) != hipSuccess) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!out || !W_host || !alpha || L < 1 || H < 8 || F < 8 || H % 8 || F % 8 || max_batch < 1 ||
+        max_batch > kMaxBatch)
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_create: bad arguments");
+    if (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "model dtype: fp16 or bf16");
+    *out = nullptr;
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    hetegen_model* m = new hetegen_model();
+    m->L = L;
+    m->H = H;
+    m->F = F;
+    m->dtype = dtype;
+    m->max_batch = max_batch;
+    m->lin.resize((size_t)4 * L);
+    m->lin_ms.assign((size_t)4 * L, 0.0);
+    size_t dev_bytes = 0;
+    for (int i = 0; i < 4 * L; ++i) {
+      auto& l = m->lin[i];
+      const int which = i % 4;
+      l.N = which == 0 ? 3 * H : which == 2 ? F : H;
+      l.K = which == 3 ? F : H;
+      l.W_host = W_host[i];
+      l.bias_host = bias_host ? bias_host[i] : nullptr;
+      l.alpha = alpha[i];
+      l.resident = resident ? resident[i] != 0 : 0;
+      if (!l.W_host || !(l.alpha >= 0 && l.alpha <= 1) || !aligned16(l.W_host)) {
         model_free(m);
-        return fail(ctx, HETEGEN_ERR_HIP, "resident upload failed");
+        return fail(ctx, HETEGEN_ERR_INVALID_ARG, "linear %d: weight pointer or alpha invalid", i);
       }
-      p += align256((size_t)l.n_gpu * l.K * 2);
-    }
-    if (l.bias_host) {
-      l.bias_dev = p;
-      if (hipMemcpy(p, l.bias_host, (size_t)l.N * 2, hipMemcpyHostToDevice) != hipSuccess) {
+      hetegen_status st = check_weight(ctx, l.W_host, (size_t)l.N * l.K * 2, &l.pageable);
+      if (st != HETEGEN_OK) {
         model_free(m);
-        return fail(ctx, HETEGEN_ERR_HIP, "bias upload failed");
+        return st;
       }
-      p += align256((size_t)l.N * 2);
+      if ((size_t)l.K * 2 > ctx->chunk_bytes && !l.resident) {
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "linear %d: a row exceeds chunk_bytes", i);
+      }
+      l.n_cpu = split_cpu_rows(l.N, l.alpha);
+      l.n_gpu = l.N - l.n_cpu;
+      if (l.resident) dev_bytes += align256((size_t)l.n_gpu * l.K * 2);
+      if (l.bias_host) dev_bytes += align256((size_t)l.N * 2);
     }
-  }
-  const size_t B = max_batch;
-  const size_t xb = align256(B * H * 2), qb = align256(B * 3 * H * 2), fb = align256(B * F * 2),
-               lb = align256(B * std::max(H, F) * 2);
-  if (hipMalloc(&m->act, xb + qb + fb + lb) != hipSuccess) {
-    (void)hipGetLastError();
-    model_free(m);
-    return fail(ctx, HETEGEN_ERR_OOM, "activation buffers");
-  }
-  m->xbuf = m->act;
-  m->qkv = (char*)m->act + xb;
-  m->fbuf = (char*)m->act + xb + qb;
-  m->lnbuf = (char*)m->act + xb + qb + fb;
-  // size the pinned hand-off buffers once, so no step reallocates them
-  if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
-  ctx->y_pending = false;
-  {
-    hetegen_status hs = ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, B * std::max(H, F) * 4);
-    if (hs == HETEGEN_OK) hs = ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, B * std::max(3 * H, F) * 4);
-    if (hs != HETEGEN_OK) {
-      model_free(m);
-      return hs;
-    }
-  }
-  m->graphable = true;
-  for (const auto& l : m->lin)
-    if (l.n_cpu > 0 || !l.W_dev) m->graphable = false;
-  if (m->graphable) {
-    m->ngroups = kBarrierGroups;
-    const size_t cb = (size_t)(m->ngroups + 1) * kCounterBytes;
-    if (hipMalloc((void**)&m->counters, cb) != hipSuccess ||
-        hipHostMalloc((void**)&m->err_host, sizeof(int), hipHostMallocCoherent) != hipSuccess) {
+    if (dev_bytes && hipMalloc(&m->arena, dev_bytes) != hipSuccess) {
       (void)hipGetLastError();
       model_free(m);
-      return fail(ctx, HETEGEN_ERR_OOM, "barrier counters");
+      return fail(ctx, HETEGEN_ERR_OOM, "%zu bytes of HBM for resident weights", dev_bytes);
     }
-    *m->err_host = 0;
-    if (hipMemset(m->counters, 0, cb) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+    char* p = (char*)m->arena;
+    for (auto& l : m->lin) {
+      if (l.resident) {
+        l.W_dev = p;
+        if (l.n_gpu > 0 && hipMemcpy(p, l.W_host, (size_t)l.n_gpu * l.K * 2, hipMemcpyHostToDevice) != hipSuccess) {
+          model_free(m);
+          return fail(ctx, HETEGEN_ERR_HIP, "resident upload failed");
+        }
+        p += align256((size_t)l.n_gpu * l.K * 2);
+      }
+      if (l.bias_host) {
+        l.bias_dev = p;
+        if (hipMemcpy(p, l.bias_host, (size_t)l.N * 2, hipMemcpyHostToDevice) != hipSuccess) {
+          model_free(m);
+          return fail(ctx, HETEGEN_ERR_HIP, "bias upload failed");
+        }
+        p += align256((size_t)l.N * 2);
+      }
+    }
+    const size_t B = max_batch;
+    const size_t xb = align256(B * H * 2), qb = align256(B * 3 * H * 2), fb = align256(B * F * 2),
+                 lb = align256(B * std::max(H, F) * 2);
+    if (hipMalloc(&m->act, xb + qb + fb + lb) != hipSuccess) {
+      (void)hipGetLastError();
       model_free(m);
-      return fail(ctx, HETEGEN_ERR_HIP, "barrier counter initialisation failed");
+      return fail(ctx, HETEGEN_ERR_OOM, "activation buffers");
     }
-  }
-  *out = m;
-  return HETEGEN_OK;
+    m->xbuf = m->act;
+    m->qkv = (char*)m->act + xb;
+    m->fbuf = (char*)m->act + xb + qb;
+    m->lnbuf = (char*)m->act + xb + qb + fb;
+    // size the pinned hand-off buffers once, so no step reallocates them
+    if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
+    ctx->y_pending = false;
+    {
+      hetegen_status hs = ensure_host(ctx, &ctx->x_host, &ctx->x_host_bytes, B * std::max(H, F) * 4);
+      if (hs == HETEGEN_OK) hs = ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, B * std::max(3 * H, F) * 4);
+      if (hs != HETEGEN_OK) {
+        model_free(m);
+        return hs;
+      }
+    }
+    m->graphable = true;
+    for (const auto& l : m->lin)
+      if (l.n_cpu > 0 || !l.W_dev) m->graphable = false;
+    if (m->graphable) {
+      m->ngroups = kBarrierGroups;
+      const size_t cb = (size_t)(m->ngroups + 1) * kCounterBytes;
+      if (hipMalloc((void**)&m->counters, cb) != hipSuccess ||
+          hipHostMalloc((void**)&m->err_host, sizeof(int), hipHostMallocCoherent) != hipSuccess) {
+        (void)hipGetLastError();
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_OOM, "barrier counters");
+      }
+      *m->err_host = 0;
+      if (hipMemset(m->counters, 0, cb) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_HIP, "barrier counter initialisation failed");
+      }
+    }
+    *out = m;
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_model_set_exec(hetegen_model* m, int mode, uint32_t barrier_spin_limit) {
-  if (!m || mode < HETEGEN_EXEC_AUTO || mode > HETEGEN_EXEC_EAGER) return HETEGEN_ERR_INVALID_ARG;
-  if ((mode == HETEGEN_EXEC_PERSISTENT || mode == HETEGEN_EXEC_GRAPH) && !m->graphable) return HETEGEN_ERR_UNSUPPORTED;
-  m->exec_mode = mode;
-  m->spin_limit = barrier_spin_limit;
-  return HETEGEN_OK;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!m || mode < HETEGEN_EXEC_AUTO || mode > HETEGEN_EXEC_EAGER) return HETEGEN_ERR_INVALID_ARG;
+    if ((mode == HETEGEN_EXEC_PERSISTENT || mode == HETEGEN_EXEC_GRAPH) && !m->graphable)
+      return HETEGEN_ERR_UNSUPPORTED;
+    m->exec_mode = mode;
+    m->spin_limit = barrier_spin_limit;
+    return HETEGEN_OK;
+  });
 }
 
 int hetegen_model_last_exec(const hetegen_model* m) { return m ? m->last_exec : -1; }
 
 hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {
-  if (!m || !alpha) return HETEGEN_ERR_INVALID_ARG;
-  for (size_t i = 0; i < m->lin.size(); ++i)
-    if (!m->lin[i].resident && !(alpha[i] >= 0 && alpha[i] <= 1)) return HETEGEN_ERR_INVALID_ARG;
-  for (size_t i = 0; i < m->lin.size(); ++i) {
-    auto& l = m->lin[i];
-    if (l.resident) continue;
-    l.alpha = alpha[i];
-    l.n_cpu = split_cpu_rows(l.N, l.alpha);
-    l.n_gpu = l.N - l.n_cpu;
-  }
-  return HETEGEN_OK;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!m || !alpha) return HETEGEN_ERR_INVALID_ARG;
+    for (size_t i = 0; i < m->lin.size(); ++i)
+      if (!m->lin[i].resident && !(alpha[i] >= 0 && alpha[i] <= 1)) return HETEGEN_ERR_INVALID_ARG;
+    for (size_t i = 0; i < m->lin.size(); ++i) {
+      auto& l = m->lin[i];
+      if (l.resident) continue;
+      l.alpha = alpha[i];
+      l.n_cpu = split_cpu_rows(l.N, l.alpha);
+      l.n_gpu = l.N - l.n_cpu;
+    }
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_model_get_alpha(const hetegen_model* m, double* alpha_out) {
-  if (!m || !alpha_out) return HETEGEN_ERR_INVALID_ARG;
-  for (size_t i = 0; i < m->lin.size(); ++i) alpha_out[i] = m->lin[i].alpha;
-  return HETEGEN_OK;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!m || !alpha_out) return HETEGEN_ERR_INVALID_ARG;
+    for (size_t i = 0; i < m->lin.size(); ++i) alpha_out[i] = m->lin[i].alpha;
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_model_read_ms(hetegen_ctx* ctx, const hetegen_model* m, int reps, void* stream,
                                      double* ms_out) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->err.clear();
-  if (!m || !ms_out || reps < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: bad arguments");
-  std::vector<std::pair<const void*, size_t>> bufs;
-  for (const auto& l : m->lin)
-    if (l.resident && l.n_gpu > 0 && l.W_dev) bufs.emplace_back(l.W_dev, (size_t)l.n_gpu * l.K * 2);
-  if (bufs.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: no resident GPU rows");
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  hipStream_t st = stream ? (hipStream_t)stream : ctx->capture_stream;
-  int ncu = 0;
-  HIPCHK(ctx, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device));
-  uint32_t* sink = nullptr;
-  if (hipMalloc((void**)&sink, 256) != hipSuccess) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!m || !ms_out || reps < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: bad arguments");
+    std::vector<std::pair<const void*, size_t>> bufs;
+    for (const auto& l : m->lin)
+      if (l.resident && l.n_gpu > 0 && l.W_dev) bufs.emplace_back(l.W_dev, (size_t)l.n_gpu * l.K * 2);
+    if (bufs.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: no resident GPU rows");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    hipStream_t st = stream ? (hipStream_t)stream : ctx->capture_stream;
+    int ncu = 0;
+    HIPCHK(ctx, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device));
+    uint32_t* sink = nullptr;
+    if (hipMalloc((void**)&sink, 256) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(ctx, HETEGEN_ERR_OOM, "hetegen_model_read_ms: sink");
+    }
+    hipEvent_t a = nullptr, b = nullptr;
+    hetegen_status rs = HETEGEN_OK;
+    std::vector<double> t;
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess)
+      rs = fail(ctx, HETEGEN_ERR_HIP, "hetegen_model_read_ms: events");
+    for (int r = 0; rs == HETEGEN_OK && r <= reps; ++r) {  // the first pass warms up
+      bool ok = hipEventRecord(a, st) == hipSuccess;
+      for (size_t i = 0; ok && i < bufs.size(); ++i)
+        ok = hg::launch_read(bufs[i].first, bufs[i].second, sink, 4 * std::max(ncu, 1), st) == hipSuccess;
+      float ms = 0;
+      ok = ok && hipEventRecord(b, st) == hipSuccess && hipEventSynchronize(b) == hipSuccess &&
+           hipEventElapsedTime(&ms, a, b) == hipSuccess;
+      if (!ok) rs = fail(ctx, HETEGEN_ERR_HIP, "hetegen_model_read_ms: read pass failed");
+      else if (r > 0) t.push_back(ms);
+    }
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    (void)hipFree(sink);
     (void)hipGetLastError();
-    return fail(ctx, HETEGEN_ERR_OOM, "hetegen_model_read_ms: sink");
-  }
-  hipEvent_t a = nullptr, b = nullptr;
-  hetegen_status rs = HETEGEN_OK;
-  std::vector<double> t;
-  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess)
-    rs = fail(ctx, HETEGEN_ERR_HIP, "hetegen_model_read_ms: events");
-  for (int r = 0; rs == HETEGEN_OK && r <= reps; ++r) {  // the first pass warms up
-    bool ok = hipEventRecord(a, st) == hipSuccess;
-    for (size_t i = 0; ok && i < bufs.size(); ++i)
-      ok = hg::launch_read(bufs[i].first, bufs[i].second, sink, 4 * std::max(ncu, 1), st) == hipSuccess;
-    float ms = 0;
-    ok = ok && hipEventRecord(b, st) == hipSuccess && hipEventSynchronize(b) == hipSuccess &&
-         hipEventElapsedTime(&ms, a, b) == hipSuccess;
-    if (!ok) rs = fail(ctx, HETEGEN_ERR_HIP, "hetegen_model_read_ms: read pass failed");
-    else if (r > 0) t.push_back(ms);
-  }
-  if (a) (void)hipEventDestroy(a);
-  if (b) (void)hipEventDestroy(b);
-  (void)hipFree(sink);
-  (void)hipGetLastError();
-  if (rs != HETEGEN_OK) return rs;
-  std::sort(t.begin(), t.end());
-  *ms_out = t[t.size() / 2];
-  return HETEGEN_OK;
+    if (rs != HETEGEN_OK) return rs;
+    std::sort(t.begin(), t.end());
+    *ms_out = t[t.size() / 2];
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_model_linear_ms(const hetegen_model* m, double* ms_out) {
-  if (!m || !ms_out) return HETEGEN_ERR_INVALID_ARG;
-  for (size_t i = 0; i < m->lin.size(); ++i) ms_out[i] = m->lin_ms[i];
-  return HETEGEN_OK;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!m || !ms_out) return HETEGEN_ERR_INVALID_ARG;
+    for (size_t i = 0; i < m->lin.size(); ++i) ms_out[i] = m->lin_ms[i];
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_model_alpha_benchmark(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev,
                                              int B, double gamma, double lambda, int degree, int reps, int objective,
                                              void* stream, double* delta_out, int* crossed) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  if (!m || !delta_out || !(gamma > 0) || !(lambda > 0) || reps < 1 || degree < 1 || degree > 3 ||
-      (objective != HETEGEN_BENCH_CROSSING && objective != HETEGEN_BENCH_WALL))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_alpha_benchmark: bad arguments");
-  std::vector<double> base(m->lin.size());
-  bool any = false;
-  for (size_t i = 0; i < m->lin.size(); ++i) {
-    base[i] = m->lin[i].alpha;
-    any = any || !m->lin[i].resident;
-  }
-  if (!any) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "no streamed linear to balance");
-  auto apply = [&](double d) {
-    std::vector<double> a(base);
-    for (size_t i = 0; i < a.size(); ++i)
-      if (!m->lin[i].resident) a[i] = std::min(1.0, std::max(0.0, base[i] + d));
-    return hetegen_model_set_alpha(m, a.data());
-  };
-  const bool was = ctx->profiling;
-  TRY(flush_profile(ctx));
-  const hetegen_profile saved = ctx->prof;
-  auto med = [](std::vector<double> v) {
-    std::sort(v.begin(), v.end());
-    return v[v.size() / 2];
-  };
-  // One pass measures the bracket [center - gamma, center + gamma]; when its solution
-  // is a bracket end (the curves do not meet inside, or the time still falls there),
-  // the bracket is re-centred on that end and measured again, up to kPasses in all.
-  constexpr int kPasses = 3;
-  double center = 0.0, d_best = 0.0;
-  int cr = 0;
-  hetegen_status st = HETEGEN_OK;
-  for (int pass = 0; pass < kPasses && st == HETEGEN_OK; ++pass) {
-    std::vector<double> ds, tc, tg, tw;
-    for (int i = 0;; ++i) {
-      const double d = -gamma + i * lambda;
-      if (d > gamma + 1e-9) break;
-      ds.push_back(center + std::min(d, gamma));
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    if (!m || !delta_out || !(gamma > 0) || !(lambda > 0) || reps < 1 || degree < 1 || degree > 3 ||
+        (objective != HETEGEN_BENCH_CROSSING && objective != HETEGEN_BENCH_WALL))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_alpha_benchmark: bad arguments");
+    std::vector<double> base(m->lin.size());
+    bool any = false;
+    for (size_t i = 0; i < m->lin.size(); ++i) {
+      base[i] = m->lin[i].alpha;
+      any = any || !m->lin[i].resident;
     }
-    if ((int)ds.size() < degree + 1) {
-      st = fail(ctx, HETEGEN_ERR_INVALID_ARG, "too few points in the bracket");
-      break;
-    }
-    ctx->profiling = objective == HETEGEN_BENCH_CROSSING;
-    for (double d : ds) {
-      st = apply(d);
-      std::vector<double> c, g, w;
-      for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
-        ctx->prof = hetegen_profile{};
-        auto t0 = Clock::now();
-        st = hetegen_decode_step(ctx, m, x_dev, out_dev, B, stream);
-        if (st == HETEGEN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
-          st = fail(ctx, HETEGEN_ERR_HIP, "hipStreamSynchronize failed");
-        const double wall = ms_since(t0);
-        if (st == HETEGEN_OK) st = flush_profile(ctx);
-        if (st == HETEGEN_OK && r > 0) {
-          c.push_back(ctx->prof.cpu_ms);
-          g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
-          w.push_back(wall);
-        }
+    if (!any) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "no streamed linear to balance");
+    auto apply = [&](double d) {
+      std::vector<double> a(base);
+      for (size_t i = 0; i < a.size(); ++i)
+        if (!m->lin[i].resident) a[i] = std::min(1.0, std::max(0.0, base[i] + d));
+      return hetegen_model_set_alpha(m, a.data());
+    };
+    const bool was = ctx->profiling;
+    TRY(flush_profile(ctx));
+    const hetegen_profile saved = ctx->prof;
+    auto med = [](std::vector<double> v) {
+      std::sort(v.begin(), v.end());
+      return v[v.size() / 2];
+    };
+    // One pass measures the bracket [center - gamma, center + gamma]; when its solution
+    // is a bracket end (the curves do not meet inside, or the time still falls there),
+    // the bracket is re-centred on that end and measured again, up to kPasses in all.
+    constexpr int kPasses = 3;
+    double center = 0.0, d_best = 0.0;
+    int cr = 0;
+    hetegen_status st = HETEGEN_OK;
+    for (int pass = 0; pass < kPasses && st == HETEGEN_OK; ++pass) {
+      std::vector<double> ds, tc, tg, tw;
+      for (int i = 0;; ++i) {
+        const double d = -gamma + i * lambda;
+        if (d > gamma + 1e-9) break;
+        ds.push_back(center + std::min(d, gamma));
       }
+      if ((int)ds.size() < degree + 1) {
+        st = fail(ctx, HETEGEN_ERR_INVALID_ARG, "too few points in the bracket");
+        break;
+      }
+      ctx->profiling = objective == HETEGEN_BENCH_CROSSING;
+      for (double d : ds) {
+        st = apply(d);
+        std::vector<double> c, g, w;
+        for (int r = 0; r <= reps && st == HETEGEN_OK; ++r) {
+          ctx->prof = hetegen_profile{};
+          auto t0 = Clock::now();
+          st = hetegen_decode_step(ctx, m, x_dev, out_dev, B, stream);
+          if (st == HETEGEN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+            st = fail(ctx, HETEGEN_ERR_HIP, "hipStreamSynchronize failed");
+          const double wall = ms_since(t0);
+          if (st == HETEGEN_OK) st = flush_profile(ctx);
+          if (st == HETEGEN_OK && r > 0) {
+            c.push_back(ctx->prof.cpu_ms);
+            g.push_back(ctx->prof.h2d_ms + ctx->prof.gpu_ms);
+            w.push_back(wall);
+          }
+        }
+        if (st != HETEGEN_OK) break;
+        tc.push_back(med(c));
+        tg.push_back(med(g));
+        tw.push_back(med(w));
+      }
+      ctx->profiling = was;
       if (st != HETEGEN_OK) break;
-      tc.push_back(med(c));
-      tg.push_back(med(g));
-      tw.push_back(med(w));
+      const double lo = center - gamma, hi = center + gamma;
+      hetegen_status fs = objective == HETEGEN_BENCH_CROSSING
+                              ? hetegen_alpha_fit(ds.data(), tc.data(), tg.data(), (int)ds.size(), degree, lo, hi,
+                                                  &d_best, &cr)
+                              : hetegen_alpha_minimize(ds.data(), tw.data(), (int)ds.size(), degree, lo, hi, &d_best);
+      if (fs != HETEGEN_OK) {
+        st = fail(ctx, fs, "alpha fit failed");
+        break;
+      }
+      const bool at_end = (d_best <= lo || d_best >= hi) && !(objective == HETEGEN_BENCH_CROSSING && cr);
+      if (!at_end) break;
+      center = d_best;
     }
+    ctx->prof = saved;
     ctx->profiling = was;
-    if (st != HETEGEN_OK) break;
-    const double lo = center - gamma, hi = center + gamma;
-    hetegen_status fs = objective == HETEGEN_BENCH_CROSSING
-                            ? hetegen_alpha_fit(ds.data(), tc.data(), tg.data(), (int)ds.size(), degree, lo, hi,
-                                                &d_best, &cr)
-                            : hetegen_alpha_minimize(ds.data(), tw.data(), (int)ds.size(), degree, lo, hi, &d_best);
-    if (fs != HETEGEN_OK) {
-      st = fail(ctx, fs, "alpha fit failed");
-      break;
+    if (st != HETEGEN_OK) {
+      (void)hetegen_model_set_alpha(m, base.data());
+      return st;
     }
-    const bool at_end = (d_best <= lo || d_best >= hi) && !(objective == HETEGEN_BENCH_CROSSING && cr);
-    if (!at_end) break;
-    center = d_best;
-  }
-  ctx->prof = saved;
-  ctx->profiling = was;
-  if (st != HETEGEN_OK) {
-    (void)hetegen_model_set_alpha(m, base.data());
-    return st;
-  }
-  TRY(apply(d_best));
-  *delta_out = d_best;
-  if (crossed) *crossed = cr;
-  return HETEGEN_OK;
+    TRY(apply(d_best));
+    *delta_out = d_best;
+    if (crossed) *crossed = cr;
+    return HETEGEN_OK;
+  });
 }
 
 size_t hetegen_model_trace_bytes(const hetegen_model* m, int B) {
@@ -1961,127 +2038,137 @@ size_t hetegen_model_trace_bytes(const hetegen_model* m, int B) {
 }
 
 hetegen_status hetegen_model_set_trace(hetegen_model* m, void* trace_dev, size_t bytes) {
-  if (!m) return HETEGEN_ERR_INVALID_ARG;
-  if (trace_dev && !aligned16(trace_dev)) return HETEGEN_ERR_INVALID_ARG;
-  m->trace = trace_dev;
-  m->trace_bytes = trace_dev ? bytes : 0;
-  return HETEGEN_OK;
+  return api_guard(nullptr, [&]() -> hetegen_status {
+    if (!m) return HETEGEN_ERR_INVALID_ARG;
+    if (trace_dev && !aligned16(trace_dev)) return HETEGEN_ERR_INVALID_ARG;
+    m->trace = trace_dev;
+    m->trace_bytes = trace_dev ? bytes : 0;
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_model_destroy(hetegen_ctx* ctx, hetegen_model* m) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  if (!m) return HETEGEN_OK;
-  (void)hipSetDevice(ctx->device);
-  (void)hipDeviceSynchronize();
-  model_free(m);
-  return HETEGEN_OK;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    if (!m) return HETEGEN_OK;
+    (void)hipSetDevice(ctx->device);
+    (void)hipDeviceSynchronize();
+    model_free(m);
+    return HETEGEN_OK;
+  });
 }
 
 hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
                                    void* stream) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  auto t0 = Clock::now();
-  ctx->err.clear();
-  if (!m || !x_dev || !out_dev || x_dev == out_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "decode_step: bad pointers");
-  if (B < 1 || B > m->max_batch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, m->max_batch);
-  if (!aligned16(x_dev) || !aligned16(out_dev)) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
-  if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
-  if (m->err_host && *(volatile int*)m->err_host)
-    return fail(ctx, HETEGEN_ERR_HIP, "a grid-barrier wait of an earlier persistent step gave up; that step's "
-                                      "output is undefined");
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  hipStream_t st = (hipStream_t)stream;
-  // AUTO runs per-linear launches directly: on this device back-to-back GEMV launches
-  // leave no gap, and the grid barrier of the persistent step costs more than a launch
-  const bool fast = m->graphable && !m->trace && !ctx->profiling && m->exec_mode != HETEGEN_EXEC_EAGER &&
-                    m->exec_mode != HETEGEN_EXEC_AUTO;
-  if (fast && m->exec_mode == HETEGEN_EXEC_PERSISTENT) {
-    bool launched = false;
-    TRY(run_persistent(ctx, m, x_dev, out_dev, B, st, &launched));
-    if (launched) {
-      m->last_exec = HETEGEN_EXEC_PERSISTENT;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    auto t0 = Clock::now();
+    ctx->err.clear();
+    if (!m || !x_dev || !out_dev || x_dev == out_dev)
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "decode_step: bad pointers");
+    if (B < 1 || B > m->max_batch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, m->max_batch);
+    if (!aligned16(x_dev) || !aligned16(out_dev))
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
+    if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
+    if (m->err_host && *(volatile int*)m->err_host)
+      return fail(ctx, HETEGEN_ERR_HIP, "a grid-barrier wait of an earlier persistent step gave up; that step's "
+                                        "output is undefined");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    hipStream_t st = (hipStream_t)stream;
+    // AUTO runs per-linear launches directly: on this device back-to-back GEMV launches
+    // leave no gap, and the grid barrier of the persistent step costs more than a launch
+    const bool fast = m->graphable && !m->trace && !ctx->profiling && m->exec_mode != HETEGEN_EXEC_EAGER &&
+                      m->exec_mode != HETEGEN_EXEC_AUTO;
+    if (fast && m->exec_mode == HETEGEN_EXEC_PERSISTENT) {
+      bool launched = false;
+      TRY(run_persistent(ctx, m, x_dev, out_dev, B, st, &launched));
+      if (launched) {
+        m->last_exec = HETEGEN_EXEC_PERSISTENT;
+        return finish_call(ctx, t0);
+      }
+      if (m->exec_mode == HETEGEN_EXEC_PERSISTENT)
+        return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "the persistent step cannot run for batch %d on this device", B);
+    }
+    const bool use_graph = fast;
+    if (use_graph) {
+      if (!m->gexec || m->g_B != B || m->g_x != x_dev || m->g_out != out_dev) {
+        if (m->gexec) {
+          HIPCHK(ctx, hipGraphExecDestroy(m->gexec));
+          m->gexec = nullptr;
+        }
+        hipGraph_t g = nullptr;
+        HIPCHK(ctx, hipStreamBeginCapture(ctx->capture_stream, hipStreamCaptureModeThreadLocal));
+        hetegen_status cs = enqueue_step(ctx, m, x_dev, out_dev, B, ctx->capture_stream);
+        hipError_t ce = hipStreamEndCapture(ctx->capture_stream, &g);
+        if (cs != HETEGEN_OK) {
+          if (g) (void)hipGraphDestroy(g);
+          return cs;
+        }
+        if (ce != hipSuccess) return fail(ctx, HETEGEN_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ce));
+        hipError_t ie = hipGraphInstantiate(&m->gexec, g, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(g);
+        if (ie != hipSuccess) {
+          m->gexec = nullptr;
+          return fail(ctx, HETEGEN_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
+        }
+        m->g_B = B;
+        m->g_x = x_dev;
+        m->g_out = out_dev;
+      }
+      HIPCHK(ctx, hipGraphLaunch(m->gexec, st));
+      m->last_exec = HETEGEN_EXEC_GRAPH;
       return finish_call(ctx, t0);
     }
-    if (m->exec_mode == HETEGEN_EXEC_PERSISTENT)
-      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "the persistent step cannot run for batch %d on this device", B);
-  }
-  const bool use_graph = fast;
-  if (use_graph) {
-    if (!m->gexec || m->g_B != B || m->g_x != x_dev || m->g_out != out_dev) {
-      if (m->gexec) {
-        HIPCHK(ctx, hipGraphExecDestroy(m->gexec));
-        m->gexec = nullptr;
-      }
-      hipGraph_t g = nullptr;
-      HIPCHK(ctx, hipStreamBeginCapture(ctx->capture_stream, hipStreamCaptureModeThreadLocal));
-      hetegen_status cs = enqueue_step(ctx, m, x_dev, out_dev, B, ctx->capture_stream);
-      hipError_t ce = hipStreamEndCapture(ctx->capture_stream, &g);
-      if (cs != HETEGEN_OK) {
-        if (g) (void)hipGraphDestroy(g);
-        return cs;
-      }
-      if (ce != hipSuccess) return fail(ctx, HETEGEN_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ce));
-      hipError_t ie = hipGraphInstantiate(&m->gexec, g, nullptr, nullptr, 0);
-      (void)hipGraphDestroy(g);
-      if (ie != hipSuccess) {
-        m->gexec = nullptr;
-        return fail(ctx, HETEGEN_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
-      }
-      m->g_B = B;
-      m->g_x = x_dev;
-      m->g_out = out_dev;
+    m->last_exec = HETEGEN_EXEC_EAGER;
+    hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, st);
+    if (s != HETEGEN_OK) {
+      reset_pipeline(ctx);
+      return s;
     }
-    HIPCHK(ctx, hipGraphLaunch(m->gexec, st));
-    m->last_exec = HETEGEN_EXEC_GRAPH;
     return finish_call(ctx, t0);
-  }
-  m->last_exec = HETEGEN_EXEC_EAGER;
-  hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, st);
-  if (s != HETEGEN_OK) {
-    reset_pipeline(ctx);
-    return s;
-  }
-  return finish_call(ctx, t0);
+  });
 }
 
 // ---- KV cache and attention steps (Sec. 2.1, Eq. 1) ----
 hetegen_status hetegen_model_kv_create(hetegen_ctx* ctx, hetegen_model* m, int max_seq, int head_dim) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->err.clear();
-  if (!m || max_seq < 1 || max_seq > hg::attn_max_positions())
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv_create: max_seq %d outside [1, %d]", max_seq,
-                hg::attn_max_positions());
-  if ((head_dim != 64 && head_dim != 128) || m->H % head_dim)
-    return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "head_dim %d: 64 or 128, dividing H = %d", head_dim, m->H);
-  if (m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv_create: the model already has a KV cache");
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  const int chunk = hg::attn_chunk();
-  m->heads = m->H / head_dim;
-  m->head_dim = head_dim;
-  m->kv_seq = max_seq;
-  m->kv_chunks = (max_seq + chunk - 1) / chunk;
-  const size_t kv_bytes = 2 * (size_t)m->L * kv_layer_elems(m) * 2;
-  const size_t part_bytes = (size_t)m->max_batch * m->heads * m->kv_chunks * (head_dim + 2) * sizeof(float);
-  const size_t cnt_bytes = (size_t)m->max_batch * m->heads * sizeof(uint32_t);
-  if (hipMalloc(&m->kv, kv_bytes) != hipSuccess || hipMalloc((void**)&m->kv_part, part_bytes) != hipSuccess ||
-      hipMalloc((void**)&m->kv_cnt, cnt_bytes) != hipSuccess ||
-      hipMalloc(&m->abuf, (size_t)m->max_batch * m->H * 2) != hipSuccess) {
-    (void)hipGetLastError();
-    if (m->kv) (void)hipFree(m->kv);
-    if (m->kv_part) (void)hipFree(m->kv_part);
-    if (m->kv_cnt) (void)hipFree(m->kv_cnt);
-    if (m->abuf) (void)hipFree(m->abuf);
-    m->kv = nullptr;
-    m->kv_part = nullptr;
-    m->kv_cnt = nullptr;
-    m->abuf = nullptr;
-    m->kv_seq = 0;
-    return fail(ctx, HETEGEN_ERR_OOM, "KV cache of %zu bytes", kv_bytes);
-  }
-  HIPCHK(ctx, hipMemset(m->kv_cnt, 0, cnt_bytes));
-  HIPCHK(ctx, hipMemset(m->kv, 0, kv_bytes));
-  return HETEGEN_OK;
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!m || max_seq < 1 || max_seq > hg::attn_max_positions())
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv_create: max_seq %d outside [1, %d]", max_seq,
+                  hg::attn_max_positions());
+    if ((head_dim != 64 && head_dim != 128) || m->H % head_dim)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "head_dim %d: 64 or 128, dividing H = %d", head_dim, m->H);
+    if (m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "kv_create: the model already has a KV cache");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    const int chunk = hg::attn_chunk();
+    m->heads = m->H / head_dim;
+    m->head_dim = head_dim;
+    m->kv_seq = max_seq;
+    m->kv_chunks = (max_seq + chunk - 1) / chunk;
+    const size_t kv_bytes = 2 * (size_t)m->L * kv_layer_elems(m) * 2;
+    const size_t part_bytes = (size_t)m->max_batch * m->heads * m->kv_chunks * (head_dim + 2) * sizeof(float);
+    const size_t cnt_bytes = (size_t)m->max_batch * m->heads * sizeof(uint32_t);
+    if (hipMalloc(&m->kv, kv_bytes) != hipSuccess || hipMalloc((void**)&m->kv_part, part_bytes) != hipSuccess ||
+        hipMalloc((void**)&m->kv_cnt, cnt_bytes) != hipSuccess ||
+        hipMalloc(&m->abuf, (size_t)m->max_batch * m->H * 2) != hipSuccess) {
+      (void)hipGetLastError();
+      if (m->kv) (void)hipFree(m->kv);
+      if (m->kv_part) (void)hipFree(m->kv_part);
+      if (m->kv_cnt) (void)hipFree(m->kv_cnt);
+      if (m->abuf) (void)hipFree(m->abuf);
+      m->kv = nullptr;
+      m->kv_part = nullptr;
+      m->kv_cnt = nullptr;
+      m->abuf = nullptr;
+      m->kv_seq = 0;
+      return fail(ctx, HETEGEN_ERR_OOM, "KV cache of %zu bytes", kv_bytes);
+    }
+    HIPCHK(ctx, hipMemset(m->kv_cnt, 0, cnt_bytes));
+    HIPCHK(ctx, hipMemset(m->kv, 0, kv_bytes));
+    return HETEGEN_OK;
+  });
 }
 
 }  // extern "C"
@@ -2118,40 +2205,48 @@ extern "C" {
 
 hetegen_status hetegen_model_kv_write(hetegen_ctx* ctx, hetegen_model* m, int layer, int B, int pos0, int n,
                                       const void* k_dev, const void* v_dev, void* stream) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->err.clear();
-  return kv_copy(ctx, m, layer, B, pos0, n, const_cast<void*>(k_dev), const_cast<void*>(v_dev),
-                 (hipStream_t)stream, true);
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    return kv_copy(ctx, m, layer, B, pos0, n, const_cast<void*>(k_dev), const_cast<void*>(v_dev),
+                   (hipStream_t)stream, true);
+  });
 }
 
 hetegen_status hetegen_model_kv_read(hetegen_ctx* ctx, hetegen_model* m, int layer, int B, int pos0, int n,
                                      void* k_dev, void* v_dev, void* stream) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  ctx->err.clear();
-  return kv_copy(ctx, m, layer, B, pos0, n, k_dev, v_dev, (hipStream_t)stream, false);
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    return kv_copy(ctx, m, layer, B, pos0, n, k_dev, v_dev, (hipStream_t)stream, false);
+  });
 }
 
 hetegen_status hetegen_decode_step_kv(hetegen_ctx* ctx, hetegen_model* m, const void* x_dev, void* out_dev, int B,
                                       int pos, void* stream) {
-  if (!ctx) return HETEGEN_ERR_INVALID_ARG;
-  auto t0 = Clock::now();
-  ctx->err.clear();
-  if (!m || !x_dev || !out_dev || x_dev == out_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "decode_step: bad pointers");
-  if (!m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "the model has no KV cache (hetegen_model_kv_create)");
-  if (pos < 0 || pos >= m->kv_seq)
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "position %d outside the cache [0, %d)", pos, m->kv_seq);
-  if (B < 1 || B > m->max_batch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, m->max_batch);
-  if (!aligned16(x_dev) || !aligned16(out_dev)) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
-  if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
-    return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
-  HIPCHK(ctx, hipSetDevice(ctx->device));
-  m->last_exec = HETEGEN_EXEC_EAGER;
-  hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, (hipStream_t)stream, pos);
-  if (s != HETEGEN_OK) {
-    reset_pipeline(ctx);
-    return s;
-  }
-  return finish_call(ctx, t0);
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    auto t0 = Clock::now();
+    ctx->err.clear();
+    if (!m || !x_dev || !out_dev || x_dev == out_dev)
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "decode_step: bad pointers");
+    if (!m->kv) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "the model has no KV cache (hetegen_model_kv_create)");
+    if (pos < 0 || pos >= m->kv_seq)
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "position %d outside the cache [0, %d)", pos, m->kv_seq);
+    if (B < 1 || B > m->max_batch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, m->max_batch);
+    if (!aligned16(x_dev) || !aligned16(out_dev))
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x/out must be 16-byte aligned");
+    if (m->trace && m->trace_bytes < hetegen_model_trace_bytes(m, B))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "trace buffer too small");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    m->last_exec = HETEGEN_EXEC_EAGER;
+    hetegen_status s = enqueue_step(ctx, m, x_dev, out_dev, B, (hipStream_t)stream, pos);
+    if (s != HETEGEN_OK) {
+      reset_pipeline(ctx);
+      return s;
+    }
+    return finish_call(ctx, t0);
+  });
 }
 
 }  // extern "C"
