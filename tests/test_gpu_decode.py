@@ -524,6 +524,33 @@ def test_kv_opt67b_shape_one_layer_context_512(ctx):
         m.free()
 
 
+def test_kv_largest_cache_last_position(ctx):
+    # the largest cache the header allows (16384 positions), decoding its last position: 256
+    # chunks, all but the first 16 merged through the kernel's tail loop
+    dtype, L, H, F, B, D, S = synth.F16, 1, 256, 512, 2, 128, 16384
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=2)
+    try:
+        hg.hetegen_model_kv_create(ctx, m.m, S, D)
+        kc, vc = _fill_cache(m, B, S - 1)
+        x = synth.normal((B, H), dtype, 0, synth.act_id(S))
+        out, tr = m.step_kv(x, S - 1, trace=True)
+        last, _ = m.check_teacher_forced(x, tr, attn=_attn_ref(m, kc, vc, D))
+        assert np.array_equal(out, last)
+        with pytest.raises(hg.HetegenError):  # one past the cache
+            hg.hetegen_decode_step_kv(ctx, m.m, torch_dev_from_np(x).data_ptr(),
+                                      torch.zeros((B, H), dtype=torch.int16, device="cuda").data_ptr(), B, S,
+                                      torch.cuda.current_stream().cuda_stream)
+    finally:
+        m.free()
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
+    try:
+        with pytest.raises(hg.HetegenError) as e:  # larger than the kernel supports
+            hg.hetegen_model_kv_create(ctx, m.m, S + 1, D)
+        assert e.value.status == hg.ERR_INVALID_ARG
+    finally:
+        m.free()
+
+
 def test_kv_argument_errors(ctx):
     dtype, L, H, F = synth.F16, 1, 256, 512
     m = Model(ctx, L, H, F, dtype, 0.0, 1)
