@@ -219,6 +219,7 @@ def test_argument_errors(ctx):
         assert status(B=0) == hg.ERR_UNSUPPORTED
         assert status(B=9) == hg.ERR_UNSUPPORTED
         assert status(K=60) == hg.ERR_UNSUPPORTED
+        assert status(K=0) == hg.ERR_UNSUPPORTED
         assert status(x=0) == hg.ERR_INVALID_ARG
         assert status(N=0) == hg.ERR_INVALID_ARG
         assert status(ydt=hg.BF16) == hg.ERR_UNSUPPORTED
