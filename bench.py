@@ -500,6 +500,14 @@ def main():
                         "tokens_per_s": round(B * 1e3 / ms_step, 2),
                         "weight_plus_kv_GBps": round((wbytes + kv_b) / (ms_step * 1e-3) / 1e9, 1)}
         log("kv: %s" % json.dumps(result["kv"]))
+        if not streamed:
+            # the step as a whole against HBM: weights, keys and values read once per step
+            # (the attention launches are latency-bound; their own times are in the kernel trace)
+            ach = (wbytes + kv_b) / (ms_step * 1e-3) / 1e9
+            result["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                  "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None,
+                                  "kernel": "whole step: %d GEMV launches + %d attn_kernel launches" % (4 * L, L),
+                                  "bytes_per_step": int(wbytes + kv_b)}
     if not streamed and P == 0:
         # dominant kernel: every dispatch of the timed region is the GEMV kernel (LayerNorm,
         # value slice, ReLU and residual are fused into it): one persistent step kernel per
