@@ -11,7 +11,7 @@ ReLU and residual fused into them.
 Other workloads (--model): opt-13b (layers 0-19 resident, 20-39 streamed from
 pinned host with the planner's CPU fraction), opt-30b (all linears in pinned host
 memory, planner alpha), opt-66b (bf16, all host, --alpha sweep).  For those the
-planner's speeds come from hetegen_probe on the box, and the JSON line adds the
+planner's speeds come from hetegen_probe on this machine, and the JSON line adds the
 heterogeneous figures (link and CPU rates, Table-2-style busy fractions).
 --placement sched lets the module scheduler (Sec. 4.5) pick the resident linears
 under --hbm-budget; --pageable keeps the weights in plain pageable memory, streamed
@@ -287,8 +287,8 @@ def main():
     ap.add_argument("--linear-reps", type=int, default=200)
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (the heterogeneous "
-              "linear would shard by output rows across GPUs, see the design notes); run with --gpus 1",
+        print("bench.py measures one GPU only: there is no multi-GPU path (the heterogeneous "
+              "linear would shard by output rows across GPUs); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 

@@ -2,8 +2,8 @@
 
 HeteGen applies heterogeneous parallelism to the linear modules only and keeps the
 other modules on the GPU (Sec. 4.2); decoding feeds one token per step through
-every layer (Sec. 2.1, Eq. 1).  The glue between the linears is this build's
-reading (the paper leaves it to the model): a pre-LayerNorm OPT-style layer with an
+every layer (Sec. 2.1, Eq. 1).  The glue between the linears is a reading (the
+paper leaves it to the model): a pre-LayerNorm OPT-style layer with an
 empty KV cache, where one-position attention returns the value projection exactly.
 
 Per layer, with act() = round-to-nearest-even to the activation type:

@@ -15,7 +15,7 @@ approximated by Eq. 6 (GPU time neglected) as alpha ~ V_COM / (V_COM + V_CPU),
 which Eq. 7 restates with whole-module times T' = W / V.  Sec. 4.2 (Eq. 8-9) splits
 communication into pinning and transfer that run concurrently, so T_COM =
 max(T_PIN, T_TRANS), i.e. V_COM = min(V_PIN, V_TRANS); with weights pinned once at
-load time the pin term vanishes (reading of the design notes).
+load time the pin term vanishes (a reading: the paper pins per module at run time).
 
 The library's alpha is the CPU fraction, 1 - alpha_paper; a module kept wholly on
 the GPU (Sec. 4.5, the module scheduler's placement) has CPU fraction 0.
