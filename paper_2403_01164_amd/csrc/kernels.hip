@@ -859,6 +859,73 @@ __global__ __launch_bounds__(kThreads) void layernorm_kernel(const uint16_t* __r
   }
 }
 
+// The same LayerNorm with the row held in registers (thread t keeps chunks t + 256 i, the
+// chunks ln_stats gives it, for i < NI): the row is read from memory once instead of once
+// per pass, and every sum is formed in ln_stats' order, so the bits are the same.
+template <class T, int NI>
+__global__ __launch_bounds__(kThreads) void layernorm_regs_kernel(const uint16_t* __restrict__ x, long long ldx,
+                                                                  int K, uint16_t* __restrict__ h, long long ldh,
+                                                                  float* __restrict__ h_host) {
+  __shared__ float red[2][kWaves];
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint16_t* xr = x + b * ldx;
+  const int n8 = K >> 3;  // <= kThreads * NI (launcher)
+  uint4 v[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int c = tid + kThreads * i;
+    v[i] = c < n8 ? *(const uint4*)(xr + (long long)c * 8) : make_uint4(0u, 0u, 0u, 0u);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    if (tid + kThreads * i < n8) {
+      float f[8];
+      unpack8<T>(v[i], f);
+      s += ((f[0] + f[1]) + (f[2] + f[3])) + ((f[4] + f[5]) + (f[6] + f[7]));
+    }
+  }
+  s = wave_sum(s);
+  if (lane == 0) red[0][wave] = s;
+  __syncthreads();
+  const float mean = ((red[0][0] + red[0][1]) + (red[0][2] + red[0][3])) / (float)K;
+  s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    if (tid + kThreads * i < n8) {
+      float f[8];
+      unpack8<T>(v[i], f);
+      float acc = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float d = f[e] - mean;
+        acc += d * d;
+      }
+      s += acc;
+    }
+  }
+  s = wave_sum(s);
+  if (lane == 0) red[1][wave] = s;
+  __syncthreads();
+  const float var = ((red[1][0] + red[1][1]) + (red[1][2] + red[1][3])) / (float)K;
+  const float rstd = 1.0f / sqrtf(var + kLnEps);
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int c = tid + kThreads * i;
+    if (c < n8) {
+      const uint4 o = normalize8<T>(v[i], mean, rstd);
+      *(uint4*)(h + b * ldh + (long long)c * 8) = o;
+      if (h_host) {
+        float f[8];
+        unpack8<T>(o, f);
+        float4* dst = (float4*)(h_host + (long long)b * K + (long long)c * 8);
+        dst[0] = make_float4(f[0], f[1], f[2], f[3]);
+        dst[1] = make_float4(f[4], f[5], f[6], f[7]);
+      }
+    }
+  }
+}
+
 template <class T>
 __global__ __launch_bounds__(kThreads) void export_kernel(const uint16_t* __restrict__ x, long long ldx, int B, int K,
                                                           float* __restrict__ dst) {
@@ -1015,10 +1082,32 @@ hipError_t launch_gemv_t(const GemvParams& p, int B, hipStream_t s, int cap) {
   return hipErrorInvalidValue;
 }
 
+template <class T, int NI>
+hipError_t launch_ln_regs(int B, const uint16_t* x, long long ldx, int K, uint16_t* h, long long ldh, float* hh,
+                          hipStream_t s) {
+  hipLaunchKernelGGL((layernorm_regs_kernel<T, NI>), dim3(1, B), dim3(kThreads), 0, s, x, ldx, K, h, ldh, hh);
+  return hipGetLastError();
+}
+
 template <class T>
 hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long long ldh, float* hh, hipStream_t s) {
   if (B < 1 || B > 8) return hipErrorInvalidValue;
   const int n8 = K >> 3;
+  // rows of up to 8 * kThreads * 8 elements (hidden sizes up to 16384) stay in registers
+  const int ni = (n8 + kThreads - 1) / kThreads;
+  const uint16_t* xx = (const uint16_t*)x;
+  uint16_t* hp = (uint16_t*)h;
+  switch (ni) {
+    case 1: return launch_ln_regs<T, 1>(B, xx, ldx, K, hp, ldh, hh, s);
+    case 2: return launch_ln_regs<T, 2>(B, xx, ldx, K, hp, ldh, hh, s);
+    case 3: return launch_ln_regs<T, 3>(B, xx, ldx, K, hp, ldh, hh, s);
+    case 4: return launch_ln_regs<T, 4>(B, xx, ldx, K, hp, ldh, hh, s);
+    case 5: return launch_ln_regs<T, 5>(B, xx, ldx, K, hp, ldh, hh, s);
+    case 6:
+    case 7:
+    case 8: return launch_ln_regs<T, 8>(B, xx, ldx, K, hp, ldh, hh, s);
+    default: break;
+  }
   int grid = (n8 + kThreads * 4 - 1) / (kThreads * 4);
   if (grid < 1) grid = 1;
   if (grid > 16) grid = 16;
