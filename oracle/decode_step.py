@@ -20,7 +20,6 @@ The linears are the oracle's binary32 linear; LN, ReLU and the residual sum are
 done in float64 on the decoded values.
 """
 import numpy as np
-import torch
 
 from . import F16, BF16, F32, decode, linear
 
@@ -35,20 +34,42 @@ def layer_norm(x):
     return (x - mu) / np.sqrt(var + LN_EPS)
 
 
+BF16_MAX = (2.0 - 2.0 ** -7) * 2.0 ** 127  # largest finite bfloat16
+
+
+def _bf16_round(v):
+    """Round float64 values once to bfloat16, nearest with ties to even; bit patterns.
+
+    bfloat16 has binary32's sign and 8-bit exponent and 8 significand bits (7 stored).
+    A value of magnitude 2^e <= |v| < 2^(e+1) is rounded to a multiple of its spacing
+    2^(e-7); below the smallest normal 2^-126 the spacing stays 2^-133 (subnormals).
+    |v| / spacing is exact in float64 and np.rint rounds its halves to even, which is
+    the even last significand bit.  Results beyond the largest finite value are
+    infinities; NaN becomes the quiet NaN 0x7FC0.
+    """
+    v = np.asarray(v, dtype=np.float64)
+    a = np.abs(v)
+    _, e = np.frexp(a)                      # a = m 2^e, 0.5 <= m < 1: exponent e - 1
+    spacing = np.ldexp(1.0, np.maximum(e - 1, -126) - 7)
+    with np.errstate(over="ignore", invalid="ignore"):
+        r = np.rint(a / spacing) * spacing
+        mag = np.where(r > BF16_MAX, np.inf, r).astype(np.float32)  # exact: r has 8 bits
+    bits = (mag.view(np.uint32) >> 16).astype(np.uint16)
+    bits = np.where(np.signbit(v), bits | np.uint16(0x8000), bits)
+    return np.where(np.isnan(v), np.uint16(0x7FC0), bits).astype(np.uint16)
+
+
 def to_bits(v, dtype):
-    """Round float values to dtype (nearest even) and return the bit patterns."""
+    """Round float values once to dtype (nearest, ties to even); bit patterns (binary32
+    values for F32)."""
     v = np.asarray(v, dtype=np.float64)
     if dtype == F16:
-        # float64 -> float16 directly (one rounding)
-        return v.astype(np.float16).view(np.uint16)
+        # float64 -> float16 directly (one rounding); beyond the range: infinities
+        with np.errstate(over="ignore"):
+            return v.astype(np.float16).view(np.uint16)
     if dtype == BF16:
-        t = torch.from_numpy(np.ascontiguousarray(v)).to(torch.bfloat16)
-        return t.view(torch.int16).numpy().view(np.uint16)
+        return _bf16_round(v)
     return v.astype(np.float32)
-
-
-def act(v, dtype):
-    return decode(to_bits(v, dtype), dtype).astype(np.float64)
 
 
 def decode_step(x_bits, layers, H, dtype):

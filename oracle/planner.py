@@ -60,7 +60,3 @@ def balance_residual(alpha_gpu, V_cpu, V_gpu, V_com):
     """Left minus right side of Eq. 4 per unit of W (seconds per byte)."""
     return (1.0 - alpha_gpu) / V_cpu - (alpha_gpu / V_gpu + alpha_gpu / V_com)
 
-
-def step_time(alpha_gpu, W, V_cpu, V_gpu, V_com):
-    """Module time when CPU and GPU(+transfer) parts run concurrently (Fig. 3a)."""
-    return max((1.0 - alpha_gpu) * W / V_cpu, alpha_gpu * W / V_gpu + alpha_gpu * W / V_com)

@@ -17,15 +17,74 @@ def test_layer_norm_matches_torch_and_invariants():
     assert np.allclose((ours ** 2).mean(-1), 1 / (1 + ds.LN_EPS / x.var(-1)), rtol=1e-12)
 
 
+def _f32(bits):
+    return np.array([bits], np.uint32).view(np.float32)[0]
+
+
+# Hand-worked rounding cases: (float64 value, expected 16-bit pattern).
+# bfloat16 keeps 7 significand bits after the point, so 1 + 2^-8 is the tie between
+# 0x3F80 (1) and 0x3F81 (1 + 2^-7); ties go to the even last bit.
+BF16_CASES = [
+    (float(_f32(0x3F808000)), 0x3F80),            # 1 + 2^-8: tie, down to even
+    (float(_f32(0x3F818000)), 0x3F82),            # 1 + 3 * 2^-8: tie, up to even
+    (float(_f32(0x3F808001)), 0x3F81),            # just above the tie
+    (float(_f32(0x3F807FFF)), 0x3F80),            # just below the tie
+    (-float(_f32(0x3F818000)), 0xBF82),           # sign kept
+    (1.0 + 2.0 ** -8 + 2.0 ** -30, 0x3F81),       # one rounding from float64 (through
+                                                  # binary32 it would round twice, to 0x3F80)
+    (float(_f32(0x3FFF8000)), 0x4000),            # 2 - 2^-8: tie, carries into the next binade
+    ((2.0 - 2.0 ** -7) * 2.0 ** 127, 0x7F7F),     # largest finite
+    ((2.0 - 2.0 ** -8) * 2.0 ** 127, 0x7F80),     # its tie with 2^128 rounds to infinity
+    (2.0 ** 200, 0x7F80),
+    (float("-inf"), 0xFF80),
+    (2.0 ** -133, 0x0001),                        # smallest subnormal
+    (2.0 ** -134, 0x0000),                        # half of it: tie, down to zero
+    (3 * 2.0 ** -134, 0x0002),                    # tie between 1 and 2 subnormal units
+    (2.0 ** -126, 0x0080),                        # smallest normal
+    (-0.0, 0x8000),
+    (0.0, 0x0000),
+]
+
+# binary16: 10 stored significand bits, so 1 + 2^-11 is the tie after 1.
+F16_CASES = [
+    (1.0 + 2.0 ** -11, 0x3C00),
+    (1.0 + 3 * 2.0 ** -11, 0x3C02),
+    (1.0 + 2.0 ** -11 + 2.0 ** -40, 0x3C01),     # above the tie by less than binary32 resolves
+    (65504.0, 0x7BFF),                           # largest finite
+    (65520.0, 0x7C00),                           # tie with 2^16: infinity
+    (2.0 ** -24, 0x0001),
+    (2.0 ** -25, 0x0000),
+    (3 * 2.0 ** -25, 0x0002),
+    (-2.5, 0xC100),
+]
+
+
+@pytest.mark.parametrize("dtype,cases", [(oracle.BF16, BF16_CASES), (oracle.F16, F16_CASES)])
+def test_to_bits_hand_worked_rounding(dtype, cases):
+    v = np.array([c[0] for c in cases], np.float64)
+    want = np.array([c[1] for c in cases], np.uint16)
+    got = ds.to_bits(v, dtype)
+    bad = [(c[0], hex(c[1]), hex(int(g))) for c, g in zip(cases, got) if int(g) != c[1]]
+    assert not bad, bad
+
+
+def test_to_bits_bf16_nan_stays_nan():
+    got = ds.to_bits(np.array([np.nan, -np.nan]), oracle.BF16)
+    assert np.all((got & 0x7F80) == 0x7F80) and np.all((got & 0x007F) != 0)
+
+
 @pytest.mark.parametrize("dtype", [oracle.F16, oracle.BF16])
-def test_to_bits_matches_library_rounding(dtype):
-    v = synth.normal((4096,), oracle.F32, 3, 1, 0, 3).astype(np.float64)
-    bits = ds.to_bits(v, dtype)
-    if dtype == oracle.F16:
-        ref = torch.from_numpy(v).to(torch.float16).view(torch.int16).numpy().view(np.uint16)
-    else:
-        ref = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
-    assert np.array_equal(bits, ref)
+def test_to_bits_on_binary32_values_matches_independent_encoder(dtype):
+    # binary32 inputs (normals over the whole range, subnormals, values near the types'
+    # limits) are rounded once by either route: the oracle's float64 path must give the
+    # bits of the generator's integer round-to-nearest-even from binary32
+    rng = np.random.default_rng(7)
+    bits = rng.integers(0, 2 ** 32, size=200000, dtype=np.uint64).astype(np.uint32)
+    bits = bits[(bits & 0x7F800000) != 0x7F800000]          # finite only
+    v = bits.view(np.float32)
+    extra = synth.normal((4096,), oracle.F32, 3, 1, 0, 3)
+    v = np.concatenate([v, extra]).astype(np.float32)
+    assert np.array_equal(ds.to_bits(v.astype(np.float64), dtype), synth.encode(v, dtype))
 
 
 def _layer(H, F, dtype, tid, zero=False):

@@ -160,3 +160,16 @@ def test_split_rows_reading():
         g, c = oracle.split_rows(1001, float(a))
         assert g + c == 1001 and c >= prev
         prev = c
+
+
+def test_linear_ptr_equals_array_form_with_row_stride():
+    # the raw-address form (pinned buffers in the benchmark's baseline) reads x with a row
+    # stride and writes the same bits as the array form
+    B, K, N, dt = 3, 72, 40, oracle.F16
+    xs = synth.normal((B, K + 8), dt, 4, 1)
+    W = synth.normal((N, K), dt, 4, 2, 0, 0.02)
+    b = synth.normal((N,), dt, 4, 3, 0, 0.02)
+    y = np.empty((B, N), np.float32)
+    oracle.linear_ptr(xs.ctypes.data, K + 8, B, K, W.ctypes.data, N, dt, b.ctypes.data, y)
+    ref = oracle.linear(np.ascontiguousarray(xs[:, :K]), W, b, dt)
+    assert np.array_equal(y.view(np.uint32), ref.view(np.uint32))
