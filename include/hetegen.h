@@ -121,6 +121,42 @@ HETEGEN_API hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, i
                               const void* bias_host, const void* bias_dev, double alpha, void* y_dev,
                               hetegen_dtype y_dtype, void* stream);
 
+/* ---- GPU rows of a resident weight in matrix-core tile order ----
+ * The GPU's share of a module (Sec. 3.1, Eq. 2; Sec. 4.2: the GPU computes its part
+ * of the output from weights in device memory), all rows resident.  The weight
+ * [N, K] is stored as 1 KiB tiles of 16 rows x 32 columns, row tile after row tile
+ * (the k-tiles of rows [16 t, 16 t + 16) are contiguous); within a tile the 16 bytes
+ * at offset 16 l hold W[16 t + l % 16][32 k + 8 (l / 16) + e], e < 8.  Rows past N
+ * and columns past K are zero.  One tile is the 16-row operand of one 16x16x32
+ * matrix-core product, so the GEMV reads every tile with one coalesced 1 KiB load
+ * and runs on the matrix cores at every batch size (decode steps of models created
+ * for batches of 5 or more keep their resident rows in this order). */
+
+/* Bytes of the tile-ordered copy of a [rows, K] weight (0 for rows < 1 or K not a
+ * positive multiple of 8). */
+HETEGEN_API size_t hetegen_tiled_bytes(int rows, int K);
+
+/* W_tiled_dev = tile order of W_dev [rows, K] (device, row-major, row stride K);
+ * both device pointers, 16-byte aligned, caller-owned; W_tiled_dev holds
+ * hetegen_tiled_bytes(rows, K) bytes and may not overlap W_dev.  Enqueued on
+ * `stream`.  K % 8 == 0. */
+HETEGEN_API hetegen_status hetegen_tile_weights(hetegen_ctx* ctx, const void* W_dev, int rows, int K,
+                                                void* W_tiled_dev, void* stream);
+
+/* y[b, j] = sum_k x[b, k] * W[j, k] + bias[j] for all N rows on the GPU, W given in
+ * tile order (hetegen_tile_weights).  x_dev [B, K] and y_dev [B, N] (row strides K
+ * and N) as in hetegen_linear; bias_dev optional device [N].  Binary32 sums (the
+ * matrix core's products of 16-bit values are exact); for K of 8192 and more the
+ * sum over K is split over up to 8 workgroups whose partial sums are added in a
+ * fixed order, so results do not depend on timing.  Uses the context's split-K
+ * workspace, which the first call with a larger need allocates (device memory,
+ * after waiting for the device); calls on one context must not overlap.  Enqueued
+ * on `stream`.  B in [1, 8], K % 8 == 0, N >= 1. */
+HETEGEN_API hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_dev, int B, int K,
+                                                const void* W_tiled_dev, int N, hetegen_dtype w_dtype,
+                                                const void* bias_dev, void* y_dev, hetegen_dtype y_dtype,
+                                                void* stream);
+
 /* ---- Alpha planner: computation distribution law (Sec. 3.2, Eq. 4-7; Eq. 8-9) ---- */
 
 typedef struct {
@@ -248,7 +284,13 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * hetegen_linear) and host biases of linear i (caller-owned, must outlive the
  * model).  alpha[i]: CPU fraction of linear i.
  * resident[i] != 0: rows [0, n_gpu) of linear i are copied to HBM at creation;
- * otherwise they are streamed every step.  max_batch in [1, 8]. */
+ * otherwise they are streamed every step.  max_batch in [1, 8]; H, F multiples
+ * of 8, H <= 16384 (UNSUPPORTED above: the LayerNorm keeps a row in registers; the
+ * largest OPT hidden size is 12288).  With max_batch
+ * >= 5 the resident rows are stored in matrix-core tile order and run on the
+ * matrix-core GEMV at every batch size (see hetegen_linear_tiled; the model then
+ * also owns its split-K workspace); below 5 they stay row-major and run on the
+ * vector GEMV, whose fused LayerNorm is faster at batches 1-4. */
 HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
                                     void* const* W_host, void* const* bias_host, const double* alpha,
                                     const int* resident, int max_batch, hetegen_model** out);
@@ -280,7 +322,7 @@ HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* 
 #define HETEGEN_EXEC_EAGER 3
 
 /* Select the execution mode (UNSUPPORTED when a forced mode cannot run this
- * model).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
+ * model; PERSISTENT needs row-major resident weights, i.e. max_batch < 5).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
  * persistent mode (0: the default, seconds of waiting); a wait that gives up lets
  * the step finish with undefined outputs and makes the next hetegen_decode_step
  * on the model fail with HETEGEN_ERR_HIP.  A small limit exists to test that path. */

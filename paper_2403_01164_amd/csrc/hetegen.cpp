@@ -61,6 +61,12 @@ constexpr int kBarrierGroups = 16;
 constexpr size_t kCounterBytes = 256;
 constexpr int kDefaultRing = 8;
 constexpr int kMaxBatch = 8;
+// Models created for batches of kTiledMinBatch or more keep their resident rows in the
+// matrix-core tile order and run them on the matrix-core GEMV at every batch size: from
+// batch 5 on the vector GEMV is bound by its dot products and LDS reads of x (OPT-6.7B
+// shapes at batch 8: 24-41 us per linear against 8-24 us on the matrix cores), while at
+// batch 1-4 the vector kernels with their fused LayerNorm are as fast or faster.
+constexpr int kTiledMinBatch = 5;
 constexpr int kDefaultPinThreads = 4;
 constexpr int kDefaultPinRing = 4;
 
@@ -199,6 +205,11 @@ struct hetegen_ctx {
   std::vector<hipEvent_t> ev_pool;
   hetegen_profile prof{};
   std::string err;
+  // split-K workspace of hetegen_linear_tiled (grown on demand; counters zero between launches)
+  float* ws = nullptr;
+  size_t ws_floats = 0;
+  uint32_t* ws_cnt = nullptr;
+  size_t ws_words = 0;
 };
 
 struct hetegen_model {
@@ -214,6 +225,9 @@ struct hetegen_model {
     void* bias_dev = nullptr;  // all N biases
   };
   int L = 0, H = 0, F = 0, dtype = 0, max_batch = 1;
+  bool tiled = false;          // resident rows in matrix-core tile order (max_batch >= kTiledMinBatch)
+  float* ws = nullptr;         // split-K partials of the matrix-core GEMV
+  uint32_t* ws_cnt = nullptr;  // its arrival counters, zero between launches
   std::vector<Lin> lin;
   std::vector<double> lin_ms;  // host time of each linear in the last eager step
   void* arena = nullptr;  // device memory for resident weights and biases
@@ -638,10 +652,13 @@ struct Job {
   void* ln_buf;     // device [B, K] for the normalised input when it must be materialised
   void* trace_in;   // optional copy of the linear's input [B, K]
   void* trace_out;  // optional copy of the output [B, N]
+  bool tiled;       // W_dev is in matrix-core tile order (matrix-core GEMV)
+  float* ws;        // its split-K workspace
+  uint32_t* cnt;
 };
 
 hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long ldx, int ln, const void* W, int row0,
-                        int rows, hipStream_t st, void* h_out) {
+                        int rows, hipStream_t st, void* h_out, bool tiled = false) {
   hg::GemvParams p{};
   const size_t ys = j.y_f32 ? 4 : 2;
   p.x = x;
@@ -660,7 +677,13 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
   p.y_f32 = j.y_f32;
   p.ln = ln;
   TimedScope ts(ctx, st, 1, (double)rows * j.K * 2);
-  HIPCHK(ctx, hg::launch_gemv(p, j.dtype, j.B, st, 0));
+  if (tiled) {
+    p.ws = j.ws;
+    p.cnt = j.cnt;
+    HIPCHK(ctx, hg::launch_gemv_mfma(p, j.dtype, j.B, st));
+  } else {
+    HIPCHK(ctx, hg::launch_gemv(p, j.dtype, j.B, st, 0));
+  }
   ts.end();
   return HETEGEN_OK;
 }
@@ -668,7 +691,7 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
 hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   const auto tl = Clock::now();
   const size_t s = 2;
-  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr && hg::gemv_fuses_ln(j.B);
+  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr && !j.tiled && hg::gemv_fuses_ln(j.B);
   const void* xin = j.x;
   long long ldin = j.ldx;
   // 1. input: materialise LayerNorm(x) unless it is fused into one resident GEMV,
@@ -723,7 +746,8 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
     return HETEGEN_OK;
   };
   if (j.n_gpu > 0 && j.W_dev)
-    TRY(run_gemv(ctx, j, xin, ldin, fused_ln ? 1 : 0, j.W_dev, 0, j.n_gpu, st, fused_ln ? j.trace_in : nullptr));
+    TRY(run_gemv(ctx, j, xin, ldin, fused_ln ? 1 : 0, j.W_dev, 0, j.n_gpu, st, fused_ln ? j.trace_in : nullptr,
+                 j.tiled));
   while (streamed && r0 < j.n_gpu) {
     bool did = false;
     TRY(next_chunk(j.n_cpu == 0, &did));
@@ -890,6 +914,8 @@ hetegen_status hetegen_destroy(hetegen_ctx* ctx) {
     if (ctx->ev_y) (void)hipEventDestroy(ctx->ev_y);
     if (ctx->x_host) (void)hipHostFree(ctx->x_host);
     if (ctx->y_host) (void)hipHostFree(ctx->y_host);
+    if (ctx->ws) (void)hipFree(ctx->ws);
+    if (ctx->ws_cnt) (void)hipFree(ctx->ws_cnt);
     if (ctx->copy_stream) (void)hipStreamDestroy(ctx->copy_stream);
     if (ctx->capture_stream) (void)hipStreamDestroy(ctx->capture_stream);
     (void)hipGetLastError();
@@ -978,6 +1004,84 @@ hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K,
       reset_pipeline(ctx);
       return stt;
     }
+    return finish_call(ctx, t0);
+  });
+}
+
+// ---- resident weights in matrix-core tile order ----
+size_t hetegen_tiled_bytes(int rows, int K) {
+  if (rows < 1 || K < 8 || K % 8) return 0;
+  return hg::tiled_bytes(rows, K);
+}
+
+hetegen_status hetegen_tile_weights(hetegen_ctx* ctx, const void* W_dev, int rows, int K, void* W_tiled_dev,
+                                    void* stream) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!W_dev || !W_tiled_dev || rows < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_tile_weights: bad arguments");
+    if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+    if (!aligned16(W_dev) || !aligned16(W_tiled_dev))
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "W and its tiled copy must be 16-byte aligned");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    HIPCHK(ctx, hg::launch_tile(W_dev, K, rows, K, W_tiled_dev, (hipStream_t)stream));
+    return HETEGEN_OK;
+  });
+}
+
+hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_dev, int B, int K, const void* W_tiled_dev, int N,
+                                    hetegen_dtype w_dtype, const void* bias_dev, void* y_dev, hetegen_dtype y_dtype,
+                                    void* stream) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    auto t0 = Clock::now();
+    ctx->err.clear();
+    if (!x_dev || !W_tiled_dev || !y_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "x_dev, W_tiled_dev and y_dev are required");
+    if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
+    if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
+    if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+    if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
+    if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "y dtype must be the weight dtype or fp32");
+    if (!aligned16(x_dev) || !aligned16(W_tiled_dev))
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x and the tiled weight must be 16-byte aligned");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    hipStream_t st = (hipStream_t)stream;
+    // split-K workspace, sized for the largest batch so that batch changes do not regrow it
+    const size_t need = hg::mfma_ws_floats(N, K, kMaxBatch), words = hg::mfma_cnt_words(N, K);
+    if (need > ctx->ws_floats || words > ctx->ws_words) {
+      HIPCHK(ctx, hipDeviceSynchronize());  // earlier launches may still use the old buffers
+      if (ctx->ws) (void)hipFree(ctx->ws);
+      if (ctx->ws_cnt) (void)hipFree(ctx->ws_cnt);
+      ctx->ws = nullptr;
+      ctx->ws_cnt = nullptr;
+      ctx->ws_floats = ctx->ws_words = 0;
+      const size_t nf = std::max(need, (size_t)1), nw = std::max(words, (size_t)1);
+      if (hipMalloc((void**)&ctx->ws, nf * 4) != hipSuccess || hipMalloc((void**)&ctx->ws_cnt, nw * 4) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ctx, HETEGEN_ERR_OOM, "split-K workspace of %zu floats", nf);
+      }
+      HIPCHK(ctx, hipMemset(ctx->ws_cnt, 0, nw * 4));
+      ctx->ws_floats = nf;
+      ctx->ws_words = nw;
+    }
+    hg::GemvParams p{};
+    p.x = x_dev;
+    p.ldx = K;
+    p.W = W_tiled_dev;
+    p.bias = bias_dev;
+    p.y = y_dev;
+    p.ldy = N;
+    p.rows = N;
+    p.K = K;
+    p.epi = hg::EPI_NONE;
+    p.y_f32 = y_dtype == HETEGEN_F32;
+    p.ws = ctx->ws;
+    p.cnt = ctx->ws_cnt;
+    TimedScope ts(ctx, st, 1, (double)N * K * 2);
+    HIPCHK(ctx, hg::launch_gemv_mfma(p, w_dtype, B, st));
+    ts.end();
     return finish_call(ctx, t0);
   });
 }
@@ -1517,6 +1621,8 @@ void model_free(hetegen_model* m) {
   if (m->kv_part) (void)hipFree(m->kv_part);
   if (m->kv_cnt) (void)hipFree(m->kv_cnt);
   if (m->abuf) (void)hipFree(m->abuf);
+  if (m->ws) (void)hipFree(m->ws);
+  if (m->ws_cnt) (void)hipFree(m->ws_cnt);
   (void)hipGetLastError();
   delete m;
 }
@@ -1583,6 +1689,9 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
       j.bias_dev = lin.bias_dev;
       j.n_gpu = lin.n_gpu;
       j.n_cpu = lin.n_cpu;
+      j.tiled = m->tiled && lin.W_dev;
+      j.ws = m->ws;
+      j.cnt = m->ws_cnt;
       j.ln_buf = m->lnbuf;
       j.y_f32 = 0;
       switch (which) {
@@ -1627,7 +1736,7 @@ hetegen_status build_plan(hetegen_ctx* ctx, hetegen_model* m, int B) {
   auto& pl = m->plan[B];
   pl.built = true;
   pl.ok = false;
-  if (!m->graphable) return HETEGEN_OK;
+  if (!m->graphable || m->tiled) return HETEGEN_OK;  // the persistent step reads row-major weights
   int ncu = 0, coop = 0;
   HIPCHK(ctx, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device));
   HIPCHK(ctx, hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, ctx->device));
@@ -1735,6 +1844,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_create: bad arguments");
     if (dtype != HETEGEN_F16 && dtype != HETEGEN_BF16)
       return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "model dtype: fp16 or bf16");
+    if (H > hg::kMaxLnK) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "hidden size %d above %d", H, hg::kMaxLnK);
     *out = nullptr;
     HIPCHK(ctx, hipSetDevice(ctx->device));
     hetegen_model* m = new hetegen_model();
@@ -1743,6 +1853,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     m->F = F;
     m->dtype = dtype;
     m->max_batch = max_batch;
+    m->tiled = max_batch >= kTiledMinBatch;
     m->lin.resize((size_t)4 * L);
     m->lin_ms.assign((size_t)4 * L, 0.0);
     size_t dev_bytes = 0;
@@ -1770,7 +1881,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       }
       l.n_cpu = split_cpu_rows(l.N, l.alpha);
       l.n_gpu = l.N - l.n_cpu;
-      if (l.resident) dev_bytes += align256((size_t)l.n_gpu * l.K * 2);
+      if (l.resident) dev_bytes += align256(m->tiled ? hg::tiled_bytes(l.n_gpu, l.K) : (size_t)l.n_gpu * l.K * 2);
       if (l.bias_host) dev_bytes += align256((size_t)l.N * 2);
     }
     if (dev_bytes && hipMalloc(&m->arena, dev_bytes) != hipSuccess) {
@@ -1778,25 +1889,62 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       model_free(m);
       return fail(ctx, HETEGEN_ERR_OOM, "%zu bytes of HBM for resident weights", dev_bytes);
     }
+    // tile order: each resident block goes through a device staging buffer and is
+    // reordered into the arena; the split-K workspace is sized for the largest need
+    void* stage = nullptr;
+    size_t ws_floats = 0, ws_words = 0;
+    if (m->tiled) {
+      size_t most = 0;
+      for (const auto& l : m->lin)
+        if (l.resident) {
+          most = std::max(most, (size_t)l.n_gpu * l.K * 2);
+          ws_floats = std::max(ws_floats, hg::mfma_ws_floats(l.n_gpu, l.K, max_batch));
+          ws_words = std::max(ws_words, hg::mfma_cnt_words(l.n_gpu, l.K));
+        }
+      if ((most && hipMalloc(&stage, most) != hipSuccess) ||
+          (ws_floats && hipMalloc((void**)&m->ws, ws_floats * 4) != hipSuccess) ||
+          (ws_words && hipMalloc((void**)&m->ws_cnt, ws_words * 4) != hipSuccess)) {
+        (void)hipGetLastError();
+        if (stage) (void)hipFree(stage);
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_OOM, "tile staging buffer or split-K workspace");
+      }
+      if (ws_words && hipMemset(m->ws_cnt, 0, ws_words * 4) != hipSuccess) {
+        (void)hipFree(stage);
+        model_free(m);
+        return fail(ctx, HETEGEN_ERR_HIP, "split-K counter initialisation failed");
+      }
+    }
     char* p = (char*)m->arena;
     for (auto& l : m->lin) {
       if (l.resident) {
         l.W_dev = p;
-        if (l.n_gpu > 0 && hipMemcpy(p, l.W_host, (size_t)l.n_gpu * l.K * 2, hipMemcpyHostToDevice) != hipSuccess) {
+        const size_t rb = (size_t)l.n_gpu * l.K * 2;
+        bool ok = true;
+        if (l.n_gpu > 0 && !m->tiled) ok = hipMemcpy(p, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess;
+        if (l.n_gpu > 0 && m->tiled)
+          ok = hipMemcpy(stage, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess &&
+               hg::launch_tile(stage, l.K, l.n_gpu, l.K, p, nullptr) == hipSuccess &&
+               hipDeviceSynchronize() == hipSuccess;
+        if (!ok) {
+          (void)hipGetLastError();
+          if (stage) (void)hipFree(stage);
           model_free(m);
           return fail(ctx, HETEGEN_ERR_HIP, "resident upload failed");
         }
-        p += align256((size_t)l.n_gpu * l.K * 2);
+        p += align256(m->tiled ? hg::tiled_bytes(l.n_gpu, l.K) : rb);
       }
       if (l.bias_host) {
         l.bias_dev = p;
         if (hipMemcpy(p, l.bias_host, (size_t)l.N * 2, hipMemcpyHostToDevice) != hipSuccess) {
+          if (stage) (void)hipFree(stage);
           model_free(m);
           return fail(ctx, HETEGEN_ERR_HIP, "bias upload failed");
         }
         p += align256((size_t)l.N * 2);
       }
     }
+    if (stage) (void)hipFree(stage);
     const size_t B = max_batch;
     const size_t xb = align256(B * H * 2), qb = align256(B * 3 * H * 2), fb = align256(B * F * 2),
                  lb = align256(B * std::max(H, F) * 2);
@@ -1848,6 +1996,7 @@ hetegen_status hetegen_model_set_exec(hetegen_model* m, int mode, uint32_t barri
     if (!m || mode < HETEGEN_EXEC_AUTO || mode > HETEGEN_EXEC_EAGER) return HETEGEN_ERR_INVALID_ARG;
     if ((mode == HETEGEN_EXEC_PERSISTENT || mode == HETEGEN_EXEC_GRAPH) && !m->graphable)
       return HETEGEN_ERR_UNSUPPORTED;
+    if (mode == HETEGEN_EXEC_PERSISTENT && m->tiled) return HETEGEN_ERR_UNSUPPORTED;
     m->exec_mode = mode;
     m->spin_limit = barrier_spin_limit;
     return HETEGEN_OK;

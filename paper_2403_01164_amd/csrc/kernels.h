@@ -27,6 +27,9 @@ struct GemvParams {
   int ln;
   int ktile;           // set by the launcher: K elements staged in LDS per pass (tiled kernel)
   int rpw;             // set by the launcher: rows per workgroup (contiguous block)
+  // matrix-core GEMV on tile-ordered weights (launch_gemv_mfma) only:
+  float* ws;           // split-K partials: mfma_ws_floats(rows, K, B) floats
+  uint32_t* cnt;       // split-K arrival counters: mfma_cnt_words(rows, K) words, zero between launches
 };
 
 // One linear of the persistent decode step (a device-resident table entry).
@@ -83,8 +86,11 @@ hipError_t launch_step(const StepArgs& a, int dtype, int B, int grid, size_t lds
 // (0 = default).  Returns the launch status.
 hipError_t launch_gemv(GemvParams p, int dtype, int B, hipStream_t stream, int grid_cap);
 
+// Largest LayerNorm width (hidden size) the kernels support.
+constexpr int kMaxLnK = 16384;
+
 // h[b, :] = act(LayerNorm(x[b, :])) for b < B (device), and optionally
-// h_host_f32[b * K + k] = float(h[b, k]) (pinned host memory).
+// h_host_f32[b * K + k] = float(h[b, k]) (pinned host memory).  K <= kMaxLnK.
 hipError_t launch_layernorm(const void* x, long long ldx, int B, int K, int dtype, void* h, long long ldh,
                             float* h_host_f32, hipStream_t stream);
 
@@ -96,5 +102,26 @@ hipError_t launch_export_f32(const void* x, long long ldx, int B, int K, int dty
 // (bias included) read from pinned host memory, finished like the GPU rows.
 hipError_t launch_import_rows(const float* src_host_f32, int B, int n, int dtype, int epi, void* y,
                               long long ldy, int y_f32, const void* resid, long long ldr, hipStream_t stream);
+
+// ---- matrix-core GEMV on tile-ordered weights ----
+// A weight block [rows, K] in tile order is a sequence of 1 KiB tiles of 16 rows x 32
+// columns, row tile by row tile (all k-tiles of rows [16 rt, 16 rt + 16) are contiguous);
+// within a tile, the 16 bytes at 16 * l hold W[16 rt + l % 16][32 kt + 8 (l / 16) + e],
+// e < 8: the operand layout of one 16x16x32 matrix-core instruction, so one load per
+// lane reads the whole tile.  Rows past `rows` and columns past K are zero.
+size_t tiled_bytes(int rows, int K);
+
+// dst = tile order of W [rows, K] (row stride ldw elements, 16-byte aligned rows).
+hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream);
+
+// K-splits of the matrix-core GEMV for reduction length K (1 = no split), and the
+// workspace a launch of `rows` rows at batch B needs (0 when not split).
+int mfma_splits(int K);
+size_t mfma_ws_floats(int rows, int K, int B);
+size_t mfma_cnt_words(int rows, int K);
+
+// y = epi(x W^T + bias) with W in tile order (p.W), every row on the GPU; p.ln must be 0.
+// Split launches need p.ws and p.cnt.
+hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream);
 
 }  // namespace hg

@@ -650,6 +650,158 @@ __global__ __launch_bounds__(kThreads) void gemv_ln1_kernel(GemvParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Matrix-core GEMV on tile-ordered weights (batches 1..8).  A linear is a product of
+// B <= 8 activation rows with N weight rows; v_mfma_f32_16x16x32 takes one 1 KiB tile
+// of 16 weight rows x 32 columns as its 16-row operand (one 16-byte load per lane,
+// the whole tile in one coalesced instruction) and the matching 32 columns of x as its
+// 16-column operand (batch row b in lanes b, b + 16, b + 32, b + 48; the columns past
+// B repeat row B - 1 and their results are dropped).  The products and their fp32 sums
+// happen in the matrix core, so no lane reduction is needed and the instruction cost
+// per weight byte does not grow with B: the kernel stays bound by HBM at every batch
+// size, where the vector GEMV becomes bound by its dot products and LDS reads of x.
+//
+// Workgroup (row tile rt, split g) of 4 wavefronts takes k-tiles of split g of the
+// 16 rows; wavefront w a contiguous quarter of them, U tiles per step with the next
+// step's loads in flight.  The four 16x16 partial tiles are summed in LDS in wavefront
+// order.  With G > 1 splits, each workgroup stores its partial (coherent stores to
+// memory: the splits run on different XCDs with their own L2) and the last of the G to
+// arrive (an arrival counter, no waiting) adds the G partials in split order, so the
+// result does not depend on timing.  Column order inside a tile is free (both
+// operands use the same one), so every lane's x fragment is 16 contiguous bytes.
+// ---------------------------------------------------------------------------
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <class T> struct Mma;
+template <> struct Mma<F16> {
+  static __device__ __forceinline__ f32x4 run(const uint4& w, const uint4& x, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w), __builtin_bit_cast(f16x8, x), c, 0, 0,
+                                                  0);
+  }
+};
+template <> struct Mma<BF16> {
+  static __device__ __forceinline__ f32x4 run(const uint4& w, const uint4& x, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), __builtin_bit_cast(bf16x8, x), c, 0,
+                                                   0, 0);
+  }
+};
+
+constexpr int kTileRows = 16, kTileK = 32;
+
+template <class T, int B, int U>
+__global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G) {
+  __shared__ float part[kWaves][4][64];
+  __shared__ int last;
+  // the wavefront index through a scalar register: every tile bound below is then
+  // wave-uniform and the skipped products are skipped by a branch.  A condition the
+  // compiler cannot prove uniform becomes an execution mask, which matrix-core
+  // instructions do not obey (they would run for every skipped tile).
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int K = p.K, KT = (K + kTileK - 1) / kTileK;
+  const int rt = blockIdx.x / G, gi = blockIdx.x - rt * G;
+  const int kg = (KT + G - 1) / G;
+  const int kb = min(KT, gi * kg), ke = min(KT, kb + kg);
+  const int pw = (ke - kb + kWaves - 1) / kWaves;
+  const int k0 = min(ke, kb + wave * pw), k1 = min(ke, k0 + pw);
+  const int nst = (k1 - k0 + U - 1) / U;
+  const uint4* wp = (const uint4*)p.W + (size_t)rt * KT * 64 + lane;
+  const int b = min(lane & 15, B - 1), grp = lane >> 4;
+  const uint16_t* xr = (const uint16_t*)p.x + (long long)b * p.ldx;
+  struct Buf {
+    uint4 w[U], x[U];
+  };
+  auto load = [&](int st, Buf& f) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kt = min(k0 + st * U + u, k1 - 1);
+      f.w[u] = load_stream(wp + (size_t)kt * 64);
+      const int kx = kt * kTileK + 8 * grp;  // K % 8 == 0: a group is wholly inside or past K
+      f.x[u] = load_g16((const uint4*)(xr + min(kx, K - 8)));
+      // columns past K, and (as a second guard) the repeated tile of a step past k1,
+      // multiply zeros
+      if (kx >= K || k0 + st * U + u >= k1) f.x[u] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int st, const Buf& f) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (k0 + st * U + u < k1) acc = Mma<T>::run(f.w[u], f.x[u], acc);
+  };
+  Buf fa, fb;
+  if (nst > 0) load(0, fa);
+  int st = 0;
+  for (; st + 2 < nst; st += 2) {
+    load(st + 1, fb);
+    compute(st, fa);
+    load(st + 2, fa);
+    compute(st + 1, fb);
+  }
+  if (st + 1 < nst) {
+    load(st + 1, fb);
+    compute(st, fa);
+    compute(st + 1, fb);
+  } else if (st < nst) {
+    compute(st, fa);
+  }
+  // lane l of the result holds rows 4 (l / 16) + v, v < 4, of column l % 16
+#pragma unroll
+  for (int v = 0; v < 4; ++v) part[wave][v][lane] = acc[v];
+  __syncthreads();
+  const int t = threadIdx.x, i = t & 15, j = t >> 4;  // row i of the tile, batch row j
+  const bool mine = t < 16 * B;
+  const int l = j + 16 * (i >> 2), v = i & 3;
+  float s = 0.f;
+  if (mine) s = (part[0][v][l] + part[1][v][l]) + (part[2][v][l] + part[3][v][l]);
+  if (G > 1) {
+    const uint32_t pbytes = (uint32_t)(G * 16 * B * sizeof(float));
+    const auto rs = rsrc(p.ws + (size_t)rt * G * 16 * B, pbytes);
+    if (mine)
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, s), rs, (gi * 16 * B + t) * 4, 0,
+                                            kCoherent);
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's partial store has completed
+    __syncthreads();
+    if (t == 0) {
+      const uint32_t prev = __hip_atomic_fetch_add(p.cnt + rt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last = prev == (uint32_t)(G - 1);
+      if (last) __hip_atomic_store(p.cnt + rt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
+    }
+    __syncthreads();
+    if (!last) return;
+    if (mine) {
+      s = 0.f;
+      for (int q = 0; q < G; ++q)
+        s += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (q * 16 * B + t) * 4, 0, kCoherent));
+    }
+  }
+  const int row = rt * kTileRows + i;
+  if (!mine || row >= p.rows) return;
+  const uint16_t* bias = (const uint16_t*)p.bias;
+  float y = s + (bias ? T::to_f32(bias[row]) : 0.f);
+  const float rv = p.epi == EPI_RESID ? T::to_f32(((const uint16_t*)p.resid)[j * p.ldr + row]) : 0.f;
+  store_y<T>(p.y, j * p.ldy + row, p.y_f32, apply_epi(y, p.epi, rv));
+}
+
+// Tile order of W [rows, K]: one 16-byte group per thread (see tiled_bytes in kernels.h).
+__global__ __launch_bounds__(kThreads) void tile_kernel(const uint16_t* __restrict__ W, long long ldw, int rows,
+                                                        int K, uint4* __restrict__ dst, long long groups) {
+  const int KT = (K + kTileK - 1) / kTileK;
+  for (long long q = (long long)blockIdx.x * kThreads + threadIdx.x; q < groups;
+       q += (long long)gridDim.x * kThreads) {
+    const int l = (int)(q & 63);
+    const long long tile = q >> 6;
+    const int kt = (int)(tile % KT);
+    const long long rt = tile / KT;
+    const long long row = rt * kTileRows + (l & 15);
+    const int k = kt * kTileK + 8 * (l >> 4);
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (row < rows && k < K) v = *(const uint4*)(W + row * ldw + k);
+    dst[q] = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Persistent decode step: one cooperative launch runs every linear of the step,
 // each workgroup taking the same row block of every linear, with a grid barrier
 // between dependent linears.  A workgroup requests the weights of its first
@@ -726,11 +878,11 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
 
 // ---------------------------------------------------------------------------
 // K-tiled GEMV for x that does not fit in LDS: x is restaged per K tile and row
-// group (grid-stride over row groups).
+// group (grid-stride over row groups).  No fused LayerNorm: a LayerNorm input fits in
+// LDS at the batches that fuse it (B <= 4, hidden size <= kMaxLnK).
 // ---------------------------------------------------------------------------
-template <class T, int B>
-__device__ __forceinline__ void stage_x_tile(const GemvParams& p, uint4* xs, int k0, int kn, const float* mean,
-                                             const float* rstd, bool write_h) {
+template <int B>
+__device__ __forceinline__ void stage_x_tile(const GemvParams& p, uint4* xs, int k0, int kn) {
   const uint16_t* x = (const uint16_t*)p.x;
   const int n8 = kn >> 3, kt8 = p.ktile >> 3;
   for (int c = threadIdx.x; c < n8; c += kThreads) {
@@ -738,35 +890,19 @@ __device__ __forceinline__ void stage_x_tile(const GemvParams& p, uint4* xs, int
 #pragma unroll
     for (int b = 0; b < B; ++b) v[b] = *(const uint4*)(x + b * p.ldx + k0 + (long long)c * 8);
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      if (p.ln) {
-        v[b] = normalize8<T>(v[b], mean[b], rstd[b]);
-        if (write_h) *(uint4*)((uint16_t*)p.h_out + b * p.ldh + k0 + (long long)c * 8) = v[b];
-      }
-      xs[b * kt8 + c] = v[b];
-    }
+    for (int b = 0; b < B; ++b) xs[b * kt8 + c] = v[b];
   }
 }
 
 template <class T, int B, int R, int U>
 __global__ __launch_bounds__(kThreads) void gemv_tiled_kernel(GemvParams p) {
   extern __shared__ uint4 xs[];
-  __shared__ float red[2][8][kWaves];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int K = p.K, ktile = p.ktile, kt8 = ktile >> 3;
   const int ntiles = (K + ktile - 1) / ktile;
-  float mean[B], rstd[B];
-#pragma unroll
-  for (int b = 0; b < B; ++b) { mean[b] = 0.f; rstd[b] = 1.f; }
-  const uint16_t* x = (const uint16_t*)p.x;
-  if (p.ln)
-    ln_stats<T, B>([&](int b, int c) { return *(const uint4*)(x + b * p.ldx + (long long)c * 8); }, K, mean, rstd,
-                   red);
-  const bool wg_writes_h = p.ln && p.h_out != nullptr && blockIdx.x == 0;
   const int nrg = (p.rows + R - 1) / R;
   const uint16_t* W = (const uint16_t*)p.W;
   const uint16_t* bias = (const uint16_t*)p.bias;
-  bool first = true;
   for (int rg0 = blockIdx.x * kWaves; rg0 < nrg; rg0 += gridDim.x * kWaves) {
     const int rg = rg0 + wave;
     const bool valid = rg < nrg;  // uniform per wavefront
@@ -782,7 +918,7 @@ __global__ __launch_bounds__(kThreads) void gemv_tiled_kernel(GemvParams p) {
     for (int t = 0; t < ntiles; ++t) {
       const int k0 = t * ktile, kn = min(ktile, K - k0);
       __syncthreads();
-      stage_x_tile<T, B>(p, xs, k0, kn, mean, rstd, wg_writes_h && first);
+      stage_x_tile<B>(p, xs, k0, kn);
       __syncthreads();
       if (valid) {
         const int n8 = kn >> 3, c0 = k0 >> 3;
@@ -830,38 +966,13 @@ __global__ __launch_bounds__(kThreads) void gemv_tiled_kernel(GemvParams p) {
         }
       }
     }
-    first = false;
   }
 }
 
-// One batch row per blockIdx.y: the statistics of a row are the same bits whatever
-// the batch (ln_stats treats rows independently), and the B rows run in parallel.
-template <class T>
-__global__ __launch_bounds__(kThreads) void layernorm_kernel(const uint16_t* __restrict__ x, long long ldx, int K,
-                                                             uint16_t* __restrict__ h, long long ldh,
-                                                             float* __restrict__ h_host) {
-  __shared__ float red[2][8][kWaves];
-  const int b = blockIdx.y;
-  const uint16_t* xr = x + b * ldx;
-  float mean, rstd;
-  ln_stats<T, 1>([&](int, int c) { return *(const uint4*)(xr + (long long)c * 8); }, K, &mean, &rstd, red);
-  const int n8 = K >> 3;
-  for (int c = blockIdx.x * kThreads + threadIdx.x; c < n8; c += gridDim.x * kThreads) {
-    uint4 v = normalize8<T>(*(const uint4*)(xr + (long long)c * 8), mean, rstd);
-    *(uint4*)(h + b * ldh + (long long)c * 8) = v;
-    if (h_host) {
-      float f[8];
-      unpack8<T>(v, f);
-      float4* dst = (float4*)(h_host + (long long)b * K + (long long)c * 8);
-      dst[0] = make_float4(f[0], f[1], f[2], f[3]);
-      dst[1] = make_float4(f[4], f[5], f[6], f[7]);
-    }
-  }
-}
-
-// The same LayerNorm with the row held in registers (thread t keeps chunks t + 256 i, the
-// chunks ln_stats gives it, for i < NI): the row is read from memory once instead of once
-// per pass, and every sum is formed in ln_stats' order, so the bits are the same.
+// LayerNorm of a materialised input, one batch row per blockIdx.y (the statistics of a
+// row are the same bits whatever the batch), the row held in registers (thread t keeps
+// chunks t + 256 i, the chunks ln_stats gives it, for i < NI): every sum is formed in
+// ln_stats' order, so the bits are those of the GEMVs that fuse the LayerNorm.
 template <class T, int NI>
 __global__ __launch_bounds__(kThreads) void layernorm_regs_kernel(const uint16_t* __restrict__ x, long long ldx,
                                                                   int K, uint16_t* __restrict__ h, long long ldh,
@@ -1057,6 +1168,7 @@ hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
     hipLaunchKernelGGL((gemv_kernel<T, B, R, U>), dim3(grid), dim3(kThreads), lds, s, p);
     return hipGetLastError();
   }
+  if (p.ln) return hipErrorInvalidValue;  // not reached: see gemv_tiled_kernel
   int kt = kTiledLdsBudget / (2 * B);
   kt -= kt % 512;
   p.ktile = kt;
@@ -1093,7 +1205,7 @@ template <class T>
 hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long long ldh, float* hh, hipStream_t s) {
   if (B < 1 || B > 8) return hipErrorInvalidValue;
   const int n8 = K >> 3;
-  // rows of up to 8 * kThreads * 8 elements (hidden sizes up to 16384) stay in registers
+  // rows of up to 8 * kThreads * 8 elements (hidden sizes up to kMaxLnK) stay in registers
   const int ni = (n8 + kThreads - 1) / kThreads;
   const uint16_t* xx = (const uint16_t*)x;
   uint16_t* hp = (uint16_t*)h;
@@ -1106,14 +1218,8 @@ hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long
     case 6:
     case 7:
     case 8: return launch_ln_regs<T, 8>(B, xx, ldx, K, hp, ldh, hh, s);
-    default: break;
+    default: return hipErrorInvalidValue;  // K > kMaxLnK
   }
-  int grid = (n8 + kThreads * 4 - 1) / (kThreads * 4);
-  if (grid < 1) grid = 1;
-  if (grid > 16) grid = 16;
-  hipLaunchKernelGGL((layernorm_kernel<T>), dim3(grid, B), dim3(kThreads), 0, s, (const uint16_t*)x, ldx, K,
-                     (uint16_t*)h, ldh, hh);
-  return hipGetLastError();
 }
 
 template <class T>
@@ -1206,6 +1312,74 @@ hipError_t launch_import_rows(const float* src, int B, int n, int dtype, int epi
     hipLaunchKernelGGL(import_kernel<F16>, dim3(grid), dim3(kThreads), 0, stream, src, B, n, epi, y, ldy, y_f32,
                        resid, ldr);
   return hipGetLastError();
+}
+
+size_t tiled_bytes(int rows, int K) {
+  if (rows <= 0 || K <= 0) return 0;
+  return (size_t)((rows + kTileRows - 1) / kTileRows) * (size_t)((K + kTileK - 1) / kTileK) * 1024;
+}
+
+hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream) {
+  const long long groups = (long long)(tiled_bytes(rows, K) / 16);
+  if (groups == 0) return hipSuccess;
+  long long g = (groups + kThreads - 1) / kThreads;
+  if (g > 4096) g = 4096;
+  hipLaunchKernelGGL(tile_kernel, dim3((unsigned)g), dim3(kThreads), 0, stream, (const uint16_t*)W, ldw, rows, K,
+                     (uint4*)dst, groups);
+  return hipGetLastError();
+}
+
+// Split K when one workgroup would walk more than 256 k-tiles (256 KiB of a row tile):
+// the short-N linears with long K (fc2) otherwise leave too few workgroups per CU
+// (OPT-6.7B fc2 [4096, 16384]: 256 workgroups; with 4 splits 25.0 -> 23.1 us at B = 1).
+// Splitting shorter K costs more in the merge than it gains.
+int mfma_splits(int K) {
+  const int KT = (K + kTileK - 1) / kTileK;
+  int g = 1;
+  while (g < 8 && KT / (2 * g) >= 128) g *= 2;
+  return g;
+}
+
+size_t mfma_ws_floats(int rows, int K, int B) {
+  const int G = mfma_splits(K);
+  if (G == 1 || rows <= 0) return 0;
+  return (size_t)((rows + kTileRows - 1) / kTileRows) * G * kTileRows * B;
+}
+
+size_t mfma_cnt_words(int rows, int K) {
+  if (mfma_splits(K) == 1 || rows <= 0) return 0;
+  return (size_t)((rows + kTileRows - 1) / kTileRows);
+}
+
+template <class T, int B>
+hipError_t launch_mfma_b(const GemvParams& p, hipStream_t s) {
+  const int G = mfma_splits(p.K);
+  const int grid = ((p.rows + kTileRows - 1) / kTileRows) * G;
+  if (G == 1) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 8>), dim3(grid), dim3(kThreads), 0, s, p, 1);
+  else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4>), dim3(grid), dim3(kThreads), 0, s, p, G);
+  return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_mfma_t(const GemvParams& p, int B, hipStream_t s) {
+  switch (B) {
+    case 1: return launch_mfma_b<T, 1>(p, s);
+    case 2: return launch_mfma_b<T, 2>(p, s);
+    case 3: return launch_mfma_b<T, 3>(p, s);
+    case 4: return launch_mfma_b<T, 4>(p, s);
+    case 5: return launch_mfma_b<T, 5>(p, s);
+    case 6: return launch_mfma_b<T, 6>(p, s);
+    case 7: return launch_mfma_b<T, 7>(p, s);
+    case 8: return launch_mfma_b<T, 8>(p, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream) {
+  if (p.rows <= 0) return hipSuccess;
+  if (p.ln || p.K < 8 || p.K % 8) return hipErrorInvalidValue;
+  if (mfma_splits(p.K) > 1 && (!p.ws || !p.cnt)) return hipErrorInvalidValue;
+  return dtype == 1 ? launch_mfma_t<BF16>(p, B, stream) : launch_mfma_t<F16>(p, B, stream);
 }
 
 }  // namespace hg

@@ -15,125 +15,12 @@ import synth
 from oracle import attention as oat
 from oracle import decode_step as ods
 from common import TOL, U_ACT, Pinned, np_from_dev, rel_err, torch_dev_from_np
+from gpu_model import NAMES, Model, shapes
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 hg = pytest.importorskip("paper_2403_01164_amd")
-
-NAMES = ("qkv", "out", "fc1", "fc2")
-
-
-def shapes(H, F):
-    return {"qkv": (3 * H, H), "out": (H, H), "fc1": (F, H), "fc2": (H, F)}
-
-
-class Model:
-    def __init__(self, ctx, L, H, F, dtype, alpha, resident, max_batch=8, seed=0):
-        self.ctx, self.L, self.H, self.F, self.dtype = ctx, L, H, F, dtype
-        self.W, self.b = [], []
-        for l in range(L):
-            for name in NAMES:
-                n, k = shapes(H, F)[name]
-                W = Pinned(hg, ctx, (n, k), np.uint16)
-                b = Pinned(hg, ctx, (n,), np.uint16)
-                synth.fill_normal_ptr(W.ptr, n * k, dtype, seed, synth.weight_id(l, name), 0.0, 0.02)
-                synth.fill_normal_ptr(b.ptr, n, dtype, seed, synth.bias_id(l, name), 0.0, 0.02)
-                self.W.append(W)
-                self.b.append(b)
-        self.alpha = list(alpha) if hasattr(alpha, "__len__") else [alpha] * (4 * L)
-        self.resident = list(resident) if hasattr(resident, "__len__") else [resident] * (4 * L)
-        self.m = hg.hetegen_model_create(ctx, L, H, F, dtype, [w.ptr for w in self.W], [b.ptr for b in self.b],
-                                         self.alpha, self.resident, max_batch)
-
-    def step(self, x_bits, trace=False):
-        B = x_bits.shape[0]
-        x = torch_dev_from_np(x_bits)
-        out = torch.full((B, self.H), -1, dtype=torch.int16, device="cuda")
-        tr = None
-        if trace:
-            nb = hg.hetegen_model_trace_bytes(self.m, B)
-            tr = torch.full((nb // 2,), -1, dtype=torch.int16, device="cuda")
-            hg.hetegen_model_set_trace(self.m, tr.data_ptr(), nb)
-        s = torch.cuda.current_stream().cuda_stream
-        hg.hetegen_decode_step(self.ctx, self.m, x.data_ptr(), out.data_ptr(), B, s)
-        torch.cuda.synchronize()
-        if trace:
-            hg.hetegen_model_set_trace(self.m, 0, 0)
-        o = np_from_dev(out, np.uint16)
-        return (o, np_from_dev(tr, np.uint16)) if trace else o
-
-    def split_trace(self, tr, B):
-        items, off = [], 0
-        for l in range(self.L):
-            for name in NAMES:
-                n, k = shapes(self.H, self.F)[name]
-                xin = tr[off:off + B * k].reshape(B, k)
-                off += B * k
-                yout = tr[off:off + B * n].reshape(B, n)
-                off += B * n
-                items.append((name, l, xin, yout))
-        return items
-
-    def step_kv(self, x_bits, pos, trace=False):
-        B = x_bits.shape[0]
-        x = torch_dev_from_np(x_bits)
-        out = torch.full((B, self.H), -1, dtype=torch.int16, device="cuda")
-        tr = None
-        if trace:
-            nb = hg.hetegen_model_trace_bytes(self.m, B)
-            tr = torch.full((nb // 2,), -1, dtype=torch.int16, device="cuda")
-            hg.hetegen_model_set_trace(self.m, tr.data_ptr(), nb)
-        s = torch.cuda.current_stream().cuda_stream
-        hg.hetegen_decode_step_kv(self.ctx, self.m, x.data_ptr(), out.data_ptr(), B, pos, s)
-        torch.cuda.synchronize()
-        if trace:
-            hg.hetegen_model_set_trace(self.m, 0, 0)
-        o = np_from_dev(out, np.uint16)
-        return (o, np_from_dev(tr, np.uint16)) if trace else o
-
-    def check_teacher_forced(self, x_bits, tr, attn=None):
-        dt, H = self.dtype, self.H
-        B = x_bits.shape[0]
-        items = self.split_trace(tr, B)
-        x_l = x_bits
-        worst = 0.0
-        for i, (name, l, xin, yout) in enumerate(items):
-            W, b = self.W[i].a, self.b[i].a
-            lin = oracle.linear(xin, W, b, dt).astype(np.float64)
-            got = oracle.decode(yout, dt)
-            if name == "qkv":
-                h_ref = ods.layer_norm(oracle.decode(x_l, dt))
-                assert rel_err(oracle.decode(xin, dt), h_ref) <= TOL + U_ACT[dt], ("LN", l)
-                ref = lin
-                qkv_out = yout
-            elif name == "out":
-                if attn is None:
-                    assert np.array_equal(xin, qkv_out[:, 2 * H:3 * H]), ("V slice", l)
-                else:  # attention over the cache, from the traced q | k | v
-                    e = rel_err(oracle.decode(xin, dt), attn(l, qkv_out))
-                    assert e <= TOL + U_ACT[dt], ("attention", l, e)
-                ref = oracle.decode(x_l, dt).astype(np.float64) + lin
-                x_mid = yout
-            elif name == "fc1":
-                h_ref = ods.layer_norm(oracle.decode(x_mid, dt))
-                assert rel_err(oracle.decode(xin, dt), h_ref) <= TOL + U_ACT[dt], ("LN2", l)
-                ref = np.maximum(lin, 0.0)
-                f_out = yout
-            else:
-                assert np.array_equal(xin, f_out), ("fc2 input", l)
-                ref = oracle.decode(x_mid, dt).astype(np.float64) + lin
-                x_l = yout
-            e = rel_err(got, ref)
-            worst = max(worst, e)
-            assert e <= TOL + U_ACT[dt], (name, l, e)
-        return x_l, worst
-
-    def free(self):
-        hg.hetegen_model_destroy(self.ctx, self.m)
-        for p in self.W + self.b:
-            p.free()
-
 
 @pytest.fixture(scope="module")
 def ctx():
@@ -259,16 +146,24 @@ def test_opt13b_shape_one_layer_hetero(ctx):
 
 
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
-@pytest.mark.parametrize("B", [1, 2, 5, 8])
-def test_exec_modes_bit_identical(ctx, dtype, B):
+@pytest.mark.parametrize("B,max_batch", [(1, 1), (2, 4), (4, 4), (1, 8), (5, 8), (8, 8)])
+def test_exec_modes_bit_identical(ctx, dtype, B, max_batch):
     # persistent (one cooperative launch, grid barriers), graph replay and eager
-    # per-linear launches compute every output row the same way
+    # per-linear launches compute every output row the same way; models for batches of 5
+    # or more (weights in matrix-core tile order) have no persistent mode
     L, H, F = 3, 512, 2048
-    m = Model(ctx, L, H, F, dtype, 0.0, 1)
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=max_batch)
+    tiled = max_batch >= 5
     try:
         xs = [synth.normal((B, H), dtype, 0, synth.act_id(t)) for t in range(3)]
         outs = {}
-        for mode in (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT, hg.EXEC_AUTO):
+        if tiled:
+            with pytest.raises(hg.HetegenError) as e:
+                hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT)
+            assert e.value.status == hg.ERR_UNSUPPORTED
+        modes = (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_AUTO) if tiled else \
+            (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT, hg.EXEC_AUTO)
+        for mode in modes:
             hg.hetegen_model_set_exec(m.m, mode)
             outs[mode] = [m.step(x) for x in xs] + [m.step(xs[0])]
             want = {hg.EXEC_AUTO: hg.EXEC_EAGER}.get(mode, mode)
@@ -276,10 +171,10 @@ def test_exec_modes_bit_identical(ctx, dtype, B):
         for mode, o in outs.items():
             for a, b in zip(o, outs[hg.EXEC_EAGER]):
                 assert np.array_equal(a, b), mode
-        # and the persistent result is the teacher-forced-checked eager result
+        # and the result is the teacher-forced-checked eager result
         _, tr = m.step(xs[1], trace=True)
         last, _ = m.check_teacher_forced(xs[1], tr)
-        assert np.array_equal(outs[hg.EXEC_PERSISTENT][1], last)
+        assert np.array_equal(outs[modes[-2]][1], last)
     finally:
         m.free()
 
