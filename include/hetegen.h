@@ -157,6 +157,23 @@ HETEGEN_API hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_
                                                 const void* bias_dev, void* y_dev, hetegen_dtype y_dtype,
                                                 void* stream);
 
+/* hetegen_linear_tiled for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation): same
+ * arguments and results, but the split-K partials and arrival counters live in a
+ * fixed scratch array compiled into the library, one per GPU, set up by
+ * hetegen_create and held until the process ends (4 MiB of partials and 65536
+ * counters, 4.25 MiB per GPU).  The call allocates nothing; it returns UNSUPPORTED,
+ * without launching, for a shape whose split needs more than that, i.e.
+ * ceil(N / 16) * splits * 16 * B floats with splits = 2, 4 or 8 for K of 8192, 16384
+ * or 32768 and more (OPT-66B's fc2 [9216, 36864] at batch 8 needs 589824).  Every
+ * call on one GPU shares that GPU's scratch: calls that overlap on one GPU (from
+ * several streams, contexts or threads) race and give undefined results.  A launch
+ * returns the counters it used to zero, so calls in stream order need no clearing. */
+HETEGEN_API hetegen_status hetegen_linear_tiled_noalloc(hetegen_ctx* ctx, const void* x_dev, int B, int K,
+                                                        const void* W_tiled_dev, int N, hetegen_dtype w_dtype,
+                                                        const void* bias_dev, void* y_dev, hetegen_dtype y_dtype,
+                                                        void* stream);
+
 /* ---- Alpha planner: computation distribution law (Sec. 3.2, Eq. 4-7; Eq. 8-9) ---- */
 
 typedef struct {

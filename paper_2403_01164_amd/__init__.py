@@ -70,6 +70,7 @@ _SIGS = {
     "hetegen_tiled_bytes": ([_i, _i], _sz),
     "hetegen_tile_weights": ([_vp, _vp, _i, _i, _vp, _vp], _i),
     "hetegen_linear_tiled": ([_vp, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _i, _vp], _i),
+    "hetegen_linear_tiled_noalloc": ([_vp, _vp, _i, _i, _vp, _i, _i, _vp, _vp, _i, _vp], _i),
     "hetegen_layer_plan": ([ctypes.POINTER(Shape), _i, ctypes.POINTER(Bw), _i, _i, ctypes.POINTER(_d)], _i),
     "hetegen_probe": ([_vp, _vp, _i, _i, _i, _i, _i, _i, ctypes.POINTER(Bw)], _i),
     "hetegen_alpha_fit": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_d), _i, _i, _d, _d,
@@ -175,6 +176,18 @@ def hetegen_tile_weights(ctx, W_dev, rows, K, W_tiled_dev, stream=0):
 def hetegen_linear_tiled(ctx, x_dev, B, K, W_tiled_dev, N, w_dtype, bias_dev, y_dev, y_dtype, stream=0):
     _check(_lib.hetegen_linear_tiled(ctx, x_dev, B, K, W_tiled_dev, N, w_dtype, bias_dev or None, y_dev, y_dtype,
                                      stream or None), ctx)
+
+
+def hetegen_linear_tiled_noalloc(ctx, x_dev, B, K, W_tiled_dev, N, w_dtype, bias_dev, y_dev, y_dtype, stream=0):
+    _check(_lib.hetegen_linear_tiled_noalloc(ctx, x_dev, B, K, W_tiled_dev, N, w_dtype, bias_dev or None, y_dev,
+                                             y_dtype, stream or None), ctx)
+
+
+def hetegen_linear_tiled_noalloc_status(ctx, *args):
+    """Same arguments as hetegen_linear_tiled_noalloc; returns the raw status instead of raising."""
+    (x_dev, B, K, W_tiled_dev, N, w_dtype, bias_dev, y_dev, y_dtype, stream) = args
+    return _lib.hetegen_linear_tiled_noalloc(ctx, x_dev, B, K, W_tiled_dev, N, w_dtype, bias_dev or None, y_dev,
+                                             y_dtype, stream or None)
 
 
 def hetegen_linear_tiled_status(ctx, *args):

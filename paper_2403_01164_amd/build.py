@@ -36,7 +36,7 @@ def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
     objs = []
     hipcc = os.path.join(ROCM, "bin", "hipcc")
-    for src in ("kernels.hip", "attention.hip", "hbm_probe.hip"):
+    for src in ("kernels.hip", "attention.hip", "hbm_probe.hip", "scratch.hip"):
         o = os.path.join(BUILD, src + ".o")
         _run([hipcc] + HIPCC_FLAGS + ["-c", os.path.join(CSRC, src), "-o", o])
         objs.append(o)

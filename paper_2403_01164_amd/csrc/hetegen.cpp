@@ -848,6 +848,11 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
       return st;
     };
     if (hipSetDevice(c.device) != hipSuccess) return bail(fail(ctx, HETEGEN_ERR_HIP, "hipSetDevice(%d)", c.device));
+    // address of this device's fixed split-K scratch (hetegen_linear_tiled_noalloc), once per device
+    {
+      const hipError_t se = hg::scratch_init(c.device);
+      if (se != hipSuccess) return bail(fail(ctx, HETEGEN_ERR_HIP, "scratch set-up: %s", hipGetErrorString(se)));
+    }
     if (hipStreamCreateWithFlags(&ctx->copy_stream, hipStreamNonBlocking) != hipSuccess ||
         hipStreamCreateWithFlags(&ctx->capture_stream, hipStreamNonBlocking) != hipSuccess)
       return bail(fail(ctx, HETEGEN_ERR_HIP, "stream creation failed"));
@@ -1083,6 +1088,49 @@ hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_dev, int B, 
     HIPCHK(ctx, hg::launch_gemv_mfma(p, w_dtype, B, st));
     ts.end();
     return finish_call(ctx, t0);
+  });
+}
+
+hetegen_status hetegen_linear_tiled_noalloc(hetegen_ctx* ctx, const void* x_dev, int B, int K,
+                                            const void* W_tiled_dev, int N, hetegen_dtype w_dtype,
+                                            const void* bias_dev, void* y_dev, hetegen_dtype y_dtype, void* stream) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!x_dev || !W_tiled_dev || !y_dev) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "x_dev, W_tiled_dev and y_dev are required");
+    if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
+    if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
+    if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+    if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
+    if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "y dtype must be the weight dtype or fp32");
+    if (!aligned16(x_dev) || !aligned16(W_tiled_dev))
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "x and the tiled weight must be 16-byte aligned");
+    const size_t need = hg::mfma_ws_floats(N, K, B), words = hg::mfma_cnt_words(N, K);
+    if (need > hg::kScratchFloats || words > hg::kScratchCounterWords)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED,
+                  "[%d, %d] at batch %d needs %zu partial floats and %zu counters of split-K scratch; the fixed "
+                  "scratch holds %zu and %zu (use hetegen_linear_tiled)",
+                  N, K, B, need, words, hg::kScratchFloats, hg::kScratchCounterWords);
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    uint32_t* base = (uint32_t*)hg::scratch_ptr(ctx->device);
+    if (!base) return fail(ctx, HETEGEN_ERR_HIP, "the fixed scratch of device %d is not set up", ctx->device);
+    hg::GemvParams p{};
+    p.x = x_dev;
+    p.ldx = K;
+    p.W = W_tiled_dev;
+    p.bias = bias_dev;
+    p.y = y_dev;
+    p.ldy = N;
+    p.rows = N;
+    p.K = K;
+    p.epi = hg::EPI_NONE;
+    p.y_f32 = y_dtype == HETEGEN_F32;
+    p.cnt = base;
+    p.ws = (float*)(base + hg::kScratchCounterWords);
+    HIPCHK(ctx, hg::launch_gemv_mfma(p, w_dtype, B, (hipStream_t)stream));
+    return HETEGEN_OK;
   });
 }
 

@@ -124,4 +124,14 @@ size_t mfma_cnt_words(int rows, int K);
 // Split launches need p.ws and p.cnt.
 hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream);
 
+// Fixed split-K scratch of the matrix-core GEMV, one per GPU, for callers that cannot
+// allocate: kScratchCounterWords counters, then kScratchFloats floats of partials.
+constexpr size_t kScratchCounterWords = 65536;
+constexpr size_t kScratchFloats = (size_t)1 << 20;
+// Takes the scratch's address on `device` (which must be current) and zeroes its counters,
+// once per device; later calls return at once.
+hipError_t scratch_init(int device);
+// The scratch's device address on `device` (nullptr before scratch_init).
+void* scratch_ptr(int device);
+
 }  // namespace hg
