@@ -17,6 +17,14 @@ heterogeneous figures (link and CPU rates, Table-2-style busy fractions).
 under --hbm-budget; --pageable keeps the weights in plain pageable memory, streamed
 through the hybrid pin || transfer path (Sec. 4.2-4.3).
 
+The default run (no --model) measures the all-resident OPT-6.7B line above and then,
+after freeing it, the streamed half of the metric in the same process (`streamed` in the
+same JSON line; --no-streamed skips it): OPT-30B shapes, 48 layers, every linear in
+pinned host memory, the planner's CPU fractions refined by the step-level alpha
+benchmark, batch 1, 32 steps; the same model with every GPU row streamed (CPU
+fraction 0, 2 steps); both against the idle link, one 1 GiB pinned host-to-device copy,
+median of 10, measured first.
+
 Prints ONE JSON line.  `value` is the effective weight bandwidth of the whole step
 (weight bytes per step / time per step); `ms_per_step` is the decode latency per
 token.  `roofline` (all-resident workloads) is the GEMV kernel's algorithmic bytes
@@ -239,12 +247,45 @@ def single_linear(args, torch, synth, hg):
     hg.hetegen_host_free(ctx, bh)
     hg.hetegen_destroy(ctx)
 
+def mfma_splits(K):
+    """Splits of the sum over K in the matrix-core GEMV (the library's rule)."""
+    kt, g = (K + 31) // 32, 1
+    while g < 8 and kt // (2 * g) >= 128:
+        g *= 2
+    return g
+
+
+def gemv_label(B, H, F, dt):
+    """GEMV kernels an all-resident eager step at batch B runs (the library's dispatch rules;
+    the bench creates its model for batch B, so B >= 5 means tile-ordered weights)."""
+    t = "BF16" if dt == 1 else "F16"
+    if B >= 5:
+        parts = {}
+        for name, (n, k) in zip(NAMES, shapes(H, F)):
+            g = mfma_splits(k)
+            key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, 8 if g == 1 else 4, "" if g == 1 else " (K split %d)" % g)
+            parts.setdefault(key, []).append(name)
+        ni = -(-H // 2048)
+        ni = ni if ni <= 5 else 8
+        return " + ".join("%s: %s" % (k, ", ".join(v)) for k, v in parts.items()) + \
+            " + layernorm_regs_kernel<%s,%d> before qkv and fc1" % (t, ni)
+    if B == 1:
+        if H % 512 == 0 and H // 512 in (1, 2, 4, 5, 8, 10, 14):
+            return "gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (t, H // 512, t)
+        return "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (t, t)
+    if B == 2:
+        return "gemv_kernel<%s,2,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,2> (out, fc2)" % (t, t)
+    return "gemv_kernel<%s,%d,1,4> (qkv, out, fc1, fc2; LayerNorm fused in qkv and fc1)" % (t, B)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=32)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--model", default="opt-6.7b", choices=sorted(OPT))
+    ap.add_argument("--model", default=None, choices=sorted(OPT),
+                    help="one workload (default: the OPT-6.7B all-resident line, followed by the streamed leg "
+                         "below unless --no-streamed)")
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N decoder layers (0: all); reported in config")
@@ -285,6 +326,13 @@ def main():
                          "CPU fractions 0, .25, .5, 1, resident and streamed, over --linear-reps calls that rotate "
                          "weight copies totalling > 512 MB (prints its own JSON line)")
     ap.add_argument("--linear-reps", type=int, default=200)
+    ap.add_argument("--no-streamed", action="store_true",
+                    help="default run only: skip the streamed leg (OPT-30B shapes, every linear in pinned host "
+                         "memory, planner alpha refined by the step-level benchmark, batch 1)")
+    ap.add_argument("--streamed-steps", type=int, default=32, help="timed steps of the streamed leg")
+    ap.add_argument("--all-streamed-steps", type=int, default=None,
+                    help="streamed workloads: also time this many steps with every GPU row streamed (CPU "
+                         "fraction 0), against the idle link (default: 2 in the streamed leg, 0 otherwise)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: there is no multi-GPU path (the heterogeneous "
@@ -301,6 +349,46 @@ def main():
     if args.linear:
         single_linear(args, torch, synth, hg)
         return
+    default_run = args.model is None
+    if default_run:
+        args.model = "opt-6.7b"
+    result = decode_workload(args, torch, synth, hg)
+    if default_run and not args.no_streamed:
+        result["streamed"] = streamed_leg(args, torch, synth, hg)
+    print(json.dumps(result), flush=True)
+
+
+def streamed_leg(args, torch, synth, hg):
+    """The streamed half of the metric, after the headline line has freed its memory:
+    OPT-30B shapes (48 layers, 59.2 GB of fp16 weights), every linear in pinned host
+    memory, CPU fractions from the planner refined by the step-level alpha benchmark,
+    batch 1; plus the all-streamed point (CPU fraction 0) and the idle link."""
+    import copy
+    a = copy.copy(args)
+    a.model, a.batch, a.layers, a.placement, a.hbm_budget = "opt-30b", 1, 0, "none", None
+    a.alpha, a.alpha_sweep, a.alpha_bench, a.pageable, a.context, a.exec = None, None, True, False, 0, "auto"
+    a.steps, a.warmup, a.no_cpu_baseline, a.copy_calibration = args.streamed_steps, 2, True, False
+    a.all_streamed_steps = 2 if args.all_streamed_steps is None else args.all_streamed_steps
+    log("streamed leg: OPT-30B shapes, all linears in pinned host memory, batch 1, %d steps" % a.steps)
+    r = decode_workload(a, torch, synth, hg)
+    h = r["hetero"]
+    keep = {"workload": r["config"]["workload"], "steps": r["steps"], "warmup": r["warmup"],
+            "ms_per_token": r["ms_per_step"], "step_ms_p10_p50_p90": r["step_ms_p10_p50_p90"],
+            "weight_GBps": r["value"], "weight_bytes_per_step": r["config"]["weight_bytes_per_step"],
+            "roofline": h["roofline"], "ideal_ms_per_step": h["ideal_ms_per_step"],
+            "frac_of_ideal": h["frac_of_ideal"], "busy_frac": h["busy_frac"],
+            "link_idle_GBps": h["link_idle_GBps"], "h2d_GBps_over_step": h["h2d_GBps_over_step"],
+            "cpu_GBps_over_step": h["cpu_GBps_over_step"], "alpha_cpu_by_linear": h["alpha_cpu_by_linear"],
+            "probe_GBps": h["probe_GBps"]}
+    for k in ("all_streamed", "alpha_benchmark"):
+        if k in r:
+            keep[k] = r[k]
+    return keep
+
+
+def decode_workload(args, torch, synth, hg):
+    """One decode-step workload (args.model, args.batch, placement ...); returns the result dict
+    after freeing every buffer it allocated."""
     L, H, F, dt, placement = OPT[args.model]
     L_full = L
     if args.layers:
@@ -311,6 +399,14 @@ def main():
                             pin_threads=args.pin_threads, pin_ring=args.pin_ring)
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
+
+    res_layers = L if placement == "all" else L // 2 if placement == "half" else 0
+    link_idle = None
+    if placement != "all":
+        # idle host-to-device link, before the weights take the pinned memory: one 1 GiB
+        # pinned copy, median of 10 (the denominator of the streamed path's roofline)
+        link_idle = hg.hetegen_probe_link(ctx, 1 << 30, 10)
+        log("idle link: %.2f GB/s (1 GiB pinned host-to-device copy, median of 10)" % (link_idle / 1e9))
 
     # ---- synthetic OPT-shaped weights in pinned (or pageable) host memory ----
     t0 = time.time()
@@ -335,7 +431,6 @@ def main():
     wbytes = sum(n * k * 2 for n, k in shp)
     log("generated %.3f GB of weights in %.1f s" % (wbytes / 1e9, time.time() - t0))
 
-    res_layers = L if placement == "all" else L // 2 if placement == "half" else 0
     resident = [1 if (i // 4) < res_layers else 0 for i in range(4 * L)]
     streamed = [i for i in range(4 * L) if not resident[i]]
 
@@ -461,7 +556,8 @@ def main():
     else:
         desc = "all linears in %s host memory, streamed + CPU share" % ("pageable" if args.pageable else "pinned")
     if placement != "all":
-        desc += ", %s" % ("planner alpha" if args.alpha is None else "alpha=%g" % args.alpha)
+        desc += ", %s" % ("alpha=%g" % args.alpha if args.alpha is not None else
+                          "planner alpha refined by the step-level alpha benchmark" if refined else "planner alpha")
     if P > 0:
         desc += ", attention over a %d-position KV cache (positions %d-%d decoded)" % (P, P + args.warmup,
                                                                                       P + nstep - 1)
@@ -519,19 +615,8 @@ def main():
         achieved = bytes_per_launch / (avg_us * 1e-6) / 1e9
         log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
             (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
-        tname = "BF16" if dt == 1 else "F16"
-        if exec_mode == "persistent":
-            kernel_label = "step_kernel<%s,%d,...>" % (tname, B)
-        elif B == 1:
-            kernel_label = ("gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (tname, H // 512, tname)
-                            if H % 512 == 0 and H // 512 in (1, 2, 4, 5, 8, 10, 14) else
-                            "gemv_kernel<%s,1,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (tname, tname))
-        elif B == 2:
-            kernel_label = "gemv_kernel<%s,2,1,8> (qkv, fc1) + gemv_x1_kernel<%s,4,2> (out, fc2)" % (tname, tname)
-        else:
-            # from batch 5 on the LayerNorm of qkv and fc1 is its own launch (counted in the
-            # time, not in the GEMV launches)
-            kernel_label = "gemv_kernel<%s,%d,...>%s" % (tname, B, " + layernorm_kernel" if B > 4 else "")
+        kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
+            else gemv_label(B, H, F, dt)
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
         read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
@@ -551,6 +636,12 @@ def main():
                               "frac_of_achievable": round(achieved / read_gbps, 4),
                               "read_same_launches_ms": round(read_step_ms, 5),
                               "frac_of_read_same_launches": round(read_step_ms / ms_step, 4)}
+        if B >= 5 and exec_mode != "persistent":
+            # the timed region also holds the LayerNorm launches before qkv and fc1 (B x H x 2
+            # bytes read and written each); they are not in launches_per_step or bytes_per_launch,
+            # so `achieved` understates the GEMV's own rate by their share of the step
+            result["roofline"]["region_also_holds"] = "%d layernorm_regs_kernel launches per step (%d bytes each)" % (
+                2 * L, B * H * 4)
     elif streamed:
         # heterogeneous figures: link and CPU rates, the ideal rate of Eq. 4, busy fractions
         sb = sum(shp[i][0] * shp[i][1] * 2 for i in streamed)
@@ -581,7 +672,16 @@ def main():
                            for k, v in probe.items()},
             "streamed_bytes_per_step": sb, "h2d_bytes_per_step": h2d_b, "cpu_bytes_per_step": cpu_b,
             "h2d_GBps_over_step": round(h2d_b / (ms_step * 1e-3) / 1e9, 2),
-            "h2d_frac_of_probe_link": round(h2d_b / (ms_step * 1e-3) / v_com, 4),
+            "link_idle_GBps": round(link_idle / 1e9, 2),
+            "h2d_frac_of_idle_link": round(h2d_b / (ms_step * 1e-3) / link_idle, 4),
+            # the planner's V_COM (copies timed while the CPU share runs), for information
+            "h2d_frac_of_concurrent_probe": round(h2d_b / (ms_step * 1e-3) / v_com, 4),
+            "roofline": {"bound": "pcie", "achieved": round(h2d_b / (ms_step * 1e-3) / 1e9, 2),
+                         "peak": round(link_idle / 1e9, 2), "unit": "GB/s",
+                         "frac": round(h2d_b / (ms_step * 1e-3) / link_idle, 4), "traffic": None,
+                         "kernel": "streamed GPU rows: chunk copies (hipMemcpyAsync on the copy stream)",
+                         "achieved_is": "weight bytes streamed host-to-device per step / step time",
+                         "peak_is": "idle 1 GiB pinned host-to-device copy, median of 10, same run"},
             "cpu_GBps_over_step": round(cpu_b / (ms_step * 1e-3) / 1e9, 2),
             # host-memory bytes of the step: the CPU share reads its rows once; a streamed row is
             # read once by the DMA from pinned memory, or, from pageable memory, read and written
@@ -606,6 +706,31 @@ def main():
                                  "n_cpu_shares": int(tprof["cpu_shares"] // args.steps)},
         }
         log("hetero: %s" % json.dumps(result["hetero"]))
+
+    n_all = args.all_streamed_steps or 0
+    if streamed and n_all > 0:
+        # every GPU row streamed (CPU fraction 0 on every host-resident linear): the streamed
+        # path alone against the idle link
+        hg.hetegen_model_set_alpha(model, [0.0] * (4 * L))
+        step(0)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for t in range(n_all):
+            step(1 + t)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_all = e0.elapsed_time(e1) / n_all
+        hg.hetegen_model_set_alpha(model, alpha)
+        ach = sb / (ms_all * 1e-3) / 1e9
+        result["all_streamed"] = {
+            "alpha_cpu": 0.0, "steps": n_all, "ms_per_step": round(ms_all, 3),
+            "weight_GBps": round(wbytes / (ms_all * 1e-3) / 1e9, 2),
+            "roofline": {"bound": "pcie", "achieved": round(ach, 2), "peak": round(link_idle / 1e9, 2), "unit": "GB/s",
+                         "frac": round(ach * 1e9 / link_idle, 4), "traffic": None,
+                         "achieved_is": "streamed weight bytes per step / step time (every row streamed)",
+                         "peak_is": "idle 1 GiB pinned host-to-device copy, median of 10, same run"}}
+        log("all streamed: %.1f ms/token, %.2f GB/s over the link (%.3f of the idle link)" %
+            (ms_all, ach, ach * 1e9 / link_idle))
 
     if refined:
         # the same step with the closed-form fractions, for comparison
@@ -681,7 +806,7 @@ def main():
     for p in (b if args.pageable else W + b):
         hg.hetegen_host_free(ctx, p)
     hg.hetegen_destroy(ctx)
-    print(json.dumps(result), flush=True)
+    return result
 
 
 if __name__ == "__main__":

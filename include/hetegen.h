@@ -229,6 +229,14 @@ HETEGEN_API hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, i
  * denominator the resident GEMV is compared with next to the nominal HBM peak. */
 HETEGEN_API hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out);
 
+/* Idle host-to-device link rate: one hipMemcpyAsync of `bytes` (>= 1 MiB, a multiple
+ * of 16) from a pinned host buffer (allocated like hetegen_host_alloc, touched first)
+ * to device memory on the context's copy stream, nothing else running in the call;
+ * *Bps_out = bytes / median time of `reps` copies after one warm-up copy.  The link
+ * figure the streamed path is compared with (Sec. 5, Table 1 lists the platform's
+ * CPU-GPU link bandwidth); the planner's V_COM comes from hetegen_probe. */
+HETEGEN_API hetegen_status hetegen_probe_link(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out);
+
 /* The CPU share alone (Sec. 3.2: the host cores compute the rows whose parameters
  * stay in host memory), on the calling thread and the library's CPU worker team (one
  * job at a time; calls from several threads are serialised), no device involved:

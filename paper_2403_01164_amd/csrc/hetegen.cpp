@@ -1607,6 +1607,51 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
   });
 }
 
+// ---- idle host-to-device link rate ----
+extern "C" hetegen_status hetegen_probe_link(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!Bps_out || reps < 1 || bytes < ((size_t)1 << 20) || (bytes & 15))
+      return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe_link: bad arguments");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    void* dev = nullptr;
+    void* host = nullptr;
+    if (host_malloc(ctx, &host, bytes, hipHostMallocDefault) != hipSuccess || hipMalloc(&dev, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      if (host) (void)hipHostFree(host);
+      if (dev) (void)hipFree(dev);
+      return fail(ctx, HETEGEN_ERR_OOM, "link probe buffers of %zu bytes", bytes);
+    }
+    memset(host, 0x11, bytes);  // touch every page before timing
+    hipEvent_t a = nullptr, b = nullptr;
+    hetegen_status st = HETEGEN_OK;
+    std::vector<double> t;
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess)
+      st = fail(ctx, HETEGEN_ERR_HIP, "link probe events");
+    for (int r = 0; st == HETEGEN_OK && r <= reps; ++r) {  // the first copy warms up
+      float ms = 0;
+      if (hipEventRecord(a, ctx->copy_stream) != hipSuccess ||
+          hipMemcpyAsync(dev, host, bytes, hipMemcpyHostToDevice, ctx->copy_stream) != hipSuccess ||
+          hipEventRecord(b, ctx->copy_stream) != hipSuccess || hipEventSynchronize(b) != hipSuccess ||
+          hipEventElapsedTime(&ms, a, b) != hipSuccess) {
+        st = fail(ctx, HETEGEN_ERR_HIP, "link probe copy failed");
+        break;
+      }
+      if (r > 0) t.push_back(ms * 1e-3);
+    }
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    (void)hipHostFree(host);
+    (void)hipFree(dev);
+    (void)hipGetLastError();
+    if (st != HETEGEN_OK) return st;
+    std::sort(t.begin(), t.end());
+    *Bps_out = (double)bytes / t[t.size() / 2];
+    return HETEGEN_OK;
+  });
+}
+
 // ---- achievable HBM read bandwidth ----
 extern "C" hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out) {
   return api_guard(ctx, [&]() -> hetegen_status {
