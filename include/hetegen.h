@@ -80,7 +80,12 @@ typedef struct {
  * the first pageable chunk.  For full overlap with the CPU share, ring_depth x
  * chunk_bytes should hold the largest GPU share of a streamed linear: the GEMVs of
  * chunks that were not yet staged when the CPU share starts are enqueued after it.
- * cfg may be NULL (device 0, defaults).  *out receives the context. */
+ * cfg may be NULL (device 0, defaults).  *out receives the context.
+ * Testing aid: with the environment variable HETEGEN_POISON set (and not "0") when the
+ * context is created, every staging slot, pinned staging buffer and host hand-off
+ * buffer is filled with all-ones bits (NaN in fp16, bf16 and binary32) before each
+ * reuse, so a read that is not ordered after the data it needs shows up as NaN; it
+ * costs one device fill per streamed chunk. */
 HETEGEN_API hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out);
 
 /* Wait for the context's work and free everything it owns.  NULL is a no-op. */

@@ -44,6 +44,7 @@
 #include "cpu_share.h"
 #include "hbm_probe.h"
 #include "kernels.h"
+#include "pin_team.h"
 
 namespace {
 
@@ -69,86 +70,6 @@ constexpr int kMaxBatch = 8;
 constexpr int kTiledMinBatch = 5;
 constexpr int kDefaultPinThreads = 4;
 constexpr int kDefaultPinRing = 4;
-
-// Fork-join team for large host copies: the calling thread takes the first part,
-// helpers the others (page-aligned contiguous parts).
-class PinTeam {
- public:
-  ~PinTeam() { shutdown(); }
-  bool started() const { return parts_ > 0; }
-  bool start(int threads) {
-    parts_ = std::max(1, threads);
-    try {
-      for (int i = 1; i < parts_; ++i) th_.emplace_back([this, i] { work(i); });
-    } catch (...) {
-      shutdown();
-      return false;
-    }
-    return true;
-  }
-  void copy(char* dst, const char* src, size_t n) {
-    if (parts_ <= 1 || n < ((size_t)1 << 20)) {
-      memcpy(dst, src, n);
-      return;
-    }
-    {
-      std::lock_guard<std::mutex> lk(m_);
-      dst_ = dst;
-      src_ = src;
-      n_ = n;
-      pending_ = parts_ - 1;
-      ++gen_;
-    }
-    cv_.notify_all();
-    part(dst, src, n, 0);
-    std::unique_lock<std::mutex> lk(m_);
-    done_.wait(lk, [&] { return pending_ == 0; });
-  }
-  void shutdown() {
-    {
-      std::lock_guard<std::mutex> lk(m_);
-      stop_ = true;
-    }
-    cv_.notify_all();
-    for (auto& t : th_) t.join();
-    th_.clear();
-    parts_ = 0;
-    stop_ = false;
-  }
-
- private:
-  void part(char* dst, const char* src, size_t n, int i) const {
-    const size_t per = (n / parts_ + 4095) & ~(size_t)4095;
-    const size_t b = per * i;
-    if (b >= n) return;
-    memcpy(dst + b, src + b, std::min(n, b + per) - b);
-  }
-  void work(int i) {
-    long long seen = 0;
-    std::unique_lock<std::mutex> lk(m_);
-    for (;;) {
-      cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
-      if (stop_) return;
-      seen = gen_;
-      char* d = dst_;
-      const char* s = src_;
-      const size_t n = n_;
-      lk.unlock();
-      part(d, s, n, i);
-      lk.lock();
-      if (--pending_ == 0) done_.notify_one();
-    }
-  }
-  std::vector<std::thread> th_;
-  std::mutex m_;
-  std::condition_variable cv_, done_;
-  long long gen_ = 0;
-  int pending_ = 0, parts_ = 0;
-  bool stop_ = false;
-  char* dst_ = nullptr;
-  const char* src_ = nullptr;
-  size_t n_ = 0;
-};
 
 }  // namespace
 
@@ -192,7 +113,7 @@ struct hetegen_ctx {
   std::vector<void*> bounce;
   std::vector<hipEvent_t> ev_bounce;
   long long bounce_seq = 0;  // manager thread only
-  PinTeam team;
+  hg::PinTeam team;
   // profiling (the manager records copy events too: `prof_mu`)
   std::mutex prof_mu;
   bool profiling = false;
@@ -205,6 +126,9 @@ struct hetegen_ctx {
   std::vector<hipEvent_t> ev_pool;
   hetegen_profile prof{};
   std::string err;
+  // HETEGEN_POISON at creation: staging slots, pinned staging buffers and hand-off buffers
+  // are filled with all-ones bits (NaN in fp16, bf16 and binary32) before every reuse
+  bool poison = false;
   // split-K workspace of hetegen_linear_tiled (grown on demand; counters zero between launches)
   float* ws = nullptr;
   size_t ws_floats = 0;
@@ -488,6 +412,7 @@ bool copy_chunk(hetegen_ctx* ctx, long long s, const hetegen_ctx::Chunk& c, std:
   if (c.pageable) {
     b = (int)(ctx->bounce_seq++ % ctx->pin_ring);
     MGR_HIP(hipEventSynchronize(ctx->ev_bounce[b]));  // its previous copy has read it
+    if (ctx->poison) memset(ctx->bounce[b], 0xFF, ctx->chunk_bytes);
     const auto t0 = Clock::now();
     ctx->team.copy((char*)ctx->bounce[b], c.src, c.bytes);
     {
@@ -504,6 +429,8 @@ bool copy_chunk(hetegen_ctx* ctx, long long s, const hetegen_ctx::Chunk& c, std:
     if (c.host_wait) MGR_HIP(hipEventSynchronize(ctx->ev_free[slot]));
     else MGR_HIP(hipStreamWaitEvent(ctx->copy_stream, ctx->ev_free[slot], 0));
   }
+  // poisoned slot: a GEMV that read it before this copy landed, or past the chunk, sees NaN
+  if (ctx->poison) MGR_HIP(hipMemsetAsync(ctx->slot[slot], 0xFF, ctx->chunk_bytes, ctx->copy_stream));
   TimedScope ts(ctx, ctx->copy_stream, 0, (double)c.bytes);
   MGR_HIP(hipMemcpyAsync(ctx->slot[slot], src, c.bytes, hipMemcpyHostToDevice, ctx->copy_stream));
   ts.end();
@@ -761,6 +688,7 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
     if (ctx->y_pending) HIPCHK(ctx, hipEventSynchronize(ctx->ev_y));
     ctx->y_pending = false;
     TRY(ensure_host(ctx, &ctx->y_host, &ctx->y_host_bytes, (size_t)j.B * j.n_cpu * 4));
+    if (ctx->poison) memset(ctx->y_host, 0xFF, (size_t)j.B * j.n_cpu * 4);  // rows the CPU share leaves unwritten
     HIPCHK(ctx, hipEventSynchronize(ctx->ev_x));
     ctx->prof.xwait_ms += ms_since(tw);
     ctx->prof.cpu_shares++;
@@ -769,6 +697,8 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
                   ctx->y_host, j.n_cpu, ctx->cpu_threads);
     ctx->prof.cpu_ms += ms_since(t0);
     ctx->prof.cpu_bytes += (double)j.n_cpu * j.K * s;
+    // the next CPU share must wait for its own hand-off: poisoned, a read before it lands is NaN
+    if (ctx->poison) memset(ctx->x_host, 0xFF, (size_t)j.B * j.K * 4);
     // 4. finish and place the CPU rows
     const size_t ys = j.y_f32 ? 4 : 2;
     HIPCHK(ctx, hg::launch_import_rows(ctx->y_host, j.B, j.n_cpu, j.dtype, j.epi, (char*)j.y + (size_t)j.n_gpu * ys,
@@ -842,6 +772,10 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
     ctx->pin_threads = c.pin_threads < 0 ? -1 : c.pin_threads;
     ctx->pin_ring = c.pin_ring;
     ctx->numa_node = c.numa_node - 1;
+    {
+      const char* pe = getenv("HETEGEN_POISON");
+      ctx->poison = pe && *pe && strcmp(pe, "0") != 0;
+    }
     auto bail = [&](hetegen_status st) {
       g_create_error = ctx->err;
       hetegen_destroy(ctx);
@@ -871,6 +805,8 @@ hetegen_status hetegen_create(const hetegen_config* cfg, hetegen_ctx** out) {
       if (hipEventCreateWithFlags(&ctx->ev_ready[i], hipEventDisableTiming) != hipSuccess ||
           hipEventCreateWithFlags(&ctx->ev_free[i], hipEventDisableTiming | hipEventBlockingSync) != hipSuccess)
         return bail(fail(ctx, HETEGEN_ERR_HIP, "event creation failed"));
+      if (ctx->poison && hipMemset(ctx->slot[i], 0xFF, c.chunk_bytes) != hipSuccess)
+        return bail(fail(ctx, HETEGEN_ERR_HIP, "staging slot poisoning failed"));
       // every slot starts free
       if (hipEventRecord(ctx->ev_free[i], ctx->copy_stream) != hipSuccess)
         return bail(fail(ctx, HETEGEN_ERR_HIP, "hipEventRecord failed"));
