@@ -247,6 +247,97 @@ def single_linear(args, torch, synth, hg):
     hg.hetegen_host_free(ctx, bh)
     hg.hetegen_destroy(ctx)
 
+def table2_linear(args, torch, synth, hg):
+    """Per-resource busy fractions of one heterogeneous linear, the analogue of Table 2 (Sec. 5.2:
+    OPT-13B, the first MLP linear, fc1 [20480, 5120]): at the planner's CPU fraction refined by
+    the alpha benchmark of this linear (Sec. 4.4), the share of the linear's wall time during which
+    the CPU share runs, the link copies chunks, the pin team stages pageable chunks and the GPU
+    runs GEMVs (events around each copy and launch).  Weights pinned, then pageable (the paper's
+    setting: its weights are pinned chunk by chunk at run time).  Two weight copies are rotated
+    so the CPU share reads DRAM, not cache."""
+    N, K = (int(v) for v in args.table2.lower().split("x"))
+    B, dt, ncopy = args.batch, 0, 2
+    ctx = hg.hetegen_create(0, cpu_threads=args.threads, chunk_bytes=args.chunk_mb << 20, ring_depth=args.ring,
+                            pin_threads=args.pin_threads, pin_ring=args.pin_ring)
+    s = torch.cuda.current_stream().cuda_stream
+    wb = N * K * 2
+    Wp, maps, Wq = [], [], []
+    for c in range(ncopy):
+        w = hg.hetegen_host_alloc(ctx, wb)
+        synth.fill_normal_ptr(w, N * K, dt, 0, synth.weight_id(c, "fc1"), 0.0, 0.02)
+        Wp.append(w)
+        mm = mmap.mmap(-1, wb)
+        if hasattr(mm, "madvise") and hasattr(mmap, "MADV_HUGEPAGE"):
+            mm.madvise(mmap.MADV_HUGEPAGE)
+        maps.append(mm)
+        q = ctypes.addressof(ctypes.c_char.from_buffer(mm))
+        ctypes.memmove(q, w, wb)
+        Wq.append(q)
+    bh = hg.hetegen_host_alloc(ctx, N * 2)
+    synth.fill_normal_ptr(bh, N, dt, 0, synth.bias_id(0, "fc1"), 0.0, 0.02)
+    bd = torch.from_numpy(np.ctypeslib.as_array((ctypes.c_int16 * N).from_address(bh)).copy()).cuda()
+    x = torch.from_numpy(synth.normal((B, K), dt, 0, synth.act_id(0)).view(np.int16)).cuda()
+    y = torch.empty((B, N), dtype=torch.float32, device="cuda")
+    rows = []
+    for kind, W in (("pinned", Wp), ("pageable", Wq)):
+        pr = hg.hetegen_probe(ctx, W[0], N, K, dt, B, 3, hg.PROBE_CONCURRENT if kind == "pinned" else 0)
+        a0 = hg.hetegen_layer_plan([(N, K, dt, 0)], [(pr["cpu_Bps"], pr["h2d_Bps"], pr["hbm_gemv_Bps"],
+                                                       pr["pin_Bps"])])[0]
+        a1, crossed = hg.hetegen_alpha_benchmark(ctx, x.data_ptr(), B, K, W[0], N, dt, bh, bd.data_ptr(),
+                                                 y.data_ptr(), a0, 0.05, 0.01, 2, 2, s)
+
+        def call(i):
+            hg.hetegen_linear(ctx, x.data_ptr(), B, K, W[i % ncopy], 0, N, dt, bh, bd.data_ptr(), a1, y.data_ptr(),
+                              hg.F32, s)
+        for i in range(3):
+            call(i)
+        torch.cuda.synchronize()
+        ts = []
+        for i in range(args.table2_reps):
+            t0 = time.perf_counter()
+            call(i)
+            torch.cuda.synchronize()
+            ts.append((time.perf_counter() - t0) * 1e3)
+        ts.sort()
+        hg.hetegen_set_profiling(ctx, 1)
+        hg.hetegen_get_profile(ctx, reset=True)
+        for i in range(args.table2_reps):
+            call(i)
+        torch.cuda.synchronize()
+        prof = hg.hetegen_get_profile(ctx, reset=True)
+        hg.hetegen_set_profiling(ctx, 0)
+        wall = prof["wall_ms"]
+        n_cpu = min(N, int(np.floor(a1 * N + 0.5)))
+        v_com = min(pr["h2d_Bps"], pr["pin_Bps"]) if pr["pin_Bps"] > 0 else pr["h2d_Bps"]
+        v_g = 1.0 / (1.0 / v_com + 1.0 / pr["hbm_gemv_Bps"])
+        ideal_ms = wb / (pr["cpu_Bps"] + v_g) * 1e3
+        row = {"weights": kind, "alpha_cpu_closed_form": round(a0, 4), "alpha_cpu": round(a1, 4),
+               "alpha_bench_crossed": crossed, "cpu_rows": n_cpu, "gpu_rows": N - n_cpu,
+               "median_ms": round(ts[len(ts) // 2], 3), "p10_ms": round(ts[len(ts) // 10], 3),
+               "p90_ms": round(ts[(9 * len(ts)) // 10], 3), "profiled_ms": round(wall / args.table2_reps, 3),
+               "eq4_ideal_ms": round(ideal_ms, 3), "frac_of_ideal": round(ideal_ms / ts[len(ts) // 2], 4),
+               "busy_frac": {"cpu": round(prof["cpu_ms"] / wall, 4), "io": round(prof["h2d_ms"] / wall, 4),
+                             "pin": round(prof["pin_ms"] / wall, 4), "gpu": round(prof["gpu_ms"] / wall, 4)},
+               "probe_GBps": {k: round(v / 1e9, 2) for k, v in pr.items()}}
+        rows.append(row)
+        log("table 2, %s weights: alpha %.4f (closed form %.4f), %.2f ms per call, busy %s" %
+            (kind, a1, a0, ts[len(ts) // 2], row["busy_frac"]))
+    print(json.dumps({
+        "metric": "per-resource busy fraction of one heterogeneous linear (Table 2 analogue)",
+        "value": rows[-1]["busy_frac"]["cpu"], "unit": "fraction of the linear's wall time", "n_gpus": 1,
+        "steps": args.table2_reps, "warmup": 3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic: seeded N(0,0.02) weights and bias, N(0,1) x",
+        "config": {"workload": "one heterogeneous linear [%d,%d] fp16 (OPT-13B fc1 shape), batch %d, planner alpha "
+                               "refined by the alpha benchmark; weights pinned, then pageable; %d weight copies "
+                               "rotated" % (N, K, B, ncopy)},
+        "results": rows, "paper_table2": {"cpu": 0.978, "io": 0.969, "pin": 0.724, "gpu": 0.001},
+        "host": host_info(torch)}), flush=True)
+    for w in Wp:
+        hg.hetegen_host_free(ctx, w)
+    hg.hetegen_host_free(ctx, bh)
+    hg.hetegen_destroy(ctx)
+
+
 def mfma_splits(K):
     """Splits of the sum over K in the matrix-core GEMV (the library's rule)."""
     kt, g = (K + 31) // 32, 1
@@ -326,6 +417,10 @@ def main():
                          "CPU fractions 0, .25, .5, 1, resident and streamed, over --linear-reps calls that rotate "
                          "weight copies totalling > 512 MB (prints its own JSON line)")
     ap.add_argument("--linear-reps", type=int, default=200)
+    ap.add_argument("--table2", default=None, metavar="NxK",
+                    help="instead of a decode step: busy fractions of one heterogeneous linear (Table 2 analogue; "
+                         "OPT-13B fc1 is 20480x5120), pinned and pageable weights (prints its own JSON line)")
+    ap.add_argument("--table2-reps", type=int, default=20)
     ap.add_argument("--no-streamed", action="store_true",
                     help="default run only: skip the streamed leg (OPT-30B shapes, every linear in pinned host "
                          "memory, planner alpha refined by the step-level benchmark, batch 1)")
@@ -348,6 +443,9 @@ def main():
     torch.cuda.set_device(0)
     if args.linear:
         single_linear(args, torch, synth, hg)
+        return
+    if args.table2:
+        table2_linear(args, torch, synth, hg)
         return
     default_run = args.model is None
     if default_run:
