@@ -447,8 +447,10 @@ def main():
     if args.table2:
         table2_linear(args, torch, synth, hg)
         return
-    default_run = args.model is None
-    if default_run:
+    # the streamed leg belongs to the default line: no workload option given
+    default_run = (args.model is None and args.batch == 1 and not args.layers and args.placement is None and
+                   args.context == 0 and not args.pageable and args.alpha is None)
+    if args.model is None:
         args.model = "opt-6.7b"
     result = decode_workload(args, torch, synth, hg)
     if default_run and not args.no_streamed:
