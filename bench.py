@@ -346,11 +346,11 @@ def mfma_splits(K):
     return g
 
 
-def gemv_label(B, H, F, dt):
+def gemv_label(B, H, F, dt, tiled):
     """GEMV kernels an all-resident eager step at batch B runs (the library's dispatch rules;
-    the bench creates its model for batch B, so B >= 5 means tile-ordered weights)."""
+    tiled: the model was created for batches of 3 or more, so its weights are in tile order)."""
     t = "BF16" if dt == 1 else "F16"
-    if B >= 5:
+    if tiled:
         parts = {}
         for name, (n, k) in zip(NAMES, shapes(H, F)):
             g = mfma_splits(k)
@@ -378,6 +378,9 @@ def main():
                     help="one workload (default: the OPT-6.7B all-resident line, followed by the streamed leg "
                          "below unless --no-streamed)")
     ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--max-batch", type=int, default=0,
+                    help="largest batch the model is created for (0: --batch); from 3 on its resident weights "
+                         "are kept in matrix-core tile order, also for smaller batches")
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N decoder layers (0: all); reported in config")
     ap.add_argument("--placement", choices=("all", "half", "none", "sched"), default=None,
@@ -580,7 +583,8 @@ def decode_workload(args, torch, synth, hg):
         alpha = [0.0 if resident[i] else args.alpha for i in range(4 * L)]
     alpha_closed = list(alpha)
     t0 = time.time()
-    model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, resident, max(B, 1))
+    max_batch = max(B, args.max_batch, 1)
+    model = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, alpha, resident, max_batch)
     log("model ready in %.1f s (resident modules %d of %d)" % (time.time() - t0, sum(resident), 4 * L))
     if args.exec != "auto" and not streamed:
         hg.hetegen_model_set_exec(model, {"persistent": hg.EXEC_PERSISTENT, "graph": hg.EXEC_GRAPH,
@@ -679,7 +683,8 @@ def decode_workload(args, torch, synth, hg):
         "config": {"workload": "%s-shaped decode step, %d layers x {qkv,out,fc1,fc2}, %s, batch %d" %
                                (args.model.upper(), L, desc, B) +
                                ("" if L == L_full else " (first %d of the model's %d layers)" % (L, L_full)),
-                   "layers": L, "hidden": H, "ffn": F, "batch": B, "weight_bytes_per_step": wbytes,
+                   "layers": L, "hidden": H, "ffn": F, "batch": B, "max_batch": max_batch,
+                   "weight_bytes_per_step": wbytes,
                    "resident_layers": res_layers, "resident_modules": sum(resident),
                    "parallelism": "single GPU"},
     }
@@ -716,7 +721,7 @@ def decode_workload(args, torch, synth, hg):
         log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
             (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
         kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
-            else gemv_label(B, H, F, dt)
+            else gemv_label(B, H, F, dt, max_batch >= 3)
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
         read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
@@ -736,7 +741,7 @@ def decode_workload(args, torch, synth, hg):
                               "frac_of_achievable": round(achieved / read_gbps, 4),
                               "read_same_launches_ms": round(read_step_ms, 5),
                               "frac_of_read_same_launches": round(read_step_ms / ms_step, 4)}
-        if B >= 5 and exec_mode != "persistent":
+        if max_batch >= 3 and exec_mode != "persistent":
             # the timed region also holds the LayerNorm launches before qkv and fc1 (B x H x 2
             # bytes read and written each); they are not in launches_per_step or bytes_per_launch,
             # so `achieved` understates the GEMV's own rate by their share of the step

@@ -135,7 +135,7 @@ HETEGEN_API hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, i
  * and columns past K are zero.  One tile is the 16-row operand of one 16x16x32
  * matrix-core product, so the GEMV reads every tile with one coalesced 1 KiB load
  * and runs on the matrix cores at every batch size (decode steps of models created
- * for batches of 5 or more keep their resident rows in this order). */
+ * for batches of 3 or more keep their resident rows in this order). */
 
 /* Bytes of the tile-ordered copy of a [rows, K] weight (0 for rows < 1 or K not a
  * positive multiple of 8). */
@@ -317,7 +317,7 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * otherwise they are streamed every step.  max_batch in [1, 8]; H, F multiples
  * of 8, H <= 16384 (UNSUPPORTED above: the LayerNorm keeps a row in registers; the
  * largest OPT hidden size is 12288).  With max_batch
- * >= 5 the resident rows are stored in matrix-core tile order and run on the
+ * >= 3 the resident rows are stored in matrix-core tile order and run on the
  * matrix-core GEMV at every batch size (see hetegen_linear_tiled; the model then
  * also owns its split-K workspace); below 5 they stay row-major and run on the
  * vector GEMV, whose fused LayerNorm is faster at batches 1-4. */
@@ -352,7 +352,7 @@ HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* 
 #define HETEGEN_EXEC_EAGER 3
 
 /* Select the execution mode (UNSUPPORTED when a forced mode cannot run this
- * model; PERSISTENT needs row-major resident weights, i.e. max_batch < 5).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
+ * model; PERSISTENT needs row-major resident weights, i.e. max_batch < 3).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
  * persistent mode (0: the default, seconds of waiting); a wait that gives up lets
  * the step finish with undefined outputs and makes the next hetegen_decode_step
  * on the model fail with HETEGEN_ERR_HIP.  A small limit exists to test that path. */

@@ -63,11 +63,12 @@ constexpr size_t kCounterBytes = 256;
 constexpr int kDefaultRing = 8;
 constexpr int kMaxBatch = 8;
 // Models created for batches of kTiledMinBatch or more keep their resident rows in the
-// matrix-core tile order and run them on the matrix-core GEMV at every batch size: from
-// batch 5 on the vector GEMV is bound by its dot products and LDS reads of x (OPT-6.7B
-// shapes at batch 8: 24-41 us per linear against 8-24 us on the matrix cores), while at
-// batch 1-4 the vector kernels with their fused LayerNorm are as fast or faster.
-constexpr int kTiledMinBatch = 5;
+// matrix-core tile order and run them on the matrix-core GEMV at every batch size: the
+// vector GEMV's dot products and LDS reads of x grow with the batch (OPT-6.7B-shaped
+// steps: 2.74 / 2.95 / 3.95 ms at batch 3 / 4 / 8 against 2.56 / 2.57 / 2.67 ms on the
+// matrix cores), while at batches 1-2 the vector kernels with their fused LayerNorm are
+// faster (2.19 / 2.45 against 2.57 / 2.55 ms).
+constexpr int kTiledMinBatch = 3;
 constexpr int kDefaultPinThreads = 4;
 constexpr int kDefaultPinRing = 4;
 

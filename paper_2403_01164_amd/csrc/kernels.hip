@@ -1222,17 +1222,13 @@ hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long
   }
 }
 
+// The persistent step runs row-major models, i.e. models created for batches of 1 or 2
+// (larger ones keep their weights in matrix-core tile order).
 template <class T>
 const void* step_fn(int B) {
   switch (B) {
     case 1: return (const void*)step_kernel<T, 1, Tile<1>::R, Tile<1>::U>;
     case 2: return (const void*)step_kernel<T, 2, Tile<2>::R, Tile<2>::U>;
-    case 3: return (const void*)step_kernel<T, 3, Tile<3>::R, Tile<3>::U>;
-    case 4: return (const void*)step_kernel<T, 4, Tile<4>::R, Tile<4>::U>;
-    case 5: return (const void*)step_kernel<T, 5, Tile<5>::R, Tile<5>::U>;
-    case 6: return (const void*)step_kernel<T, 6, Tile<6>::R, Tile<6>::U>;
-    case 7: return (const void*)step_kernel<T, 7, Tile<7>::R, Tile<7>::U>;
-    case 8: return (const void*)step_kernel<T, 8, Tile<8>::R, Tile<8>::U>;
   }
   return nullptr;
 }

@@ -146,14 +146,14 @@ def test_opt13b_shape_one_layer_hetero(ctx):
 
 
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
-@pytest.mark.parametrize("B,max_batch", [(1, 1), (2, 4), (4, 4), (1, 8), (5, 8), (8, 8)])
+@pytest.mark.parametrize("B,max_batch", [(1, 1), (1, 2), (2, 2), (2, 4), (4, 4), (1, 8), (5, 8), (8, 8)])
 def test_exec_modes_bit_identical(ctx, dtype, B, max_batch):
     # persistent (one cooperative launch, grid barriers), graph replay and eager
-    # per-linear launches compute every output row the same way; models for batches of 5
+    # per-linear launches compute every output row the same way; models for batches of 3
     # or more (weights in matrix-core tile order) have no persistent mode
     L, H, F = 3, 512, 2048
     m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=max_batch)
-    tiled = max_batch >= 5
+    tiled = max_batch >= 3
     try:
         xs = [synth.normal((B, H), dtype, 0, synth.act_id(t)) for t in range(3)]
         outs = {}
