@@ -348,7 +348,7 @@ def mfma_splits(K):
 
 def gemv_label(B, H, F, dt, tiled):
     """GEMV kernels an all-resident eager step at batch B runs (the library's dispatch rules;
-    tiled: the model was created for batches of 3 or more, so its weights are in tile order)."""
+    tiled: the step runs the tile-ordered copy of the weights)."""
     t = "BF16" if dt == 1 else "F16"
     if tiled:
         parts = {}
@@ -720,8 +720,10 @@ def decode_workload(args, torch, synth, hg):
         achieved = bytes_per_launch / (avg_us * 1e-6) / 1e9
         log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
             (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
+        layouts = hg.hetegen_model_layouts(model)
+        tiled_used = bool(layouts & hg.LAYOUT_TILED) and (B >= 3 or not layouts & hg.LAYOUT_ROWMAJOR)
         kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
-            else gemv_label(B, H, F, dt, max_batch >= 3)
+            else gemv_label(B, H, F, dt, tiled_used)
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
         read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
@@ -741,7 +743,9 @@ def decode_workload(args, torch, synth, hg):
                               "frac_of_achievable": round(achieved / read_gbps, 4),
                               "read_same_launches_ms": round(read_step_ms, 5),
                               "frac_of_read_same_launches": round(read_step_ms / ms_step, 4)}
-        if max_batch >= 3 and exec_mode != "persistent":
+        result["config"]["weight_layouts"] = "+".join(n for f, n in ((hg.LAYOUT_ROWMAJOR, "row-major"),
+                                                                    (hg.LAYOUT_TILED, "tiled")) if layouts & f)
+        if tiled_used and exec_mode != "persistent":
             # the timed region also holds the LayerNorm launches before qkv and fc1 (B x H x 2
             # bytes read and written each); they are not in launches_per_step or bytes_per_launch,
             # so `achieved` understates the GEMV's own rate by their share of the step

@@ -316,11 +316,16 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * resident[i] != 0: rows [0, n_gpu) of linear i are copied to HBM at creation;
  * otherwise they are streamed every step.  max_batch in [1, 8]; H, F multiples
  * of 8, H <= 16384 (UNSUPPORTED above: the LayerNorm keeps a row in registers; the
- * largest OPT hidden size is 12288).  With max_batch
- * >= 3 the resident rows are stored in matrix-core tile order and run on the
- * matrix-core GEMV at every batch size (see hetegen_linear_tiled; the model then
- * also owns its split-K workspace); below 5 they stay row-major and run on the
- * vector GEMV, whose fused LayerNorm is faster at batches 1-4. */
+ * largest OPT hidden size is 12288).  Layout of the resident rows: with max_batch
+ * < 3 they are row-major and run on the vector GEMV (fused LayerNorm, the faster
+ * kernels at batches 1-2); with max_batch >= 3 they are stored in matrix-core tile
+ * order and batches of 3 and more run on the matrix-core GEMV (see
+ * hetegen_linear_tiled; the model also owns its split-K workspace).  Such a model
+ * also keeps the row-major copy, and runs batches 1-2 from it, when both copies
+ * take at most half of the device memory free at creation (the environment
+ * variable HETEGEN_DUAL_LAYOUT=0 at creation keeps the tile order only);
+ * hetegen_model_layouts tells which copies a model holds.  Results do not depend
+ * on the layout beyond rounding (both pass the oracle's tolerance). */
 HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
                                     void* const* W_host, void* const* bias_host, const double* alpha,
                                     const int* resident, int max_batch, hetegen_model** out);
@@ -352,7 +357,8 @@ HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* 
 #define HETEGEN_EXEC_EAGER 3
 
 /* Select the execution mode (UNSUPPORTED when a forced mode cannot run this
- * model; PERSISTENT needs row-major resident weights, i.e. max_batch < 3).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
+ * model; PERSISTENT needs the row-major copy of the resident rows and runs batches
+ * 1-2 only).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
  * persistent mode (0: the default, seconds of waiting); a wait that gives up lets
  * the step finish with undefined outputs and makes the next hetegen_decode_step
  * on the model fail with HETEGEN_ERR_HIP.  A small limit exists to test that path. */
@@ -360,6 +366,13 @@ HETEGEN_API hetegen_status hetegen_model_set_exec(hetegen_model* model, int mode
 
 /* Mode the last hetegen_decode_step on the model used (HETEGEN_EXEC_*), or -1. */
 HETEGEN_API int hetegen_model_last_exec(const hetegen_model* model);
+
+/* Layouts of the model's resident rows (see hetegen_model_create): a bitwise OR of
+ * HETEGEN_LAYOUT_ROWMAJOR and HETEGEN_LAYOUT_TILED (0 for NULL or no resident rows
+ * kept in either). */
+#define HETEGEN_LAYOUT_ROWMAJOR 1
+#define HETEGEN_LAYOUT_TILED 2
+HETEGEN_API int hetegen_model_layouts(const hetegen_model* model);
 
 /* Alpha benchmark at the granularity of the decode step (Sec. 4.4 applied to the
  * chain of modules).  The call shifts the CPU fraction of every streamed linear by

@@ -97,6 +97,7 @@ _SIGS = {
     "hetegen_module_schedule": ([ctypes.POINTER(_d), ctypes.POINTER(_d), ctypes.POINTER(_i), _i, _d,
                                  ctypes.POINTER(_i), ctypes.POINTER(_d)], _i),
     "hetegen_model_last_exec": ([_vp], _i),
+    "hetegen_model_layouts": ([_vp], _i),
     "hetegen_decode_step": ([_vp, _vp, _vp, _vp, _i, _vp], _i),
     "hetegen_model_trace_bytes": ([_vp, _i], _sz),
     "hetegen_model_set_trace": ([_vp, _vp, _sz], _i),
@@ -324,6 +325,14 @@ def hetegen_model_set_exec(model, mode, barrier_spin_limit=0):
 
 def hetegen_model_last_exec(model):
     return _lib.hetegen_model_last_exec(model)
+
+
+LAYOUT_ROWMAJOR, LAYOUT_TILED = 1, 2
+
+
+def hetegen_model_layouts(model):
+    """Bitmask of the layouts the model keeps its resident rows in (LAYOUT_ROWMAJOR, LAYOUT_TILED)."""
+    return _lib.hetegen_model_layouts(model)
 
 
 def hetegen_decode_step(ctx, model, x_dev, out_dev, B, stream=0):

@@ -146,11 +146,14 @@ struct hetegen_model {
     int resident = 0;
     int n_gpu = 0, n_cpu = 0;
     bool pageable = false;     // W_host is plain host memory (staged when streamed)
-    void* W_dev = nullptr;     // rows [0, n_gpu) when resident
+    void* W_dev = nullptr;     // rows [0, n_gpu) when resident, row-major (batches 1-2 and row-major models)
+    void* W_tile = nullptr;    // the same rows in matrix-core tile order (tiled models)
     void* bias_dev = nullptr;  // all N biases
   };
   int L = 0, H = 0, F = 0, dtype = 0, max_batch = 1;
   bool tiled = false;          // resident rows in matrix-core tile order (max_batch >= kTiledMinBatch)
+  bool rowmajor = true;        // resident rows row-major (all models below kTiledMinBatch; tiled ones when
+                               // both copies fit, see hetegen_model_create)
   float* ws = nullptr;         // split-K partials of the matrix-core GEMV
   uint32_t* ws_cnt = nullptr;  // its arrival counters, zero between launches
   std::vector<Lin> lin;
@@ -1694,9 +1697,9 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
   // ahead across linears and layers, bounded by the ring
   if (!pipeline_idle(ctx)) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "internal: stale chunk plan");
   for (const auto& l : m->lin)
-    if (!l.W_dev && l.n_gpu > 0 && l.pageable) TRY(ensure_pin_resources(ctx));
+    if (!l.resident && l.n_gpu > 0 && l.pageable) TRY(ensure_pin_resources(ctx));
   for (const auto& l : m->lin)
-    if (!l.W_dev && l.n_gpu > 0) plan_chunks(ctx, l.W_host, l.n_gpu, l.K, m->dtype, l.pageable, l.n_cpu == 0);
+    if (!l.resident && l.n_gpu > 0) plan_chunks(ctx, l.W_host, l.n_gpu, l.K, m->dtype, l.pageable, l.n_cpu == 0);
   char* tr = (char*)m->trace;
   auto take = [&](size_t elems) -> void* {
     if (!tr) return nullptr;
@@ -1714,12 +1717,14 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
       j.N = lin.N;
       j.dtype = m->dtype;
       j.W_host = lin.W_host;
-      j.W_dev = lin.W_dev;
+      // resident rows: the tile-ordered copy from kTiledMinBatch on (or when it is the only one)
+      const bool use_tile = lin.W_tile && (B >= kTiledMinBatch || !lin.W_dev);
+      j.W_dev = use_tile ? lin.W_tile : lin.W_dev;
       j.bias_host = lin.bias_host;
       j.bias_dev = lin.bias_dev;
       j.n_gpu = lin.n_gpu;
       j.n_cpu = lin.n_cpu;
-      j.tiled = m->tiled && lin.W_dev;
+      j.tiled = use_tile;
       j.ws = m->ws;
       j.cnt = m->ws_cnt;
       j.ln_buf = m->lnbuf;
@@ -1766,7 +1771,7 @@ hetegen_status build_plan(hetegen_ctx* ctx, hetegen_model* m, int B) {
   auto& pl = m->plan[B];
   pl.built = true;
   pl.ok = false;
-  if (!m->graphable || m->tiled) return HETEGEN_OK;  // the persistent step reads row-major weights
+  if (!m->graphable || !m->rowmajor || B >= kTiledMinBatch) return HETEGEN_OK;  // reads row-major weights
   int ncu = 0, coop = 0;
   HIPCHK(ctx, hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, ctx->device));
   HIPCHK(ctx, hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, ctx->device));
@@ -1884,9 +1889,10 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     m->dtype = dtype;
     m->max_batch = max_batch;
     m->tiled = max_batch >= kTiledMinBatch;
+    m->rowmajor = !m->tiled;
     m->lin.resize((size_t)4 * L);
     m->lin_ms.assign((size_t)4 * L, 0.0);
-    size_t dev_bytes = 0;
+    size_t dev_bytes = 0, rm_bytes = 0, tile_bytes = 0;
     for (int i = 0; i < 4 * L; ++i) {
       auto& l = m->lin[i];
       const int which = i % 4;
@@ -1911,9 +1917,24 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       }
       l.n_cpu = split_cpu_rows(l.N, l.alpha);
       l.n_gpu = l.N - l.n_cpu;
-      if (l.resident) dev_bytes += align256(m->tiled ? hg::tiled_bytes(l.n_gpu, l.K) : (size_t)l.n_gpu * l.K * 2);
+      if (l.resident) {
+        rm_bytes += align256((size_t)l.n_gpu * l.K * 2);
+        tile_bytes += align256(hg::tiled_bytes(l.n_gpu, l.K));
+      }
       if (l.bias_host) dev_bytes += align256((size_t)l.N * 2);
     }
+    // A tiled model also keeps the row-major copy, for batches 1-2 on the vector GEMV, when
+    // both copies take at most half of the device memory free now (HETEGEN_DUAL_LAYOUT=0 at
+    // creation: tile order only)
+    if (m->tiled && rm_bytes) {
+      size_t free_b = 0, total_b = 0;
+      const char* de = getenv("HETEGEN_DUAL_LAYOUT");
+      const bool allow = !(de && strcmp(de, "0") == 0);
+      if (allow && hipMemGetInfo(&free_b, &total_b) == hipSuccess && rm_bytes + tile_bytes <= free_b / 2)
+        m->rowmajor = true;
+      (void)hipGetLastError();
+    }
+    dev_bytes += (m->rowmajor ? rm_bytes : 0) + (m->tiled ? tile_bytes : 0);
     if (dev_bytes && hipMalloc(&m->arena, dev_bytes) != hipSuccess) {
       (void)hipGetLastError();
       model_free(m);
@@ -1931,7 +1952,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
           ws_floats = std::max(ws_floats, hg::mfma_ws_floats(l.n_gpu, l.K, max_batch));
           ws_words = std::max(ws_words, hg::mfma_cnt_words(l.n_gpu, l.K));
         }
-      if ((most && hipMalloc(&stage, most) != hipSuccess) ||
+      if ((most && !m->rowmajor && hipMalloc(&stage, most) != hipSuccess) ||
           (ws_floats && hipMalloc((void**)&m->ws, ws_floats * 4) != hipSuccess) ||
           (ws_words && hipMalloc((void**)&m->ws_cnt, ws_words * 4) != hipSuccess)) {
         (void)hipGetLastError();
@@ -1948,21 +1969,31 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     char* p = (char*)m->arena;
     for (auto& l : m->lin) {
       if (l.resident) {
-        l.W_dev = p;
+        // the row-major copy (when kept) is uploaded first and is also the tiling's source;
+        // otherwise the rows pass through the staging buffer
         const size_t rb = (size_t)l.n_gpu * l.K * 2;
         bool ok = true;
-        if (l.n_gpu > 0 && !m->tiled) ok = hipMemcpy(p, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess;
-        if (l.n_gpu > 0 && m->tiled)
-          ok = hipMemcpy(stage, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess &&
-               hg::launch_tile(stage, l.K, l.n_gpu, l.K, p, nullptr) == hipSuccess &&
-               hipDeviceSynchronize() == hipSuccess;
+        void* src = stage;
+        if (m->rowmajor) {
+          l.W_dev = p;
+          src = p;
+          p += align256(rb);
+          if (l.n_gpu > 0) ok = hipMemcpy(l.W_dev, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess;
+        }
+        if (m->tiled) {
+          l.W_tile = p;
+          p += align256(hg::tiled_bytes(l.n_gpu, l.K));
+          if (ok && l.n_gpu > 0)
+            ok = (m->rowmajor || hipMemcpy(stage, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess) &&
+                 hg::launch_tile(src, l.K, l.n_gpu, l.K, l.W_tile, nullptr) == hipSuccess &&
+                 hipDeviceSynchronize() == hipSuccess;
+        }
         if (!ok) {
           (void)hipGetLastError();
           if (stage) (void)hipFree(stage);
           model_free(m);
           return fail(ctx, HETEGEN_ERR_HIP, "resident upload failed");
         }
-        p += align256(m->tiled ? hg::tiled_bytes(l.n_gpu, l.K) : rb);
       }
       if (l.bias_host) {
         l.bias_dev = p;
@@ -2000,7 +2031,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     }
     m->graphable = true;
     for (const auto& l : m->lin)
-      if (l.n_cpu > 0 || !l.W_dev) m->graphable = false;
+      if (l.n_cpu > 0 || !l.resident) m->graphable = false;
     if (m->graphable) {
       m->ngroups = kBarrierGroups;
       const size_t cb = (size_t)(m->ngroups + 1) * kCounterBytes;
@@ -2026,7 +2057,7 @@ hetegen_status hetegen_model_set_exec(hetegen_model* m, int mode, uint32_t barri
     if (!m || mode < HETEGEN_EXEC_AUTO || mode > HETEGEN_EXEC_EAGER) return HETEGEN_ERR_INVALID_ARG;
     if ((mode == HETEGEN_EXEC_PERSISTENT || mode == HETEGEN_EXEC_GRAPH) && !m->graphable)
       return HETEGEN_ERR_UNSUPPORTED;
-    if (mode == HETEGEN_EXEC_PERSISTENT && m->tiled) return HETEGEN_ERR_UNSUPPORTED;
+    if (mode == HETEGEN_EXEC_PERSISTENT && !m->rowmajor) return HETEGEN_ERR_UNSUPPORTED;
     m->exec_mode = mode;
     m->spin_limit = barrier_spin_limit;
     return HETEGEN_OK;
@@ -2034,6 +2065,10 @@ hetegen_status hetegen_model_set_exec(hetegen_model* m, int mode, uint32_t barri
 }
 
 int hetegen_model_last_exec(const hetegen_model* m) { return m ? m->last_exec : -1; }
+
+int hetegen_model_layouts(const hetegen_model* m) {
+  return m ? (m->rowmajor ? HETEGEN_LAYOUT_ROWMAJOR : 0) | (m->tiled ? HETEGEN_LAYOUT_TILED : 0) : 0;
+}
 
 hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {
   return api_guard(nullptr, [&]() -> hetegen_status {
@@ -2067,7 +2102,7 @@ hetegen_status hetegen_model_read_ms(hetegen_ctx* ctx, const hetegen_model* m, i
     if (!m || !ms_out || reps < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: bad arguments");
     std::vector<std::pair<const void*, size_t>> bufs;
     for (const auto& l : m->lin)
-      if (l.resident && l.n_gpu > 0 && l.W_dev) bufs.emplace_back(l.W_dev, (size_t)l.n_gpu * l.K * 2);
+      if (l.resident && l.n_gpu > 0) bufs.emplace_back(l.W_dev ? l.W_dev : l.W_tile, (size_t)l.n_gpu * l.K * 2);
     if (bufs.empty()) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_model_read_ms: no resident GPU rows");
     HIPCHK(ctx, hipSetDevice(ctx->device));
     hipStream_t st = stream ? (hipStream_t)stream : ctx->capture_stream;

@@ -145,24 +145,44 @@ def test_opt13b_shape_one_layer_hetero(ctx):
         m.free()
 
 
+def _model_with_env(ctx, env, *args, **kw):
+    import os
+    old = {k: os.environ.get(k) for k in env}
+    os.environ.update(env)
+    try:
+        return Model(ctx, *args, **kw)
+    finally:
+        for k, v in old.items():
+            if v is None:
+                del os.environ[k]
+            else:
+                os.environ[k] = v
+
+
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
-@pytest.mark.parametrize("B,max_batch", [(1, 1), (1, 2), (2, 2), (2, 4), (4, 4), (1, 8), (5, 8), (8, 8)])
-def test_exec_modes_bit_identical(ctx, dtype, B, max_batch):
+@pytest.mark.parametrize("B,max_batch,dual", [(1, 1, True), (1, 2, True), (2, 2, True), (2, 4, True), (4, 4, True),
+                                              (1, 8, True), (1, 8, False), (5, 8, True), (8, 8, False)])
+def test_exec_modes_bit_identical(ctx, dtype, B, max_batch, dual):
     # persistent (one cooperative launch, grid barriers), graph replay and eager
-    # per-linear launches compute every output row the same way; models for batches of 3
-    # or more (weights in matrix-core tile order) have no persistent mode
+    # per-linear launches compute every output row the same way; the persistent step runs
+    # the row-major copy at batches 1-2 only (models for batches of 3 or more keep it
+    # beside the tile order when memory allows, HETEGEN_DUAL_LAYOUT=0 keeps tiles only)
     L, H, F = 3, 512, 2048
-    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=max_batch)
-    tiled = max_batch >= 3
+    m = _model_with_env(ctx, {} if dual else {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1,
+                        max_batch=max_batch)
+    layouts = hg.hetegen_model_layouts(m.m)
+    assert layouts == (hg.LAYOUT_ROWMAJOR if max_batch < 3 else
+                       hg.LAYOUT_TILED | (hg.LAYOUT_ROWMAJOR if dual else 0))
     try:
         xs = [synth.normal((B, H), dtype, 0, synth.act_id(t)) for t in range(3)]
         outs = {}
-        if tiled:
+        if not layouts & hg.LAYOUT_ROWMAJOR:
             with pytest.raises(hg.HetegenError) as e:
                 hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT)
             assert e.value.status == hg.ERR_UNSUPPORTED
-        modes = (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_AUTO) if tiled else \
-            (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT, hg.EXEC_AUTO)
+        persistent = bool(layouts & hg.LAYOUT_ROWMAJOR) and B <= 2
+        modes = (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT, hg.EXEC_AUTO) if persistent else \
+            (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_AUTO)
         for mode in modes:
             hg.hetegen_model_set_exec(m.m, mode)
             outs[mode] = [m.step(x) for x in xs] + [m.step(xs[0])]
@@ -177,6 +197,39 @@ def test_exec_modes_bit_identical(ctx, dtype, B, max_batch):
         assert np.array_equal(outs[modes[-2]][1], last)
     finally:
         m.free()
+
+
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+def test_dual_layout_runs_each_batch_on_the_matching_copy(ctx, dtype):
+    # a model for batches up to 8 with both copies gives, at batches 1-2, the bits of a
+    # row-major model and, from batch 3, the bits of a tile-only model (same weights)
+    L, H, F = 2, 1024, 8192
+    rm = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=2)
+    try:
+        dual = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=8, weights=(rm.W, rm.b))
+        tiles = _model_with_env(ctx, {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1, max_batch=8,
+                                weights=(rm.W, rm.b))
+        try:
+            assert hg.hetegen_model_layouts(rm.m) == hg.LAYOUT_ROWMAJOR
+            assert hg.hetegen_model_layouts(dual.m) == hg.LAYOUT_ROWMAJOR | hg.LAYOUT_TILED
+            assert hg.hetegen_model_layouts(tiles.m) == hg.LAYOUT_TILED
+            for B in (1, 2, 3, 8):
+                x = synth.normal((B, H), dtype, 0, synth.act_id(10 + B))
+                want = (rm if B <= 2 else tiles).step(x)
+                out, tr = dual.step(x, trace=True)
+                assert np.array_equal(out, want), B
+                last, _ = dual.check_teacher_forced(x, tr)
+                assert np.array_equal(out, last)
+            # the tile-only model at batch 1 (matrix-core GEMV) passes teacher-forced too
+            x = synth.normal((1, H), dtype, 0, synth.act_id(20))
+            out, tr = tiles.step(x, trace=True)
+            last, _ = tiles.check_teacher_forced(x, tr)
+            assert np.array_equal(out, last)
+        finally:
+            tiles.free()
+            dual.free()
+    finally:
+        rm.free()
 
 
 def test_persistent_opt67b_shapes_two_layers(ctx):
