@@ -346,20 +346,35 @@ def mfma_splits(K):
     return g
 
 
-def gemv_label(B, H, F, dt, tiled):
+def ln_partials_on():
+    """Whether tiled models normalise the inputs of qkv (after layer 0) and fc1 from the
+    LayerNorm partials of the out / fc2 before them (the library default)."""
+    return os.environ.get("HETEGEN_LN_PARTIALS") != "0"
+
+
+def gemv_label(B, H, F, dt, tiled, partials=True):
     """GEMV kernels an all-resident eager step at batch B runs (the library's dispatch rules;
-    tiled: the step runs the tile-ordered copy of the weights)."""
+    tiled: the step runs the tile-ordered copy of the weights; partials: with LayerNorm
+    partials between its matrix-core linears)."""
     t = "BF16" if dt == 1 else "F16"
     if tiled:
         parts = {}
         for name, (n, k) in zip(NAMES, shapes(H, F)):
             g = mfma_splits(k)
-            key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, 8 if g == 1 else 4, "" if g == 1 else " (K split %d)" % g)
+            split = "" if g == 1 else " (K split %d)" % g
+            if partials and name in ("qkv", "fc1"):
+                key = "gemv_mfma_kernel<%s,%d,4,LayerNorm from partials>%s" % (t, B, split)
+                parts.setdefault(key, []).append("qkv after layer 0" if name == "qkv" else name)
+                if name == "qkv":
+                    key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, 8 if g == 1 else 4, split)
+                    parts.setdefault(key, []).append("layer 0's qkv")
+                continue
+            key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, 8 if g == 1 else 4, split)
             parts.setdefault(key, []).append(name)
         ni = -(-H // 2048)
         ni = ni if ni <= 5 else 8
         return " + ".join("%s: %s" % (k, ", ".join(v)) for k, v in parts.items()) + \
-            " + layernorm_regs_kernel<%s,%d> before qkv and fc1" % (t, ni)
+            " + layernorm_regs_kernel<%s,%d> before %s" % (t, ni, "layer 0's qkv" if partials else "qkv and fc1")
     if B == 1:
         if H % 512 == 0 and H // 512 in (1, 2, 4, 5, 8, 10, 14):
             return "gemv_ln1_kernel<%s,%d> (qkv, fc1) + gemv_x1_kernel<%s,4,1> (out, fc2)" % (t, H // 512, t)
@@ -723,7 +738,7 @@ def decode_workload(args, torch, synth, hg):
         layouts = hg.hetegen_model_layouts(model)
         tiled_used = bool(layouts & hg.LAYOUT_TILED) and (B >= 3 or not layouts & hg.LAYOUT_ROWMAJOR)
         kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
-            else gemv_label(B, H, F, dt, tiled_used)
+            else gemv_label(B, H, F, dt, tiled_used, ln_partials_on())
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
         read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
@@ -746,11 +761,13 @@ def decode_workload(args, torch, synth, hg):
         result["config"]["weight_layouts"] = "+".join(n for f, n in ((hg.LAYOUT_ROWMAJOR, "row-major"),
                                                                     (hg.LAYOUT_TILED, "tiled")) if layouts & f)
         if tiled_used and exec_mode != "persistent":
-            # the timed region also holds the LayerNorm launches before qkv and fc1 (B x H x 2
-            # bytes read and written each); they are not in launches_per_step or bytes_per_launch,
-            # so `achieved` understates the GEMV's own rate by their share of the step
-            result["roofline"]["region_also_holds"] = "%d layernorm_regs_kernel launches per step (%d bytes each)" % (
-                2 * L, B * H * 4)
+            # the timed region also holds the LayerNorm launches (B x H x 2 bytes read and written
+            # each): before layer 0's qkv, or before every qkv and fc1 without the partials; they
+            # are not in launches_per_step or bytes_per_launch, so `achieved` understates the
+            # GEMV's own rate by their share of the step
+            n_ln = 1 if ln_partials_on() else 2 * L
+            result["roofline"]["region_also_holds"] = "%d layernorm_regs_kernel launch%s per step (%d bytes each)" % (
+                n_ln, "" if n_ln == 1 else "es", B * H * 4)
     elif streamed:
         # heterogeneous figures: link and CPU rates, the ideal rate of Eq. 4, busy fractions
         sb = sum(shp[i][0] * shp[i][1] * 2 for i in streamed)

@@ -324,8 +324,14 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * also keeps the row-major copy, and runs batches 1-2 from it, when both copies
  * take at most half of the device memory free at creation (the environment
  * variable HETEGEN_DUAL_LAYOUT=0 at creation keeps the tile order only);
- * hetegen_model_layouts tells which copies a model holds.  Results do not depend
- * on the layout beyond rounding (both pass the oracle's tolerance). */
+ * hetegen_model_layouts tells which copies a model holds.  On the matrix-core path,
+ * when out (fc2) and the fc1 (next qkv) after it run every row on the GPU, out / fc2
+ * also leave per-16-element LayerNorm partials of their output (sum, sum of squared
+ * deviations), and fc1 / qkv normalise their input from them instead of after a
+ * LayerNorm launch (Chan-Golub-LeVeque combination in a fixed order; the variable
+ * HETEGEN_LN_PARTIALS=0 at creation keeps the LayerNorm launches).  Results do not
+ * depend on the layout or the LayerNorm path beyond rounding (all pass the oracle's
+ * tolerance). */
 HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
                                     void* const* W_host, void* const* bias_host, const double* alpha,
                                     const int* resident, int max_batch, hetegen_model** out);

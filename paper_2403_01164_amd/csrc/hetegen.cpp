@@ -156,6 +156,9 @@ struct hetegen_model {
                                // both copies fit, see hetegen_model_create)
   float* ws = nullptr;         // split-K partials of the matrix-core GEMV
   uint32_t* ws_cnt = nullptr;  // its arrival counters, zero between launches
+  float* ln_part = nullptr;    // LayerNorm partials of x after out / fc2 (two buffers of
+                               // ln_partials_floats(H)), for the tiled GEMVs of fc1 / qkv
+  bool ln_partials = true;     // use them (HETEGEN_LN_PARTIALS=0 at creation: LayerNorm launches)
   std::vector<Lin> lin;
   std::vector<double> lin_ms;  // host time of each linear in the last eager step
   void* arena = nullptr;  // device memory for resident weights and biases
@@ -586,6 +589,8 @@ struct Job {
   bool tiled;       // W_dev is in matrix-core tile order (matrix-core GEMV)
   float* ws;        // its split-K workspace
   uint32_t* cnt;
+  const float* ln_in;  // tiled, ln, all rows resident: LayerNorm from these partials of x
+  float* ln_out;       // tiled, all rows resident: also write the partials of y here
 };
 
 hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long ldx, int ln, const void* W, int row0,
@@ -611,6 +616,8 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
   if (tiled) {
     p.ws = j.ws;
     p.cnt = j.cnt;
+    p.ln_in = ln ? j.ln_in : nullptr;
+    p.ln_out = j.ln_out;
     HIPCHK(ctx, hg::launch_gemv_mfma(p, j.dtype, j.B, st));
   } else {
     HIPCHK(ctx, hg::launch_gemv(p, j.dtype, j.B, st, 0));
@@ -622,7 +629,10 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
 hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   const auto tl = Clock::now();
   const size_t s = 2;
-  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr && !j.tiled && hg::gemv_fuses_ln(j.B);
+  // the LayerNorm inside the one resident GEMV: the vector kernels normalise x themselves,
+  // the matrix-core kernel from the partials its producer wrote
+  const bool fused_ln = j.ln && j.n_cpu == 0 && j.W_dev != nullptr &&
+                        (j.tiled ? j.ln_in != nullptr : hg::gemv_fuses_ln(j.B));
   const void* xin = j.x;
   long long ldin = j.ldx;
   // 1. input: materialise LayerNorm(x) unless it is fused into one resident GEMV,
@@ -1656,6 +1666,7 @@ void model_free(hetegen_model* m) {
   if (m->abuf) (void)hipFree(m->abuf);
   if (m->ws) (void)hipFree(m->ws);
   if (m->ws_cnt) (void)hipFree(m->ws_cnt);
+  if (m->ln_part) (void)hipFree(m->ln_part);
   (void)hipGetLastError();
   delete m;
 }
@@ -1707,6 +1718,15 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
     tr += elems * 2;
     return p;
   };
+  // every row of linear i on the matrix-core GEMV (resident, tile order, no CPU rows):
+  // then out and fc2 leave LayerNorm partials of x for a following fc1 / qkv of that
+  // kind, which normalises its input itself instead of after a LayerNorm launch
+  auto all_tiled = [&](int i) {
+    const auto& lin = m->lin[i];
+    return m->ln_partials && lin.W_tile && lin.n_cpu == 0 && lin.n_gpu == lin.N &&
+           (B >= kTiledMinBatch || !lin.W_dev);
+  };
+  const size_t part = hg::ln_partials_floats(H);
   for (int l = 0; l < m->L; ++l) {
     const void* xl = l == 0 ? x_dev : m->xbuf;
     for (int which = 0; which < 4; ++which) {
@@ -1728,6 +1748,11 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
       j.ws = m->ws;
       j.cnt = m->ws_cnt;
       j.ln_buf = m->lnbuf;
+      const int i = 4 * l + which;
+      if (which == 0 && l > 0 && all_tiled(i - 1) && all_tiled(i)) j.ln_in = m->ln_part;
+      if (which == 1 && all_tiled(i) && all_tiled(i + 1)) j.ln_out = m->ln_part + part;
+      if (which == 2 && all_tiled(i - 1) && all_tiled(i)) j.ln_in = m->ln_part + part;
+      if (which == 3 && l + 1 < m->L && all_tiled(i) && all_tiled(i + 1)) j.ln_out = m->ln_part;
       j.y_f32 = 0;
       switch (which) {
         case 0:  // qkv = LN(x) Wqkv^T + b
@@ -1923,6 +1948,10 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       }
       if (l.bias_host) dev_bytes += align256((size_t)l.N * 2);
     }
+    if (m->tiled) {
+      const char* lp = getenv("HETEGEN_LN_PARTIALS");
+      m->ln_partials = !(lp && strcmp(lp, "0") == 0);
+    }
     // A tiled model also keeps the row-major copy, for batches 1-2 on the vector GEMV, when
     // both copies take at most half of the device memory free now (HETEGEN_DUAL_LAYOUT=0 at
     // creation: tile order only)
@@ -1954,11 +1983,12 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
         }
       if ((most && !m->rowmajor && hipMalloc(&stage, most) != hipSuccess) ||
           (ws_floats && hipMalloc((void**)&m->ws, ws_floats * 4) != hipSuccess) ||
-          (ws_words && hipMalloc((void**)&m->ws_cnt, ws_words * 4) != hipSuccess)) {
+          (ws_words && hipMalloc((void**)&m->ws_cnt, ws_words * 4) != hipSuccess) ||
+          hipMalloc((void**)&m->ln_part, 2 * hg::ln_partials_floats(H) * 4) != hipSuccess) {
         (void)hipGetLastError();
         if (stage) (void)hipFree(stage);
         model_free(m);
-        return fail(ctx, HETEGEN_ERR_OOM, "tile staging buffer or split-K workspace");
+        return fail(ctx, HETEGEN_ERR_OOM, "tile staging buffer, split-K workspace or LayerNorm partials");
       }
       if (ws_words && hipMemset(m->ws_cnt, 0, ws_words * 4) != hipSuccess) {
         (void)hipFree(stage);

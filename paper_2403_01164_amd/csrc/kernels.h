@@ -30,6 +30,9 @@ struct GemvParams {
   // matrix-core GEMV on tile-ordered weights (launch_gemv_mfma) only:
   float* ws;           // split-K partials: mfma_ws_floats(rows, K, B) floats
   uint32_t* cnt;       // split-K arrival counters: mfma_cnt_words(rows, K) words, zero between launches
+  const float* ln_in;  // ln != 0: LayerNorm partials of x (ln_partials_floats(K)), written by the
+                       // launch that produced x through ln_out
+  float* ln_out;       // or nullptr: LayerNorm partials of y (y in the activation type)
 };
 
 // One linear of the persistent decode step (a device-resident table entry).
@@ -120,8 +123,16 @@ int mfma_splits(int K);
 size_t mfma_ws_floats(int rows, int K, int B);
 size_t mfma_cnt_words(int rows, int K);
 
-// y = epi(x W^T + bias) with W in tile order (p.W), every row on the GPU; p.ln must be 0.
-// Split launches need p.ws and p.cnt.
+// LayerNorm partials of a [B, n] activation: for every 16-element group q of a row and
+// batch row b < 8, the pair (sum of the group's values, sum of their squared deviations
+// from the group's mean) at floats 2 (8 q + b) and 2 (8 q + b) + 1 (the last group may
+// hold 8 elements).  A LayerNorm of the row combines them in a fixed order.
+size_t ln_partials_floats(int n);
+
+// y = epi(xn W^T + bias) with W in tile order (p.W), every row on the GPU, where xn is x,
+// or, when p.ln != 0, LayerNorm(x) from the partials p.ln_in (h_out, if set, receives xn
+// from workgroup 0).  With p.ln_out set the launch also writes the partials of y (p.y_f32
+// must be 0).  Split launches need p.ws and p.cnt.
 hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream);
 
 // Fixed split-K scratch of the matrix-core GEMV, one per GPU, for callers that cannot

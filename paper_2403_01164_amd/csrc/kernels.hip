@@ -131,6 +131,20 @@ __device__ __forceinline__ float wave_sum(float v) {
   return (r0 + r1) + (r2 + r3);
 }
 
+// Sum over each row of 16 lanes (lanes 16 r .. 16 r + 15); every lane of the row returns
+// its row's total, formed in a fixed order.
+__device__ __forceinline__ float row16_sum(float v) {
+  int iv = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, iv, 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
+  iv = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, iv, 0x4E, 0xF, 0xF, false));  // quad_perm 2,3,0,1
+  iv = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, iv, 0x141, 0xF, 0xF, false)); // row_half_mirror
+  iv = __builtin_bit_cast(int, v);
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, iv, 0x140, 0xF, 0xF, false)); // row_mirror
+  return v;
+}
+
 // LayerNorm statistics of B rows of x (16-byte chunk c of row b read by get(b, c))
 // for one 256-thread workgroup, two passes (mean, then the mean of squared
 // deviations).  Chunk c is always summed by thread c % 256 in increasing c and the
@@ -668,10 +682,16 @@ __global__ __launch_bounds__(kThreads) void gemv_ln1_kernel(GemvParams p) {
 // arrive (an arrival counter, no waiting) adds the G partials in split order, so the
 // result does not depend on timing.  Column order inside a tile is free (both
 // operands use the same one), so every lane's x fragment is 16 contiguous bytes.
+//
+// LayerNorm without a launch of its own (LN = true): the linear that produced x (out or
+// fc2, this kernel with ln_out) left per-16-row partials of its output; the consumer
+// combines them in its prologue, while its first weight tiles are in flight, and
+// normalises each x fragment as it multiplies it (one fused multiply-add per element).
 // ---------------------------------------------------------------------------
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 template <class T> struct Mma;
 template <> struct Mma<F16> {
@@ -687,11 +707,108 @@ template <> struct Mma<BF16> {
   }
 };
 
-constexpr int kTileRows = 16, kTileK = 32;
+// (x - mean) * rstd for 8 packed elements as one fused multiply-add x * a + c (a = rstd,
+// c = -mean * rstd), rounded to the activation type: for fp16 a mixed-precision fma that
+// reads the halves of a register and writes one half (v_fma_mix{lo,hi}_f16, 8
+// instructions), for bf16 fp32 fmas and packed conversions (v_cvt_pk_bf16_f32).  A GEMV
+// that normalises every x fragment it multiplies does this once per weight tile.
+template <class T> struct NormFma;
+template <> struct NormFma<F16> {
+  static __device__ __forceinline__ uint32_t two(uint32_t w, float a, float c) {
+    const f16x2 h = __builtin_bit_cast(f16x2, w);
+    const f16x2 r = {(_Float16)__builtin_fmaf((float)h.x, a, c), (_Float16)__builtin_fmaf((float)h.y, a, c)};
+    return __builtin_bit_cast(uint32_t, r);
+  }
+};
+template <> struct NormFma<BF16> {
+  static __device__ __forceinline__ uint32_t two(uint32_t w, float a, float c) {
+    const f32x2 f = {__builtin_fmaf(__builtin_bit_cast(float, w << 16), a, c),
+                     __builtin_fmaf(__builtin_bit_cast(float, w & 0xFFFF0000u), a, c)};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+  }
+};
+template <class T>
+__device__ __forceinline__ uint4 normalize8_fma(const uint4& v, float a, float c) {
+  return make_uint4(NormFma<T>::two(v.x, a, c), NormFma<T>::two(v.y, a, c), NormFma<T>::two(v.z, a, c),
+                    NormFma<T>::two(v.w, a, c));
+}
 
-template <class T, int B, int U>
+constexpr int kTileRows = 16, kTileK = 32;
+constexpr int kLnGroup = 16;    // elements per LayerNorm partial
+constexpr int kLnSlots = 8;     // batch rows per partial group (the largest batch)
+constexpr int kLnMaxGroups = kMaxLnK / kLnGroup;
+constexpr int kLnPerThread = (kLnMaxGroups + kThreads - 1) / kThreads;
+
+// LayerNorm statistics of B rows from their partials (see ln_partials_floats): the mean
+// is the sum of the group sums over K, and the variance combines each group's squared
+// deviations with its count times the squared distance of its mean from the row mean
+// (the pairwise combination of Chan, Golub and LeVeque), so no large sums of squares
+// are subtracted.  Thread t takes groups t + 256 i in increasing i, then the lanes and
+// wavefronts are combined in a fixed tree: every workgroup gets the same bits.
+template <int B>
+__device__ __forceinline__ void ln_partials_load(const float* __restrict__ pt, int K, f32x2 (&v)[kLnPerThread][B]) {
+  const int QG = (K + kLnGroup - 1) / kLnGroup;
+  // rounds of 256 groups: the same for the whole workgroup (a scalar branch); a thread past
+  // the last group of a round rereads it and the reduction drops it
+  const int rounds = (QG + kThreads - 1) / kThreads;
+#pragma unroll
+  for (int i = 0; i < kLnPerThread; ++i) {
+    const int q = min((int)threadIdx.x + kThreads * i, QG - 1);
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+      v[i][b] = i < rounds ? *gmem((const f32x2*)pt + (size_t)q * kLnSlots + b) : f32x2{0.f, 0.f};
+  }
+}
+
+template <int B>
+__device__ __forceinline__ void ln_partials_reduce(const f32x2 (&v)[kLnPerThread][B], int K, float* mean,
+                                                   float* rstd, float (*red)[kLnSlots][kWaves]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int QG = (K + kLnGroup - 1) / kLnGroup;
+  float s[B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    s[b] = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLnPerThread; ++i) s[b] += tid + kThreads * i < QG ? v[i][b].x : 0.f;
+    s[b] = wave_sum(s[b]);
+  }
+  if (lane == 0)
+#pragma unroll
+    for (int b = 0; b < B; ++b) red[0][b][wave] = s[b];
+  __syncthreads();
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    mean[b] = ((red[0][b][0] + red[0][b][1]) + (red[0][b][2] + red[0][b][3])) / (float)K;
+    s[b] = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLnPerThread; ++i) {
+      const int q = tid + kThreads * i;
+      // a group holds 16 elements, or 8 (the last one when K % 16 == 8; K % 8 == 0): the
+      // group mean is its sum times an exact power-of-two reciprocal
+      const bool full = K - kLnGroup * q >= kLnGroup;
+      if (q < QG) {
+        const float d = v[i][b].x * (full ? 1.f / kLnGroup : 0.125f) - mean[b];
+        s[b] += v[i][b].y + (full ? (float)kLnGroup : 8.f) * d * d;
+      }
+    }
+    s[b] = wave_sum(s[b]);
+  }
+  if (lane == 0)
+#pragma unroll
+    for (int b = 0; b < B; ++b) red[1][b][wave] = s[b];
+  __syncthreads();
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const float var = ((red[1][b][0] + red[1][b][1]) + (red[1][b][2] + red[1][b][3])) / (float)K;
+    rstd[b] = 1.0f / sqrtf(var + kLnEps);
+  }
+}
+
+template <class T, int B, int U, bool LN>
 __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G) {
   __shared__ float part[kWaves][4][64];
+  __shared__ float red[2][kLnSlots][kWaves];
   __shared__ int last;
   // the wavefront index through a scalar register: every tile bound below is then
   // wave-uniform and the skipped products are skipped by a branch.  A condition the
@@ -720,17 +837,64 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
       f.x[u] = load_g16((const uint4*)(xr + min(kx, K - 8)));
       // columns past K, and (as a second guard) the repeated tile of a step past k1,
       // multiply zeros
-      if (kx >= K || k0 + st * U + u >= k1) f.x[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (!LN && (kx >= K || k0 + st * U + u >= k1)) f.x[u] = make_uint4(0u, 0u, 0u, 0u);
     }
   };
+  // LayerNorm of x on the fly: xn = x * ln_a + ln_c for this lane's batch row
+  float ln_a = 0.f, ln_c = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   auto compute = [&](int st, const Buf& f) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (k0 + st * U + u < k1) acc = Mma<T>::run(f.w[u], f.x[u], acc);
+    for (int u = 0; u < U; ++u) {
+      const int kt = k0 + st * U + u;
+      if (kt < k1) {
+        uint4 xv = f.x[u];
+        if (LN) {
+          xv = normalize8_fma<T>(xv, ln_a, ln_c);
+          // columns past K (only in the last k-tile when K % 32 != 0) multiply zeros
+          if ((K & (kTileK - 1)) && kt == KT - 1 && kt * kTileK + 8 * grp >= K) xv = make_uint4(0u, 0u, 0u, 0u);
+        }
+        acc = Mma<T>::run(f.w[u], xv, acc);
+      }
+    }
   };
   Buf fa, fb;
-  if (nst > 0) load(0, fa);
+  // the LayerNorm partials are requested before the first weights, so that waiting for
+  // them leaves the weight loads in flight
+  f32x2 lnv[LN ? kLnPerThread : 1][B];
+  if constexpr (LN) {
+    ln_partials_load<B>(p.ln_in, K, lnv);
+    __builtin_amdgcn_sched_barrier(0);  // keep them ahead of the weight loads
+  }
+  // (with the LayerNorm the first loads are unconditional, for the same reason; a
+  // wavefront without tiles rereads tile k1 - 1 >= 0 and computes nothing)
+  if (LN || nst > 0) load(0, fa);
+  if constexpr (LN) {
+    float mean[B], rstd[B];
+    ln_partials_reduce<B>(lnv, K, mean, rstd, red);
+#pragma unroll
+    for (int q = 0; q < B; ++q)
+      if (q == b) {
+        ln_a = rstd[q];
+        ln_c = -mean[q] * rstd[q];
+      }
+    if (p.h_out && blockIdx.x == 0) {
+      // the normalised input, for a caller that records it
+      const int n8 = K >> 3;
+      for (int c = threadIdx.x; c < B * n8; c += kThreads) {
+        const int r = c / n8, cc = c - r * n8;
+        float a = 0.f, cr = 0.f;
+#pragma unroll
+        for (int q = 0; q < B; ++q)
+          if (q == r) {
+            a = rstd[q];
+            cr = -mean[q] * rstd[q];
+          }
+        const uint4 xv = load_g16((const uint4*)((const uint16_t*)p.x + (long long)r * p.ldx + 8 * cc));
+        *(uint4*)((uint16_t*)p.h_out + (long long)r * p.ldh + 8 * cc) = normalize8_fma<T>(xv, a, cr);
+      }
+    }
+  }
   int st = 0;
   for (; st + 2 < nst; st += 2) {
     load(st + 1, fb);
@@ -776,11 +940,24 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
     }
   }
   const int row = rt * kTileRows + i;
-  if (!mine || row >= p.rows) return;
-  const uint16_t* bias = (const uint16_t*)p.bias;
-  float y = s + (bias ? T::to_f32(bias[row]) : 0.f);
-  const float rv = p.epi == EPI_RESID ? T::to_f32(((const uint16_t*)p.resid)[j * p.ldr + row]) : 0.f;
-  store_y<T>(p.y, j * p.ldy + row, p.y_f32, apply_epi(y, p.epi, rv));
+  const bool valid = mine && row < p.rows;
+  float yv = 0.f;
+  if (valid) {
+    const uint16_t* bias = (const uint16_t*)p.bias;
+    const float y = s + (bias ? T::to_f32(bias[row]) : 0.f);
+    const float rv = p.epi == EPI_RESID ? T::to_f32(((const uint16_t*)p.resid)[j * p.ldr + row]) : 0.f;
+    yv = apply_epi(y, p.epi, rv);
+    store_y<T>(p.y, j * p.ldy + row, p.y_f32, yv);
+  }
+  // LayerNorm partials of this row tile's outputs for the next linear: a row of 16
+  // lanes holds the 16 rows of one batch row (lanes past 16 B hold none)
+  if (!p.ln_out || wave * 64 >= 16 * B) return;
+  const float n = (float)min(kTileRows, p.rows - rt * kTileRows);
+  const float a = valid ? T::to_f32(round_act<T>(yv)) : 0.f;
+  const float s1 = row16_sum(a);
+  const float d = valid ? a - s1 / n : 0.f;
+  const float m2 = row16_sum(d * d);
+  if (mine && i == 0) *(f32x2*)(p.ln_out + ((size_t)rt * kLnSlots + j) * 2) = f32x2{s1, m2};
 }
 
 // Tile order of W [rows, K]: one 16-byte group per thread (see tiled_bytes in kernels.h).
@@ -1347,13 +1524,18 @@ size_t mfma_cnt_words(int rows, int K) {
   return (size_t)((rows + kTileRows - 1) / kTileRows);
 }
 
-template <class T, int B>
-hipError_t launch_mfma_b(const GemvParams& p, hipStream_t s) {
+template <class T, int B, bool LN>
+hipError_t launch_mfma_ln(const GemvParams& p, hipStream_t s) {
   const int G = mfma_splits(p.K);
   const int grid = ((p.rows + kTileRows - 1) / kTileRows) * G;
-  if (G == 1) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 8>), dim3(grid), dim3(kThreads), 0, s, p, 1);
-  else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4>), dim3(grid), dim3(kThreads), 0, s, p, G);
+  if (G == 1) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, LN ? 4 : 8, LN>), dim3(grid), dim3(kThreads), 0, s, p, 1);
+  else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4, LN>), dim3(grid), dim3(kThreads), 0, s, p, G);
   return hipGetLastError();
+}
+
+template <class T, int B>
+hipError_t launch_mfma_b(const GemvParams& p, hipStream_t s) {
+  return p.ln ? launch_mfma_ln<T, B, true>(p, s) : launch_mfma_ln<T, B, false>(p, s);
 }
 
 template <class T>
@@ -1371,9 +1553,13 @@ hipError_t launch_mfma_t(const GemvParams& p, int B, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+size_t ln_partials_floats(int n) { return n > 0 ? (size_t)((n + kLnGroup - 1) / kLnGroup) * kLnSlots * 2 : 0; }
+
 hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream) {
   if (p.rows <= 0) return hipSuccess;
-  if (p.ln || p.K < 8 || p.K % 8) return hipErrorInvalidValue;
+  if (p.K < 8 || p.K % 8 || B < 1 || B > kLnSlots) return hipErrorInvalidValue;
+  if (p.ln && (!p.ln_in || p.K > kMaxLnK)) return hipErrorInvalidValue;
+  if (p.ln_out && p.y_f32) return hipErrorInvalidValue;
   if (mfma_splits(p.K) > 1 && (!p.ws || !p.cnt)) return hipErrorInvalidValue;
   return dtype == 1 ? launch_mfma_t<BF16>(p, B, stream) : launch_mfma_t<F16>(p, B, stream);
 }

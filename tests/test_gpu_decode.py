@@ -232,6 +232,62 @@ def test_dual_layout_runs_each_batch_on_the_matching_copy(ctx, dtype):
         rm.free()
 
 
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+@pytest.mark.parametrize("H,F", [(1032, 2056), (512, 2048)])
+def test_tiled_layernorm_from_partials(ctx, dtype, H, F):
+    # on a model in tile order, qkv (after the first layer's) and fc1 take their LayerNorm
+    # from the partials that the fc2 / out before them wrote (one pair per 16 outputs and
+    # batch row; H = 1032 ends in a group of 8): teacher-forced against the oracle over
+    # three layers, and each batch row's bits do not depend on the batch size
+    L = 3
+    m = _model_with_env(ctx, {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1, max_batch=8)
+    try:
+        assert hg.hetegen_model_layouts(m.m) == hg.LAYOUT_TILED
+        x = synth.normal((8, H), dtype, 0, synth.act_id(3))
+        out8, tr = m.step(x, trace=True)
+        last, _ = m.check_teacher_forced(x, tr)
+        assert np.array_equal(out8, last)
+        for B in (3, 5, 1):
+            assert np.array_equal(m.step(np.ascontiguousarray(x[:B])), out8[:B]), B
+        # the same model with LayerNorm launches instead passes too, and the two agree
+        # within the tolerance per layer, relative to each row's largest output (their
+        # LayerNorm roundings differ in places, and a one-unit difference in a large
+        # value carries over to the small values after it)
+        k = _model_with_env(ctx, {"HETEGEN_DUAL_LAYOUT": "0", "HETEGEN_LN_PARTIALS": "0"}, L, H, F, dtype, 0.0, 1,
+                            max_batch=8, weights=(m.W, m.b))
+        try:
+            outk, trk = k.step(x, trace=True)
+            lastk, _ = k.check_teacher_forced(x, trk)
+            assert np.array_equal(outk, lastk)
+            assert rel_err(oracle.decode(out8, dtype), oracle.decode(outk, dtype), floor=1.0) <= \
+                L * (TOL + U_ACT[dtype])
+        finally:
+            k.free()
+    finally:
+        m.free()
+
+
+@pytest.mark.parametrize("B", [3, 8])
+def test_tiled_partials_only_between_matrix_core_linears(ctx, B):
+    # a linear with CPU rows (layer 1's out) or host-resident rows (layer 2's fc2) writes no
+    # partials, so the fc1 / qkv after it normalises after a LayerNorm launch, while the
+    # other pairs keep the partials; stale partials would fail the teacher-forced check
+    dtype, L, H, F = synth.F16, 3, 512, 2048
+    alpha = [0.0] * (4 * L)
+    alpha[4 * 1 + 1] = 0.3
+    resident = [1] * (4 * L)
+    resident[4 * 2 + 3] = 0
+    m = _model_with_env(ctx, {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, alpha, resident, max_batch=8)
+    try:
+        x = synth.normal((B, H), dtype, 0, synth.act_id(4))
+        out, tr = m.step(x, trace=True)
+        last, _ = m.check_teacher_forced(x, tr)
+        assert np.array_equal(out, last)
+        assert np.array_equal(m.step(x), out)
+    finally:
+        m.free()
+
+
 def test_persistent_opt67b_shapes_two_layers(ctx):
     dtype, L, H, F = synth.F16, 2, 4096, 16384
     m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
