@@ -170,6 +170,17 @@ def single_linear(args, torch, synth, hg):
     probe = hg.hetegen_probe(ctx, Wh[0], N, K, dt, B, 5)
     log("single linear [%d,%d] B=%d: %d weight copies (%.0f MB); probe %s" %
         (N, K, B, ncopy, ncopy * wb / 1e6, {k: round(v / 1e9, 1) for k, v in probe.items()}))
+    # fixed costs of a synchronous call that no kernel work removes: the launch round trip
+    # (empty kernel + stream synchronisation, timed in C) and this binding's own overhead (the
+    # same call refused by its first argument check: ctypes marshalling, no GPU work)
+    launch_us = hg.hetegen_probe_launch(ctx, 1000, sptr)
+    nb = 20000
+    c0 = time.perf_counter()
+    for _ in range(nb):
+        hg.hetegen_linear_status(ctx, x.data_ptr(), B, K, Wh[0], 0, N, dt, bh, bd.data_ptr(), 2.0, y.data_ptr(),
+                                 hg.F32, sptr)
+    binding_us = (time.perf_counter() - c0) / nb * 1e6
+    log("launch round trip %.2f us, binding %.2f us per call" % (launch_us, binding_us))
     rows = []
     for resident in (True, False):
         for alpha in (0.0, 0.25, 0.5, 1.0):
@@ -192,18 +203,25 @@ def single_linear(args, torch, synth, hg):
             # ones, host reads for CPU rows (Eq. 4 balance when split)
             v_g = HBM_PEAK_GBPS * 1e9 if resident else 1.0 / (1.0 / probe["h2d_Bps"] + 1.0 / probe["hbm_gemv_Bps"])
             if n_cpu == 0:
-                floor_us, bound = wb / v_g * 1e6, ("hbm" if resident else "h2d")
+                work_us, bound = wb / v_g * 1e6, ("hbm" if resident else "h2d")
             elif n_cpu == N:
-                floor_us, bound = wb / probe["cpu_Bps"] * 1e6, "cpu"
+                work_us, bound = wb / probe["cpu_Bps"] * 1e6, "cpu"
             else:
-                floor_us = max(n_cpu * K * 2 / probe["cpu_Bps"], (N - n_cpu) * K * 2 / v_g) * 1e6
+                work_us = max(n_cpu * K * 2 / probe["cpu_Bps"], (N - n_cpu) * K * 2 / v_g) * 1e6
                 bound = "cpu+" + ("hbm" if resident else "h2d")
+            # the latency floor: the work at those rates plus the binding and one launch round
+            # trip per hand-off (the final synchronisation; with CPU rows also x to the host)
+            trips = 1 if n_cpu == 0 else 2
+            floor_us = work_us + binding_us + trips * launch_us
             rows.append({"alpha_cpu": alpha, "resident": resident, "median_us": round(q(0.5), 2),
                          "p10_us": round(q(0.1), 2), "p90_us": round(q(0.9), 2),
                          "GBps": round(wb / (q(0.5) * 1e-6) / 1e9, 2), "bound": bound,
-                         "floor_us": round(floor_us, 2), "frac_of_floor": round(floor_us / q(0.5), 4)})
-            log("alpha %.2f %s: median %.1f us (p10 %.1f, p90 %.1f), floor %.1f us (%s)" %
-                (alpha, "resident" if resident else "streamed", q(0.5), q(0.1), q(0.9), floor_us, bound))
+                         "work_floor_us": round(work_us, 2), "launch_round_trips": trips,
+                         "floor_us": round(floor_us, 2), "frac_of_floor": round(floor_us / q(0.5), 4),
+                         "frac_of_work_floor": round(work_us / q(0.5), 4)})
+            log("alpha %.2f %s: median %.1f us (p10 %.1f, p90 %.1f), floor %.1f us (%s work %.1f + %d trips)" %
+                (alpha, "resident" if resident else "streamed", q(0.5), q(0.1), q(0.9), floor_us, bound, work_us,
+                 trips))
     head = rows[0]
     cpu_base = None
     if not args.no_cpu_baseline:
@@ -241,6 +259,7 @@ def single_linear(args, torch, synth, hg):
         "config": {"workload": "single Linear [%d,%d] fp16, batch %d, CPU fractions 0/.25/.5/1, resident and "
                                "streamed; %d weight copies rotated (%.0f MB)" % (N, K, B, ncopy, ncopy * wb / 1e6)},
         "probe_GBps": {k: round(v / 1e9, 2) for k, v in probe.items()},
+        "launch_round_trip_us": round(launch_us, 2), "binding_us_per_call": round(binding_us, 2),
         "results": rows, "cpu_baseline": cpu_base, "host": host_info(torch)}))
     for w in Wh:
         hg.hetegen_host_free(ctx, w)

@@ -242,6 +242,14 @@ HETEGEN_API hetegen_status hetegen_probe_hbm(hetegen_ctx* ctx, size_t bytes, int
  * CPU-GPU link bandwidth); the planner's V_COM comes from hetegen_probe. */
 HETEGEN_API hetegen_status hetegen_probe_link(hetegen_ctx* ctx, size_t bytes, int reps, double* Bps_out);
 
+/* Launch round trip: host time from the launch of an empty kernel (one wavefront) on
+ * `stream` to the return of hipStreamSynchronize(stream), median of `reps` >= 1 after
+ * ten warm-ups, in microseconds (*us_out).  The fixed cost of a synchronous call on
+ * top of the duration of its kernels: the floor of a single small linear's latency,
+ * which no kernel work reaches below (hetegen_linear hands x to the host and y back,
+ * i.e. one such round trip per direction when it has CPU rows). */
+HETEGEN_API hetegen_status hetegen_probe_launch(hetegen_ctx* ctx, int reps, void* stream, double* us_out);
+
 /* The CPU share alone (Sec. 3.2: the host cores compute the rows whose parameters
  * stay in host memory), on the calling thread and the library's CPU worker team (one
  * job at a time; calls from several threads are serialised), no device involved:

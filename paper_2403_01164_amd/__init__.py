@@ -90,6 +90,7 @@ _SIGS = {
     "hetegen_cpu_linear": ([_vp, _i, _i, _vp, _i, _vp, _i, _i, _vp, _i, _i], _i),
     "hetegen_probe_hbm": ([_vp, _sz, _i, ctypes.POINTER(_d)], _i),
     "hetegen_probe_link": ([_vp, _sz, _i, ctypes.POINTER(_d)], _i),
+    "hetegen_probe_launch": ([_vp, _i, _vp, ctypes.POINTER(_d)], _i),
     "hetegen_model_kv_create": ([_vp, _vp, _i, _i], _i),
     "hetegen_model_kv_write": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
     "hetegen_model_kv_read": ([_vp, _vp, _i, _i, _i, _i, _vp, _vp, _vp], _i),
@@ -410,4 +411,11 @@ def hetegen_probe_link(ctx, nbytes, reps=10):
     """Idle pinned host-to-device copy rate in bytes/s (median of reps copies)."""
     out = _d()
     _check(_lib.hetegen_probe_link(ctx, nbytes, reps, ctypes.byref(out)), ctx)
+    return out.value
+
+
+def hetegen_probe_launch(ctx, reps=1000, stream=0):
+    """Empty-kernel launch + stream synchronisation round trip in microseconds (median)."""
+    out = _d()
+    _check(_lib.hetegen_probe_launch(ctx, reps, stream or None, ctypes.byref(out)), ctx)
     return out.value

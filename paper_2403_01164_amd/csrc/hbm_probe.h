@@ -9,4 +9,7 @@ namespace hg {
 // sink is a device word the kernel writes only for one value of the data.
 hipError_t launch_read(const void* buf, size_t bytes, uint32_t* sink, int grid, hipStream_t stream);
 
+// One workgroup of one wavefront that does nothing (the launch round-trip probe).
+hipError_t launch_empty(hipStream_t stream);
+
 }  // namespace hg

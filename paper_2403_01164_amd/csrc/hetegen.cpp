@@ -926,7 +926,9 @@ hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, int B, int K,
     if ((n_cpu > 0 && !bias_host && bias_dev) || (n_gpu > 0 && !bias_dev && bias_host))
       return fail(ctx, HETEGEN_ERR_INVALID_ARG, "bias: pass bias_host and bias_dev, or neither");
     bool pageable = false;
-    TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
+    // W_host is read by the CPU share and by the streamed chunks; a call with every row
+    // resident on the GPU does not touch it
+    if (n_cpu > 0 || !W_dev_resident) TRY(check_weight(ctx, W_host, (size_t)N * K * 2, &pageable));
     const size_t row = (size_t)K * 2;
     if (!W_dev_resident && n_gpu > 0 && row > ctx->chunk_bytes)
       return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "a weight row (%zu bytes) exceeds chunk_bytes", row);
@@ -1553,6 +1555,28 @@ extern "C" hetegen_status hetegen_probe(hetegen_ctx* ctx, const void* W_host, in
     out->h2d_Bps = wbytes / median(cm.empty() ? tm : cm);
     out->hbm_gemv_Bps = wbytes / median(tg);
     out->pin_Bps = pageable ? wbytes / median(tp) : 0;
+    return HETEGEN_OK;
+  });
+}
+
+// ---- launch round trip ----
+extern "C" hetegen_status hetegen_probe_launch(hetegen_ctx* ctx, int reps, void* stream, double* us_out) {
+  return api_guard(ctx, [&]() -> hetegen_status {
+    if (!ctx) return HETEGEN_ERR_INVALID_ARG;
+    ctx->err.clear();
+    if (!us_out || reps < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_probe_launch: bad arguments");
+    HIPCHK(ctx, hipSetDevice(ctx->device));
+    hipStream_t st = (hipStream_t)stream;
+    HIPCHK(ctx, hipStreamSynchronize(st));
+    std::vector<double> t;
+    for (int r = 0; r < reps + 10; ++r) {
+      const auto t0 = Clock::now();
+      HIPCHK(ctx, hg::launch_empty(st));
+      HIPCHK(ctx, hipStreamSynchronize(st));
+      if (r >= 10) t.push_back(ms_since(t0) * 1e3);
+    }
+    std::sort(t.begin(), t.end());
+    *us_out = t[t.size() / 2];
     return HETEGEN_OK;
   });
 }

@@ -285,6 +285,16 @@ def test_probe_hbm_read_bandwidth(ctx):
         hg.hetegen_probe_hbm(ctx, 1000, 3)
 
 
+def test_probe_launch_round_trip(ctx):
+    # an empty launch plus a stream synchronisation takes microseconds
+    s = torch.cuda.current_stream().cuda_stream
+    us = hg.hetegen_probe_launch(ctx, 200, s)
+    assert 0.5 < us < 1000
+    with pytest.raises(hg.HetegenError) as e:
+        hg.hetegen_probe_launch(ctx, 0, s)
+    assert e.value.status == hg.ERR_INVALID_ARG
+
+
 def _page_node(addr):
     """NUMA node of the page at `addr` (get_mempolicy with MPOL_F_NODE | MPOL_F_ADDR)."""
     import ctypes
