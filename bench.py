@@ -131,6 +131,11 @@ def host_info(torch):
         pass
     info["amdgpu_module"] = read("/sys/module/amdgpu/version")
     try:
+        import paper_2403_01164_amd as hg_mod
+        info["cpu_share_isa"] = hg_mod.hetegen_cpu_share_isa()
+    except Exception:
+        pass
+    try:
         pr = torch.cuda.get_device_properties(0)
         info["gpu"] = "%s (%s, %d CUs)" % (pr.name, pr.gcnArchName, pr.multi_processor_count)
         bdf = "%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)

@@ -96,6 +96,12 @@ HETEGEN_API hetegen_status hetegen_destroy(hetegen_ctx* ctx);
  * valid until the next call on ctx. */
 HETEGEN_API const char* hetegen_last_error(const hetegen_ctx* ctx);
 
+/* Instruction set the CPU share uses on this host, chosen at load time: "avx512+bf16"
+ * (bf16 weights through the AVX512-BF16 dot product, fp16 widened to binary32 and
+ * FMA; the environment variable HETEGEN_CPU_BF16=0 at load keeps bf16 on the widening
+ * path too), "avx512", "avx2" or "scalar".  A static string. */
+HETEGEN_API const char* hetegen_cpu_share_isa(void);
+
 /* Page-locked host memory for weights: *p receives `bytes` bytes that the CPU
  * share reads directly and the copy engines read over PCIe (not write-combined).
  * Free with hetegen_host_free.  OOM if the allocation fails. */

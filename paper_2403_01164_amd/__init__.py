@@ -64,6 +64,7 @@ _SIGS = {
     "hetegen_create": ([ctypes.POINTER(Config), ctypes.POINTER(_vp)], _i),
     "hetegen_destroy": ([_vp], _i),
     "hetegen_last_error": ([_vp], ctypes.c_char_p),
+    "hetegen_cpu_share_isa": ([], ctypes.c_char_p),
     "hetegen_host_alloc": ([_vp, _sz, ctypes.POINTER(_vp)], _i),
     "hetegen_host_free": ([_vp, _vp], _i),
     "hetegen_linear": ([_vp, _vp, _i, _i, _vp, _vp, _i, _i, _vp, _vp, _d, _vp, _i, _vp], _i),
@@ -143,6 +144,11 @@ def hetegen_destroy(ctx):
 def hetegen_last_error(ctx):
     m = _lib.hetegen_last_error(ctx)
     return m.decode() if m else ""
+
+
+def hetegen_cpu_share_isa():
+    """Instruction set of the CPU share on this host ("avx512+bf16", "avx512", "avx2", "scalar")."""
+    return _lib.hetegen_cpu_share_isa().decode()
 
 
 def hetegen_host_alloc(ctx, nbytes):

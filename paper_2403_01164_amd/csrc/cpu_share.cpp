@@ -6,9 +6,11 @@
 // streams whole weight rows sequentially from DRAM.  A row block of R rows is
 // processed together so that each binary32 x vector loaded from cache is used R
 // times; 16-bit weights are widened to binary32 in registers (vcvtph2ps for fp16,
-// a 16-bit shift for bf16) and accumulated with FMA.  The instruction set is
-// chosen at run time (AVX-512, else AVX2+F16C+FMA, else portable C), so one build
-// runs on any x86-64 host.
+// a 16-bit shift for bf16) and accumulated with FMA; on hosts with AVX512-BF16, bf16
+// weights instead go through vdpbf16ps (two bf16 products per binary32 lane, so one
+// instruction per 32 weights and batch row, against a widening and two FMAs).  The
+// instruction set is chosen at run time (AVX-512, else AVX2+F16C+FMA, else portable
+// C), so one build runs on any x86-64 host.
 #include "cpu_share.h"
 
 #include <immintrin.h>
@@ -295,6 +297,150 @@ __attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) void block512_spli
   }
 }
 
+// ---------------- AVX512-BF16 (bf16 weights) ----------------
+// x [B, K] arrives as binary32 values that are bf16 values (the activation type), so it
+// is narrowed to bf16 exactly, once per call.  vdpbf16ps multiplies bf16 pairs exactly
+// and adds them to binary32 lanes (lane j of a 32-element chunk takes elements 2j and
+// 2j + 1); like every bf16 instruction of this extension it treats bf16 subnormal
+// inputs as zero and flushes binary32 subnormal results (|v| < 2^-126), far below the
+// oracle's tolerance for any row with a normal output.  Every (row, batch row)
+// accumulator adds the chunks in increasing k, the masked tail last, in both kernels
+// below, so a row's bits do not depend on the batch size.
+#define HG_BF16_TARGET __attribute__((target("avx512f,avx512bw,avx512vl,avx512bf16,fma")))
+
+HG_BF16_TARGET inline __m512bh ld_bh(const uint16_t* p) { return (__m512bh)_mm512_loadu_si512((const void*)p); }
+HG_BF16_TARGET inline __m512bh ld_bh_tail(const uint16_t* p, int n) {  // n < 32 elements, the rest zero
+  return (__m512bh)_mm512_maskz_loadu_epi16((__mmask32)((1u << n) - 1u), p);
+}
+
+// x (binary32, exact bf16 values) -> bf16 [B, K]
+HG_BF16_TARGET void narrow_bf16(const float* x, int n, uint16_t* out) {
+  int i = 0;
+  for (; i + 32 <= n; i += 32) {
+    const __m512bh v = _mm512_cvtne2ps_pbh(_mm512_loadu_ps(x + i + 16), _mm512_loadu_ps(x + i));
+    _mm512_storeu_si512((void*)(out + i), (__m512i)v);
+  }
+  for (; i < n; ++i) {
+    uint32_t b;
+    memcpy(&b, x + i, 4);
+    out[i] = (uint16_t)(b >> 16);
+  }
+}
+
+template <int B, int R>
+HG_BF16_TARGET void block_bf16(const uint16_t* xb, int K, const uint16_t* W, const uint16_t* bias, int r0, int r,
+                               float* y, int ldy) {
+  __m512 acc[R][B];
+  for (int i = 0; i < R; ++i)
+    for (int b = 0; b < B; ++b) acc[i][b] = _mm512_setzero_ps();
+  const uint16_t* w[R];
+  for (int i = 0; i < R; ++i) w[i] = W + (int64_t)(r + i) * K;
+  const int K32 = K & ~31;
+  for (int k = 0; k < K32; k += 32) {
+    for (int i = 0; i < R; ++i) _mm_prefetch((const char*)(w[i] + k) + kPrefetchBytes, _MM_HINT_T0);
+    __m512bh wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = ld_bh(w[i] + k);
+    for (int b = 0; b < B; ++b) {
+      const __m512bh xv = ld_bh(xb + (int64_t)b * K + k);
+      for (int i = 0; i < R; ++i) acc[i][b] = _mm512_dpbf16_ps(acc[i][b], wv[i], xv);
+    }
+  }
+  if (K32 < K) {
+    __m512bh wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = ld_bh_tail(w[i] + K32, K - K32);
+    for (int b = 0; b < B; ++b) {
+      const __m512bh xv = ld_bh_tail(xb + (int64_t)b * K + K32, K - K32);
+      for (int i = 0; i < R; ++i) acc[i][b] = _mm512_dpbf16_ps(acc[i][b], wv[i], xv);
+    }
+  }
+  for (int i = 0; i < R; ++i) {
+    const float bv = bias ? bf16_to_f32(bias[r + i]) : 0.f;
+    for (int b = 0; b < B; ++b) y[(int64_t)b * ldy + (r + i - r0)] = _mm512_reduce_add_ps(acc[i][b]) + bv;
+  }
+}
+
+// Batch 5-8: the R x B accumulators do not fit the registers; as in block512_split, the
+// batch runs in two groups over chunks of KC elements, the second reusing the chunk
+// of the R rows from L1.
+template <int R, int LO, int NB>
+HG_BF16_TARGET __attribute__((always_inline)) inline void group_bf16(const uint16_t* xb, int K, const uint16_t* const* w,
+                                                                     int k0, int k1, int tail, __m512 (*acc)[R]) {
+  __m512 a[NB][R];
+  for (int bb = 0; bb < NB; ++bb)
+    for (int i = 0; i < R; ++i) a[bb][i] = acc[LO + bb][i];
+  for (int k = k0; k < k1; k += 32) {
+    if (LO == 0)
+      for (int i = 0; i < R; ++i) _mm_prefetch((const char*)(w[i] + k) + kPrefetchBytes, _MM_HINT_T0);
+    __m512bh wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = ld_bh(w[i] + k);
+    for (int bb = 0; bb < NB; ++bb) {
+      const __m512bh xv = ld_bh(xb + (int64_t)(LO + bb) * K + k);
+      for (int i = 0; i < R; ++i) a[bb][i] = _mm512_dpbf16_ps(a[bb][i], wv[i], xv);
+    }
+  }
+  if (tail) {  // tail < 32 elements at k1
+    __m512bh wv[R];
+    for (int i = 0; i < R; ++i) wv[i] = ld_bh_tail(w[i] + k1, tail);
+    for (int bb = 0; bb < NB; ++bb) {
+      const __m512bh xv = ld_bh_tail(xb + (int64_t)(LO + bb) * K + k1, tail);
+      for (int i = 0; i < R; ++i) a[bb][i] = _mm512_dpbf16_ps(a[bb][i], wv[i], xv);
+    }
+  }
+  for (int bb = 0; bb < NB; ++bb)
+    for (int i = 0; i < R; ++i) acc[LO + bb][i] = a[bb][i];
+}
+
+template <int B, int R>
+HG_BF16_TARGET void block_bf16_split(const uint16_t* xb, int K, const uint16_t* W, const uint16_t* bias, int r0, int r,
+                                     float* y, int ldy) {
+  constexpr int KC = 256, H0 = (B + 1) / 2;
+  __m512 acc[B][R];
+  for (int b = 0; b < B; ++b)
+    for (int i = 0; i < R; ++i) acc[b][i] = _mm512_setzero_ps();
+  const uint16_t* w[R];
+  for (int i = 0; i < R; ++i) w[i] = W + (int64_t)(r + i) * K;
+  const int K32 = K & ~31;
+  for (int k0 = 0; k0 < K; k0 += KC) {
+    const int k1 = k0 + KC < K32 ? k0 + KC : K32;  // full 32-element chunks of this block
+    const int tail = k0 + KC >= K ? K - K32 : 0;
+    group_bf16<R, 0, H0>(xb, K, w, k0, k1, tail, acc);
+    group_bf16<R, H0, B - H0>(xb, K, w, k0, k1, tail, acc);
+  }
+  for (int i = 0; i < R; ++i) {
+    const float bv = bias ? bf16_to_f32(bias[r + i]) : 0.f;
+    for (int b = 0; b < B; ++b) y[(int64_t)b * ldy + (r + i - r0)] = _mm512_reduce_add_ps(acc[b][i]) + bv;
+  }
+}
+
+typedef void (*BlockBf16Fn)(const uint16_t*, int, const uint16_t*, const uint16_t*, int, int, float*, int);
+
+template <int B>
+void run_blocks_bf16(const uint16_t* xb, int K, const uint16_t* W, const uint16_t* bias, int r0, int r1, int ba,
+                     int bb, float* y, int ldy) {
+  constexpr int R = 4;
+  const BlockBf16Fn blk = B >= 5 ? block_bf16_split<B, R> : block_bf16<B, R>;
+  for (int i = ba; i < bb; ++i) {
+    const int r = r0 + R * i;
+    if (r + R <= r1) blk(xb, K, W, bias, r0, r, y, ldy);
+    else
+      for (int q = r; q < r1; ++q) block_bf16<B, 1>(xb, K, W, bias, r0, q, y, ldy);
+  }
+}
+
+void run_blocks_bf16_b(const uint16_t* xb, int B, int K, const uint16_t* W, const uint16_t* bias, int r0, int r1,
+                       int ba, int bb, float* y, int ldy) {
+  switch (B) {
+    case 1: run_blocks_bf16<1>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 2: run_blocks_bf16<2>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 3: run_blocks_bf16<3>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 4: run_blocks_bf16<4>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 5: run_blocks_bf16<5>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 6: run_blocks_bf16<6>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    case 7: run_blocks_bf16<7>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+    default: run_blocks_bf16<8>(xb, K, W, bias, r0, r1, ba, bb, y, ldy); break;
+  }
+}
+
 // ---------------- AVX2 + F16C + FMA ----------------
 template <bool BF>
 __attribute__((target("avx2,f16c,fma"))) inline __m256 load8_avx2(const uint16_t* p) {
@@ -347,6 +493,14 @@ Isa detect() {
 
 const Isa g_isa = detect();
 
+bool detect_bf16() {
+  __builtin_cpu_init();
+  const char* e = getenv("HETEGEN_CPU_BF16");  // "0": keep the widening FMA path
+  return g_isa == ISA_AVX512 && __builtin_cpu_supports("avx512bf16") && !(e && strcmp(e, "0") == 0);
+}
+
+const bool g_bf16 = detect_bf16();
+
 typedef void (*BlockFn)(const float*, int, const uint16_t*, const uint16_t*, int, int, float*, int);
 
 // Four rows per block (four weight streams per core); the AVX-512 loop is unrolled
@@ -387,7 +541,7 @@ void run_blocks_b(Isa isa, const float* x, int B, int K, const uint16_t* W, cons
 }  // namespace
 
 const char* cpu_share_isa() {
-  return g_isa == ISA_AVX512 ? "avx512" : g_isa == ISA_AVX2 ? "avx2" : "scalar";
+  return g_isa == ISA_AVX512 ? (g_bf16 ? "avx512+bf16" : "avx512") : g_isa == ISA_AVX2 ? "avx2" : "scalar";
 }
 
 void team_streamed_chunks(long long delta) { g_streamed_chunks.fetch_add(delta, std::memory_order_relaxed); }
@@ -414,7 +568,15 @@ void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const
     int r0, r1, blocks;
     float* y;
     int ldy;
-  } job{x, B, K, W, dtype, bias, r0, r1, (n + 3) / 4, y, ldy};
+    const uint16_t* xb;  // x narrowed to bf16 (bf16 weights on AVX512-BF16 hosts)
+  } job{x, B, K, W, dtype, bias, r0, r1, (n + 3) / 4, y, ldy, nullptr};
+  if (dtype == 1 && g_bf16) {
+    // the calling thread's buffer: it stays valid while the job runs (the caller takes part)
+    thread_local std::vector<uint16_t> xb;
+    if (xb.size() < (size_t)B * K) xb.resize((size_t)B * K);
+    narrow_bf16(x, B * K, xb.data());
+    job.xb = xb.data();
+  }
   if (g_isa == ISA_SCALAR) {
     Team::get().run(nt, n, [](void* a, int g) {
       const Job& j = *(const Job*)a;
@@ -431,7 +593,8 @@ void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const
   Team::get().run(nt, grains, [](void* a, int g) {
     const Job& j = *(const Job*)a;
     const int ba = g * kGrain, bb = ba + kGrain < j.blocks ? ba + kGrain : j.blocks;
-    if (j.dtype == 1) run_blocks_b<true>(g_isa, j.x, j.B, j.K, j.W, j.bias, j.r0, j.r1, ba, bb, j.y, j.ldy);
+    if (j.xb) run_blocks_bf16_b(j.xb, j.B, j.K, j.W, j.bias, j.r0, j.r1, ba, bb, j.y, j.ldy);
+    else if (j.dtype == 1) run_blocks_b<true>(g_isa, j.x, j.B, j.K, j.W, j.bias, j.r0, j.r1, ba, bb, j.y, j.ldy);
     else run_blocks_b<false>(g_isa, j.x, j.B, j.K, j.W, j.bias, j.r0, j.r1, ba, bb, j.y, j.ldy);
   }, &job);
 }

@@ -881,6 +881,8 @@ hetegen_status hetegen_destroy(hetegen_ctx* ctx) {
 
 const char* hetegen_last_error(const hetegen_ctx* ctx) { return ctx ? ctx->err.c_str() : g_create_error.c_str(); }
 
+const char* hetegen_cpu_share_isa(void) { return hg::cpu_share_isa(); }
+
 hetegen_status hetegen_host_alloc(hetegen_ctx* ctx, size_t bytes, void** p) {
   return api_guard(ctx, [&]() -> hetegen_status {
     if (!ctx || !p || bytes == 0) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "hetegen_host_alloc: bad arguments");

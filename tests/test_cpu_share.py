@@ -25,8 +25,10 @@ def _problem(B, K, N, dtype, kind, seed):
 
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
 @pytest.mark.parametrize("B", [1, 2, 3, 4, 5, 8])
-@pytest.mark.parametrize("K", [8, 24, 520, 1032])
+@pytest.mark.parametrize("K", [8, 24, 48, 520, 1032, 4096])
 def test_random_inputs_match_oracle(dtype, B, K):
+    # K covers a tail of 8, 16 or 24 elements after whole 32-element chunks, no tail, and
+    # shares shorter than one chunk (the bf16 dot-product path works in 32-element chunks)
     N = 77
     x, W, b = _problem(B, K, N, dtype, "normal", seed=K + B)
     ref = oracle.linear(x, W, b, dtype)
@@ -76,7 +78,7 @@ def test_bad_arguments():
 
 
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
-@pytest.mark.parametrize("K", [264, 520, 4104])
+@pytest.mark.parametrize("K", [48, 264, 520, 4104])
 def test_batch_rows_independent(dtype, K):
     # every batch row gets the bits it gets alone (batches of 5-8 run in two groups over
     # L1-resident chunks; the order of each row's products does not change)
