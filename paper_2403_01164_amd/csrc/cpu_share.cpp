@@ -192,8 +192,12 @@ __attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) inline __m512 load
 
 // Software prefetch distance along each weight row: the hardware prefetcher alone
 // leaves a core's memory pipe partly idle (measured on the 16-core Zen 5 host:
-// +10-40 % at batch 1-4).
+// +10-40 % at batch 1-4); at batch 4 twice as far (+2 % on both paths, interleaved A/B).
 constexpr int kPrefetchBytes = 1024;
+template <int B>
+constexpr int prefetch_bytes() {
+  return B == 4 ? 2 * kPrefetchBytes : kPrefetchBytes;
+}
 
 template <bool BF, int B, int R, int UN>
 __attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) void block512(const float* x, int K, const uint16_t* W,
@@ -207,7 +211,7 @@ __attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) void block512(cons
   int k = 0;
   for (; k + 16 * UN <= K; k += 16 * UN) {
     if ((k & 31) == 0)  // one prefetch per 64-byte line of every row (past the end: harmless)
-      for (int i = 0; i < R; ++i) _mm_prefetch((const char*)(w[i] + k) + kPrefetchBytes, _MM_HINT_T0);
+      for (int i = 0; i < R; ++i) _mm_prefetch((const char*)(w[i] + k) + prefetch_bytes<B>(), _MM_HINT_T0);
     for (int u = 0; u < UN; ++u) {
       __m512 wv[R];
       for (int i = 0; i < R; ++i) wv[i] = load16<BF>(w[i] + k + 16 * u);
@@ -339,7 +343,7 @@ HG_BF16_TARGET void block_bf16(const uint16_t* xb, int K, const uint16_t* W, con
   for (int i = 0; i < R; ++i) w[i] = W + (int64_t)(r + i) * K;
   const int K32 = K & ~31;
   for (int k = 0; k < K32; k += 32) {
-    for (int i = 0; i < R; ++i) _mm_prefetch((const char*)(w[i] + k) + kPrefetchBytes, _MM_HINT_T0);
+    for (int i = 0; i < R; ++i) _mm_prefetch((const char*)(w[i] + k) + prefetch_bytes<B>(), _MM_HINT_T0);
     __m512bh wv[R];
     for (int i = 0; i < R; ++i) wv[i] = ld_bh(w[i] + k);
     for (int b = 0; b < B; ++b) {
@@ -422,14 +426,22 @@ typedef void (*BlockBf16Fn)(const uint16_t*, int, const uint16_t*, const uint16_
 template <int B>
 void run_blocks_bf16(const uint16_t* xb, int K, const uint16_t* W, const uint16_t* bias, int r0, int r1, int ba,
                      int bb, float* y, int ldy) {
-  // one group up to B = 6 (B = 5 / 6: 357.7 -> 377.6 / 358.1 -> 370.3 GB/s against two groups)
+  // one group up to B = 6 (B = 5 / 6: 357.7 -> 377.6 / 358.1 -> 370.3 GB/s against two groups);
+  // eight rows per block at B <= 2 (B = 2: 341.4 -> 353.3 GB/s; the same at B = 1)
   constexpr int R = 4;
   const BlockBf16Fn blk = B >= 7 ? block_bf16_split<B, R> : block_bf16<B, R>;
-  for (int i = ba; i < bb; ++i) {
+  const BlockBf16Fn blk8 = B <= 2 ? block_bf16<B, 8> : nullptr;
+  for (int i = ba; i < bb;) {
     const int r = r0 + R * i;
+    if (blk8 && i + 1 < bb && r + 2 * R <= r1) {
+      blk8(xb, K, W, bias, r0, r, y, ldy);
+      i += 2;
+      continue;
+    }
     if (r + R <= r1) blk(xb, K, W, bias, r0, r, y, ldy);
     else
       for (int q = r; q < r1; ++q) block_bf16<B, 1>(xb, K, W, bias, r0, q, y, ldy);
+    ++i;
   }
 }
 
@@ -509,23 +521,34 @@ const bool g_bf16 = detect_bf16();
 
 typedef void (*BlockFn)(const float*, int, const uint16_t*, const uint16_t*, int, int, float*, int);
 
-// Four rows per block (four weight streams per core); the AVX-512 loop is unrolled
-// twice at B <= 4 (at B = 4 on the 16-core Zen 5 host, OPT-30B shapes: 327 -> 372 GB/s),
-// and from B = 5 on the batch runs in two groups per chunk (block512_split).  Blocks [ba, bb) of 4 rows from r0; the
-// last block of the share may be partial.
+// Four rows per block (four weight streams per core), eight at B <= 3 on AVX-512 (the
+// accumulators still fit the registers; interleaved A/B on the 16-core Zen 5 host,
+// OPT-30B fc1 shape: +3-5 % at B = 1-3); the AVX-512 loop is unrolled twice at B <= 4
+// (at B = 4, OPT-30B shapes: 327 -> 372 GB/s) and once with eight rows at B = 3, and
+// from B = 5 on the batch runs in two groups per chunk (block512_split).  Blocks [ba, bb)
+// of 4 rows from r0 (a grain starts at a multiple of 8 of them); the last block of the
+// share may be partial.  A row's sums do not depend on the block it is computed in.
 template <bool BF, int B>
 void run_blocks(Isa isa, const float* x, int K, const uint16_t* W, const uint16_t* bias, int r0, int r1, int ba,
                 int bb, float* y, int ldy) {
   constexpr int R = 4, UN = B <= 4 ? 2 : 1;
+  constexpr bool R8 = B <= 3;
   BlockFn blk = isa != ISA_AVX512 ? block256<BF, B, R>
                 : B >= 5         ? block512_split<BF, B, R>
                                  : block512<BF, B, R, UN>;
+  BlockFn blk8 = isa == ISA_AVX512 && R8 ? block512<BF, B, 8, B <= 2 ? 2 : 1> : nullptr;
   BlockFn one = isa == ISA_AVX512 ? block512<BF, B, 1, 1> : block256<BF, B, 1>;
-  for (int i = ba; i < bb; ++i) {
+  for (int i = ba; i < bb;) {
     const int r = r0 + R * i;
+    if (blk8 && i + 1 < bb && r + 2 * R <= r1) {
+      blk8(x, K, W, bias, r0, r, y, ldy);
+      i += 2;
+      continue;
+    }
     if (r + R <= r1) blk(x, K, W, bias, r0, r, y, ldy);
     else
       for (int q = r; q < r1; ++q) one(x, K, W, bias, r0, q, y, ldy);
+    ++i;
   }
 }
 
