@@ -26,6 +26,11 @@ def test_header_declares_the_calls():
         assert must in names
 
 
+def test_cpu_share_isa_is_reported():
+    # the CPU share's instruction set, chosen when the library loads (no device needed)
+    assert hg.hetegen_cpu_share_isa() in ("avx512+bf16", "avx512", "avx2", "scalar")
+
+
 def test_every_declared_symbol_is_exported():
     import ctypes
     lib = ctypes.CDLL(hg.LIB_PATH)
