@@ -855,6 +855,24 @@ def decode_workload(args, torch, synth, hg):
                                  "outside_linears": round(ms_step - tprof["hetlin_ms"] / args.steps, 3),
                                  "n_cpu_shares": int(tprof["cpu_shares"] // args.steps)},
         }
+        if hbm_b > 0:
+            # a mixed placement: the HBM-resident rows against 8 TB/s (their GEMVs' event-timed
+            # GPU time in the profiled pass), and the rest of the step against the heterogeneous
+            # ideal of the streamed bytes (the resident linears run between them, not beside)
+            res_ms = prof["res_gpu_ms"] / nprof
+            res_b = prof["res_gpu_bytes"] / nprof
+            rest_ms = ms_step - res_ms
+            str_ideal_ms = sb / (v_cpu + v_g) * 1e3
+            result["hetero"]["resident_part"] = {
+                "bytes_per_step": int(res_b), "gpu_ms_per_step": round(res_ms, 3),
+                "GBps": round(res_b / (res_ms * 1e-3) / 1e9, 1) if res_ms > 0 else None,
+                "frac_of_hbm_peak": round(res_b / (res_ms * 1e-3) / (HBM_PEAK_GBPS * 1e9), 4) if res_ms > 0 else None,
+                "measured_as": "events around each resident GEMV launch in the profiled pass"}
+            result["hetero"]["streamed_part"] = {
+                "bytes_per_step": int(sb), "ms_per_step": round(rest_ms, 3),
+                "ideal_ms_per_step": round(str_ideal_ms, 3),
+                "frac_of_ideal": round(str_ideal_ms / rest_ms, 4) if rest_ms > 0 else None,
+                "measured_as": "step time less the resident GEMVs' GPU time"}
         log("hetero: %s" % json.dumps(result["hetero"]))
 
     n_all = args.all_streamed_steps or 0

@@ -500,6 +500,8 @@ typedef struct {
   int64_t cpu_shares;  /* linears computed with CPU rows */
   double hetlin_ms;    /* host time inside those linears (CPU share, the waits above, and enqueueing
                           their kernels and chunk GEMVs) */
+  double res_gpu_ms;   /* the part of gpu_ms spent on HBM-resident rows (not streamed chunks) */
+  double res_gpu_bytes; /* the weight bytes of those launches */
 } hetegen_profile;
 
 /* on != 0: bracket every chunk copy and GEMV launch with events and synchronise at

@@ -52,7 +52,8 @@ class Profile(ctypes.Structure):
                 ("gpu_ms", ctypes.c_double), ("h2d_bytes", ctypes.c_double), ("gpu_bytes", ctypes.c_double),
                 ("cpu_bytes", ctypes.c_double), ("gemv_launches", ctypes.c_int64), ("pin_ms", ctypes.c_double),
                 ("pin_bytes", ctypes.c_double), ("xwait_ms", ctypes.c_double), ("tailwait_ms", ctypes.c_double),
-                ("cpu_shares", ctypes.c_int64), ("hetlin_ms", ctypes.c_double)]
+                ("cpu_shares", ctypes.c_int64), ("hetlin_ms", ctypes.c_double), ("res_gpu_ms", ctypes.c_double),
+                ("res_gpu_bytes", ctypes.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -357,10 +357,14 @@ hetegen_status flush_profile(hetegen_ctx* ctx) {
     if (t.kind == 0) {
       ctx->prof.h2d_ms += ms;
       ctx->prof.h2d_bytes += t.bytes;
-    } else {
+    } else {  // 1: a GEMV of streamed chunk rows, 2: of resident rows
       ctx->prof.gpu_ms += ms;
       ctx->prof.gpu_bytes += t.bytes;
       ctx->prof.gemv_launches++;
+      if (t.kind == 2) {
+        ctx->prof.res_gpu_ms += ms;
+        ctx->prof.res_gpu_bytes += t.bytes;
+      }
     }
     ctx->ev_pool.push_back(t.a);
     ctx->ev_pool.push_back(t.b);
@@ -594,7 +598,7 @@ struct Job {
 };
 
 hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long ldx, int ln, const void* W, int row0,
-                        int rows, hipStream_t st, void* h_out, bool tiled = false) {
+                        int rows, hipStream_t st, void* h_out, bool tiled = false, bool resident = false) {
   hg::GemvParams p{};
   const size_t ys = j.y_f32 ? 4 : 2;
   p.x = x;
@@ -612,7 +616,7 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
   p.epi = j.epi;
   p.y_f32 = j.y_f32;
   p.ln = ln;
-  TimedScope ts(ctx, st, 1, (double)rows * j.K * 2);
+  TimedScope ts(ctx, st, resident ? 2 : 1, (double)rows * j.K * 2);
   if (tiled) {
     p.ws = j.ws;
     p.cnt = j.cnt;
@@ -688,7 +692,7 @@ hetegen_status run_linear(hetegen_ctx* ctx, const Job& j, hipStream_t st) {
   };
   if (j.n_gpu > 0 && j.W_dev)
     TRY(run_gemv(ctx, j, xin, ldin, fused_ln ? 1 : 0, j.W_dev, 0, j.n_gpu, st, fused_ln ? j.trace_in : nullptr,
-                 j.tiled));
+                 j.tiled, true));
   while (streamed && r0 < j.n_gpu) {
     bool did = false;
     TRY(next_chunk(j.n_cpu == 0, &did));
