@@ -590,6 +590,21 @@ def decode_workload(args, torch, synth, hg):
             log("probe %s [%d,%d]: V_CPU %.1f GB/s, V_COM %.1f GB/s, V_GPU %.0f GB/s, V_PIN %.1f GB/s (%.1f s)" %
                 (NAMES[m], n, k, p["cpu_Bps"] / 1e9, p["h2d_Bps"] / 1e9, p["hbm_gemv_Bps"] / 1e9,
                  p["pin_Bps"] / 1e9, time.time() - t0))
+        # the host is shared with other tenants: a probe whose CPU rate falls below 3/4 of the
+        # best linear's was slowed while it ran (the shapes' CPU rates differ by far less), so it
+        # is taken again, up to twice, keeping the faster result; the planner and the Eq. 4 ideal
+        # both read these rates
+        for m in range(4):
+            for again in range(2):
+                best = max(probe[q]["cpu_Bps"] for q in NAMES)
+                if probe[NAMES[m]]["cpu_Bps"] >= 0.75 * best:
+                    break
+                n, k = shp[last + m]
+                p = hg.hetegen_probe(ctx, W[last + m], n, k, dt, B, 3, hg.PROBE_CONCURRENT)
+                log("probe %s again: V_CPU %.1f GB/s (was %.1f)" %
+                    (NAMES[m], p["cpu_Bps"] / 1e9, probe[NAMES[m]]["cpu_Bps"] / 1e9))
+                if p["cpu_Bps"] > probe[NAMES[m]]["cpu_Bps"]:
+                    probe[NAMES[m]] = p
         bws = [tuple(probe[NAMES[i % 4]][f] for f in ("cpu_Bps", "h2d_Bps", "hbm_gemv_Bps", "pin_Bps"))
                for i in range(4 * L)]
     # fresh input per step, resident in HBM before timing
