@@ -615,17 +615,27 @@ def decode_workload(args, torch, synth, hg):
     out = torch.empty((2, B, H), dtype=torch.int16, device="cuda")
 
     if placement == "sched":
-        # module scheduler (Sec. 4.5, Eq. 13): T_CPU of each module is its CPU time at
-        # the planned split (CPU rows x K x 2 bytes over the probed CPU speed of its
-        # shape, Eq. 11 read off the distribution law), against the HBM bytes of its
-        # resident copy
+        # module scheduler (Sec. 4.5, Eq. 13): T_CPU of each module is its benchmarked time
+        # in heterogeneous mode, against the HBM bytes of its resident copy.  A model with
+        # every linear heterogeneous at the planned split runs a few steps, and each linear's
+        # share of the calling thread's critical path (hetegen_model_linear_ms: its CPU share,
+        # the waits around it and the hand-offs) is averaged over them; the fixed cost of a
+        # hand-off makes small modules gain more per byte than their CPU time alone says.
         a_all = hg.hetegen_layer_plan([(n, k, dt, 0) for n, k in shp], bws)
-        t_het = [a_all[i] * n * k * 2 / bws[i][0] for i, (n, k) in enumerate(shp)]
+        tmp = hg.hetegen_model_create(ctx, L, H, F, dt, W, b, a_all, [0] * (4 * L), max(B, args.max_batch, 1))
+        t_het, nb = [0.0] * (4 * L), 3
+        for t in range(nb + 1):  # the first step warms up
+            hg.hetegen_decode_step(ctx, tmp, xs[t % nstep].data_ptr(), out[0].data_ptr(), B, sptr)
+            torch.cuda.synchronize()
+            if t > 0:
+                t_het = [a + ms * 1e-3 / nb for a, ms in zip(t_het, hg.hetegen_model_linear_ms(tmp, 4 * L))]
+        hg.hetegen_model_destroy(ctx, tmp)
         mem = [float(n * k * 2) for n, k in shp]
         budget = args.hbm_budget * 1e9 if args.hbm_budget is not None else sum(mem) / 2
         resident, used = hg.hetegen_module_schedule(t_het, mem, [i // 4 for i in range(4 * L)], budget)
         streamed = [i for i in range(4 * L) if not resident[i]]
-        schedule = {"hbm_budget_GB": round(budget / 1e9, 3), "resident_GB": round(used / 1e9, 3),
+        schedule = {"T_is": "benchmarked: each linear's time with every linear heterogeneous, mean of %d steps" % nb,
+                    "hbm_budget_GB": round(budget / 1e9, 3), "resident_GB": round(used / 1e9, 3),
                     "resident_modules": sum(resident),
                     "resident_by_linear": {NAMES[m]: sum(resident[m::4]) for m in range(4)},
                     "gain_s_per_GB_mean": {NAMES[m]: round(float(np.mean([t_het[i] / mem[i] * 1e9
