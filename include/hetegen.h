@@ -262,7 +262,9 @@ HETEGEN_API hetegen_status hetegen_probe_launch(hetegen_ctx* ctx, int reps, void
  *   y[b * ldy + (j - r0)] = sum_k x[b * K + k] * W[j * K + k] + bias[j],
  *   j in [r0, r1), b < B,
  * x binary32 [B, K] host, W [N, K] host (pinned or pageable), bias host [N] or NULL,
- * y binary32 host.  Binary32 accumulation, 16-bit weights widened exactly.
+ * y binary32 host.  Binary32 accumulation, 16-bit weights widened exactly (with bf16
+ * weights and every x value a bf16 value, on AVX512-BF16 hosts: bf16 pair products, exact,
+ * added to binary32 lanes; bf16 subnormals count as zero there).
  * threads <= 0: the OpenMP default thread count.  B in [1, 8], K % 8 == 0, 0 <= r0 <= r1. */
 HETEGEN_API hetegen_status hetegen_cpu_linear(const float* x, int B, int K, const void* W_host, hetegen_dtype dtype,
                                               const void* bias_host, int r0, int r1, float* y, int ldy, int threads);

@@ -305,7 +305,8 @@ __attribute__((target("avx512f,avx512bw,avx512vl,f16c,fma"))) void block512_spli
 
 // ---------------- AVX512-BF16 (bf16 weights) ----------------
 // x [B, K] arrives as binary32 values that are bf16 values (the activation type), so it
-// is narrowed to bf16 exactly, once per call.  vdpbf16ps multiplies bf16 pairs exactly
+// is narrowed to bf16 exactly, once per call; x with any value that bf16 cannot hold
+// (low 16 bits set: possible through hetegen_cpu_linear) takes the widening path.  vdpbf16ps multiplies bf16 pairs exactly
 // and adds them to binary32 lanes (lane j of a 32-element chunk takes elements 2j and
 // 2j + 1); like every bf16 instruction of this extension it treats bf16 subnormal
 // inputs as zero and flushes binary32 subnormal results (|v| < 2^-126), far below the
@@ -319,18 +320,28 @@ HG_BF16_TARGET inline __m512bh ld_bh_tail(const uint16_t* p, int n) {  // n < 32
   return (__m512bh)_mm512_maskz_loadu_epi16((__mmask32)((1u << n) - 1u), p);
 }
 
-// x (binary32, exact bf16 values) -> bf16 [B, K]
-HG_BF16_TARGET void narrow_bf16(const float* x, int n, uint16_t* out) {
+// x (binary32) -> bf16 [B, K]: the upper halves of the binary32 patterns; returns whether
+// every value was a bf16 value (lower half zero), i.e. the narrowing was exact
+HG_BF16_TARGET bool narrow_bf16(const float* x, int n, uint16_t* out) {
+  const __m512i low = _mm512_set1_epi32(0xFFFF);
+  __mmask16 inexact = 0;
   int i = 0;
   for (; i + 32 <= n; i += 32) {
-    const __m512bh v = _mm512_cvtne2ps_pbh(_mm512_loadu_ps(x + i + 16), _mm512_loadu_ps(x + i));
-    _mm512_storeu_si512((void*)(out + i), (__m512i)v);
+    const __m512i lo = _mm512_loadu_si512((const void*)(x + i)), hi = _mm512_loadu_si512((const void*)(x + i + 16));
+    inexact |= _mm512_test_epi32_mask(lo, low) | _mm512_test_epi32_mask(hi, low);
+    // the upper 16 bits of each lane, in lane order: 32 bf16 values
+    const __m512i idx = _mm512_set_epi16(63, 61, 59, 57, 55, 53, 51, 49, 47, 45, 43, 41, 39, 37, 35, 33, 31, 29, 27, 25,
+                                         23, 21, 19, 17, 15, 13, 11, 9, 7, 5, 3, 1);
+    _mm512_storeu_si512((void*)(out + i), _mm512_permutex2var_epi16(lo, idx, hi));
   }
+  bool exact = inexact == 0;
   for (; i < n; ++i) {
     uint32_t b;
     memcpy(&b, x + i, 4);
+    exact = exact && (b & 0xFFFFu) == 0;
     out[i] = (uint16_t)(b >> 16);
   }
+  return exact;
 }
 
 template <int B, int R>
@@ -603,8 +614,7 @@ void cpu_share(const float* x, int B, int K, const uint16_t* W, int dtype, const
     // the calling thread's buffer: it stays valid while the job runs (the caller takes part)
     thread_local std::vector<uint16_t> xb;
     if (xb.size() < (size_t)B * K) xb.resize((size_t)B * K);
-    narrow_bf16(x, B * K, xb.data());
-    job.xb = xb.data();
+    if (narrow_bf16(x, B * K, xb.data())) job.xb = xb.data();
   }
   if (g_isa == ISA_SCALAR) {
     Team::get().run(nt, n, [](void* a, int g) {

@@ -60,6 +60,25 @@ def test_same_bits_for_any_thread_count_and_row_range(B):
     assert np.array_equal(part, full[:, 37:151])
 
 
+@pytest.mark.parametrize("K", [8, 40, 1032])
+def test_bf16_weights_keep_binary32_x(K):
+    # x values that bf16 cannot hold (1 + 2^-10) with bf16 weights of 1 (and of 2 in one
+    # row): the exact binary32 sums, not those of x rounded to bf16; and bf16 x values on
+    # the same weights still give exact sums (the dot-product path where the host has it)
+    B, N = 2, 9
+    one, two = 0x3F80, 0x4000  # bf16 bit patterns of 1 and 2
+    W = np.full((N, K), one, np.uint16)
+    W[3] = two
+    xf = np.full((B, K), 1.0 + 2.0 ** -10, np.float32)
+    xf[1, ::2] = 1.0  # a second row mixing bf16 values in
+    y = hg.hetegen_cpu_linear(xf, W.ctypes.data, 0, synth.BF16, 0, N)
+    ref = xf.astype(np.float64).sum(axis=1)[:, None] * np.where(np.arange(N) == 3, 2.0, 1.0)[None, :]
+    assert np.array_equal(y.astype(np.float64), ref)
+    xb = np.full((B, K), 1.5, np.float32)
+    y = hg.hetegen_cpu_linear(xb, W.ctypes.data, 0, synth.BF16, 0, N)
+    assert np.array_equal(y.astype(np.float64), 1.5 * K * np.where(np.arange(N) == 3, 2.0, 1.0)[None, :].repeat(B, 0))
+
+
 def test_no_bias_and_empty_range():
     dtype, B, K, N = synth.BF16, 2, 64, 10
     x, W, b = _problem(B, K, N, dtype, "normal", seed=5)
