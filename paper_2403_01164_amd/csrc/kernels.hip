@@ -737,78 +737,80 @@ constexpr int kTileRows = 16, kTileK = 32;
 constexpr int kLnGroup = 16;    // elements per LayerNorm partial
 constexpr int kLnSlots = 8;     // batch rows per partial group (the largest batch)
 constexpr int kLnMaxGroups = kMaxLnK / kLnGroup;
-constexpr int kLnPerThread = (kLnMaxGroups + kThreads - 1) / kThreads;
 
 // LayerNorm statistics of B rows from their partials (see ln_partials_floats): the mean
 // is the sum of the group sums over K, and the variance combines each group's squared
 // deviations with its count times the squared distance of its mean from the row mean
 // (the pairwise combination of Chan, Golub and LeVeque), so no large sums of squares
-// are subtracted.  Thread t takes groups t + 256 i in increasing i, then the lanes and
-// wavefronts are combined in a fixed tree: every workgroup gets the same bits.
+// are subtracted.  Wavefront w owns batch rows 2w and 2w + 1 (one 16-byte load per
+// group holds both rows' pairs): lane l takes groups l + 64 i in increasing i, and the
+// lanes are combined in a fixed DPP tree, so every workgroup gets the same bits with no
+// reduction across wavefronts; one barrier publishes the statistics.
+constexpr int kLnGroupsPerLane = kLnMaxGroups / 64;
+
 template <int B>
-__device__ __forceinline__ void ln_partials_load(const float* __restrict__ pt, int K, f32x2 (&v)[kLnPerThread][B]) {
-  const int QG = (K + kLnGroup - 1) / kLnGroup;
-  // rounds of 256 groups: the same for the whole workgroup (a scalar branch); a thread past
-  // the last group of a round rereads it and the reduction drops it
-  const int rounds = (QG + kThreads - 1) / kThreads;
+__device__ __forceinline__ void ln_partials_load(const float* __restrict__ pt, int K,
+                                                 f32x4 (&v)[kLnGroupsPerLane]) {
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int QG = (K + kLnGroup - 1) / kLnGroup, rounds = (QG + 63) / 64;  // the same for the workgroup
+  if (2 * wave >= B) return;
+  // a lane past the last group of a round rereads it (the reduction drops it); slot 2w + 1
+  // past B holds nothing this launch uses
 #pragma unroll
-  for (int i = 0; i < kLnPerThread; ++i) {
-    const int q = min((int)threadIdx.x + kThreads * i, QG - 1);
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-      v[i][b] = i < rounds ? *gmem((const f32x2*)pt + (size_t)q * kLnSlots + b) : f32x2{0.f, 0.f};
-  }
+  for (int i = 0; i < kLnGroupsPerLane; ++i)
+    if (i < rounds) {
+      const int q = min(lane + 64 * i, QG - 1);
+      v[i] = *gmem((const f32x4*)(pt + ((size_t)q * kLnSlots + 2 * wave) * 2));
+    }
 }
 
 template <int B>
-__device__ __forceinline__ void ln_partials_reduce(const f32x2 (&v)[kLnPerThread][B], int K, float* mean,
-                                                   float* rstd, float (*red)[kLnSlots][kWaves]) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int QG = (K + kLnGroup - 1) / kLnGroup;
-  float s[B];
+__device__ __forceinline__ void ln_partials_reduce(const f32x4 (&v)[kLnGroupsPerLane], int K,
+                                                   float (*st)[2]) {
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int QG = (K + kLnGroup - 1) / kLnGroup, rounds = (QG + 63) / 64;
+  if (2 * wave < B) {
+    const float inv_k = 1.0f / (float)K;
+    float s0 = 0.f, s1 = 0.f;
 #pragma unroll
-  for (int b = 0; b < B; ++b) {
-    s[b] = 0.f;
+    for (int i = 0; i < kLnGroupsPerLane; ++i)
+      if (i < rounds && lane + 64 * i < QG) {
+        s0 += v[i].x;
+        s1 += v[i].z;
+      }
+    const float m0 = wave_sum(s0) * inv_k, m1 = wave_sum(s1) * inv_k;
+    float t0 = 0.f, t1 = 0.f;
 #pragma unroll
-    for (int i = 0; i < kLnPerThread; ++i) s[b] += tid + kThreads * i < QG ? v[i][b].x : 0.f;
-    s[b] = wave_sum(s[b]);
-  }
-  if (lane == 0)
-#pragma unroll
-    for (int b = 0; b < B; ++b) red[0][b][wave] = s[b];
-  __syncthreads();
-#pragma unroll
-  for (int b = 0; b < B; ++b) {
-    mean[b] = ((red[0][b][0] + red[0][b][1]) + (red[0][b][2] + red[0][b][3])) / (float)K;
-    s[b] = 0.f;
-#pragma unroll
-    for (int i = 0; i < kLnPerThread; ++i) {
-      const int q = tid + kThreads * i;
-      // a group holds 16 elements, or 8 (the last one when K % 16 == 8; K % 8 == 0): the
-      // group mean is its sum times an exact power-of-two reciprocal
-      const bool full = K - kLnGroup * q >= kLnGroup;
-      if (q < QG) {
-        const float d = v[i][b].x * (full ? 1.f / kLnGroup : 0.125f) - mean[b];
-        s[b] += v[i][b].y + (full ? (float)kLnGroup : 8.f) * d * d;
+    for (int i = 0; i < kLnGroupsPerLane; ++i) {
+      const int q = lane + 64 * i;
+      if (i < rounds && q < QG) {
+        // a group holds 16 elements, or 8 (the last one when K % 16 == 8; K % 8 == 0): its
+        // mean is its sum times an exact power-of-two reciprocal
+        const bool full = K - kLnGroup * q >= kLnGroup;
+        const float n = full ? (float)kLnGroup : 8.f, inv_n = full ? 1.f / kLnGroup : 0.125f;
+        const float d0 = v[i].x * inv_n - m0, d1 = v[i].z * inv_n - m1;
+        t0 += v[i].y + n * d0 * d0;
+        t1 += v[i].w + n * d1 * d1;
       }
     }
-    s[b] = wave_sum(s[b]);
+    t0 = wave_sum(t0);
+    t1 = wave_sum(t1);
+    if (lane == 0) {
+      st[2 * wave][0] = m0;
+      st[2 * wave][1] = 1.0f / sqrtf(t0 * inv_k + kLnEps);
+      if (2 * wave + 1 < B) {
+        st[2 * wave + 1][0] = m1;
+        st[2 * wave + 1][1] = 1.0f / sqrtf(t1 * inv_k + kLnEps);
+      }
+    }
   }
-  if (lane == 0)
-#pragma unroll
-    for (int b = 0; b < B; ++b) red[1][b][wave] = s[b];
   __syncthreads();
-#pragma unroll
-  for (int b = 0; b < B; ++b) {
-    const float var = ((red[1][b][0] + red[1][b][1]) + (red[1][b][2] + red[1][b][3])) / (float)K;
-    rstd[b] = 1.0f / sqrtf(var + kLnEps);
-  }
 }
 
 template <class T, int B, int U, bool LN>
 __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G) {
   __shared__ float part[kWaves][4][64];
-  __shared__ float red[2][kLnSlots][kWaves];
+  __shared__ float lnst[kLnSlots][2];  // LN: mean and 1 / sqrt(var + eps) of each batch row
   __shared__ int last;
   // the wavefront index through a scalar register: every tile bound below is then
   // wave-uniform and the skipped products are skipped by a branch.  A condition the
@@ -861,7 +863,7 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
   Buf fa, fb;
   // the LayerNorm partials are requested before the first weights, so that waiting for
   // them leaves the weight loads in flight
-  f32x2 lnv[LN ? kLnPerThread : 1][B];
+  f32x4 lnv[LN ? kLnGroupsPerLane : 1];
   if constexpr (LN) {
     ln_partials_load<B>(p.ln_in, K, lnv);
     __builtin_amdgcn_sched_barrier(0);  // keep them ahead of the weight loads
@@ -870,28 +872,17 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
   // wavefront without tiles rereads tile k1 - 1 >= 0 and computes nothing)
   if (LN || nst > 0) load(0, fa);
   if constexpr (LN) {
-    float mean[B], rstd[B];
-    ln_partials_reduce<B>(lnv, K, mean, rstd, red);
-#pragma unroll
-    for (int q = 0; q < B; ++q)
-      if (q == b) {
-        ln_a = rstd[q];
-        ln_c = -mean[q] * rstd[q];
-      }
+    ln_partials_reduce<B>(lnv, K, lnst);
+    ln_a = lnst[b][1];
+    ln_c = -lnst[b][0] * lnst[b][1];
     if (p.h_out && blockIdx.x == 0) {
       // the normalised input, for a caller that records it
       const int n8 = K >> 3;
       for (int c = threadIdx.x; c < B * n8; c += kThreads) {
         const int r = c / n8, cc = c - r * n8;
-        float a = 0.f, cr = 0.f;
-#pragma unroll
-        for (int q = 0; q < B; ++q)
-          if (q == r) {
-            a = rstd[q];
-            cr = -mean[q] * rstd[q];
-          }
         const uint4 xv = load_g16((const uint4*)((const uint16_t*)p.x + (long long)r * p.ldx + 8 * cc));
-        *(uint4*)((uint16_t*)p.h_out + (long long)r * p.ldh + 8 * cc) = normalize8_fma<T>(xv, a, cr);
+        *(uint4*)((uint16_t*)p.h_out + (long long)r * p.ldh + 8 * cc) =
+            normalize8_fma<T>(xv, lnst[r][1], -lnst[r][0] * lnst[r][1]);
       }
     }
   }
