@@ -656,10 +656,12 @@ def decode_workload(args, torch, synth, hg):
 
     P = args.context
     if P > 0:
-        # KV cache for positions [0, P + warmup + steps); positions [0, P) get synthetic
-        # keys and values (the same for every layer), step t decodes position P + t
+        # KV cache for positions [0, P + warmup + steps) and those of the extra passes (an alpha
+        # sweep, the all-streamed point); positions [0, P) get synthetic keys and values (the
+        # same for every layer), step t decodes position P + t
         hd = 128
-        hg.hetegen_model_kv_create(ctx, model, P + nstep, hd)
+        kv_len = P + max(nstep, 1 + args.sweep_steps, 1 + (args.all_streamed_steps or 0))
+        hg.hetegen_model_kv_create(ctx, model, kv_len, hd)
         kd = torch.from_numpy(synth.normal((B, P, H), dt, 0, 7001).view(np.int16)).cuda()
         vd = torch.from_numpy(synth.normal((B, P, H), dt, 0, 7002).view(np.int16)).cuda()
         for l in range(L):
@@ -668,10 +670,12 @@ def decode_workload(args, torch, synth, hg):
         del kd, vd
 
     def step(t):
+        # step t decodes position P + t (KV cache); the extra passes (sweeps, the all-streamed
+        # point) reuse the per-step inputs in turn
         if P > 0:
-            hg.hetegen_decode_step_kv(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, P + t, sptr)
+            hg.hetegen_decode_step_kv(ctx, model, xs[t % nstep].data_ptr(), out[t % 2].data_ptr(), B, P + t, sptr)
         else:
-            hg.hetegen_decode_step(ctx, model, xs[t].data_ptr(), out[t % 2].data_ptr(), B, sptr)
+            hg.hetegen_decode_step(ctx, model, xs[t % nstep].data_ptr(), out[t % 2].data_ptr(), B, sptr)
 
     refined = None
     if args.alpha_bench and streamed and args.alpha is None:
