@@ -362,12 +362,26 @@ def table2_linear(args, torch, synth, hg):
     hg.hetegen_destroy(ctx)
 
 
-def mfma_splits(K):
-    """Splits of the sum over K in the matrix-core GEMV (the library's rule)."""
-    kt, g = (K + 31) // 32, 1
-    while g < 8 and kt // (2 * g) >= 128:
+def mfma_splits(rows, K, cus):
+    """Splits of the sum over K in the matrix-core GEMV on a device of `cus` compute units
+    (the library's rule: unsplit unless one workgroup per 16-row tile loads the units more
+    than 1.15x unevenly; then the fewest splits of at least 32 k-tiles that do not, or the
+    most even)."""
+    def uneven(wgs):
+        return -(-wgs // cus) * cus / wgs
+    rt, kt = -(-rows // 16), -(-K // 32)
+    best, best_u = 1, uneven(rt)
+    if best_u <= 1.15:
+        return 1
+    g = 2
+    while g <= 8 and kt // g >= 32:
+        u = uneven(rt * g)
+        if u <= 1.15:
+            return g
+        if u < best_u:
+            best, best_u = g, u
         g *= 2
-    return g
+    return best
 
 
 def ln_partials_on():
@@ -376,24 +390,27 @@ def ln_partials_on():
     return os.environ.get("HETEGEN_LN_PARTIALS") != "0"
 
 
-def gemv_label(B, H, F, dt, tiled, partials=True):
+def gemv_label(B, H, F, dt, tiled, partials=True, cus=256):
     """GEMV kernels an all-resident eager step at batch B runs (the library's dispatch rules;
     tiled: the step runs the tile-ordered copy of the weights; partials: with LayerNorm
-    partials between its matrix-core linears)."""
+    partials between its matrix-core linears; cus: the device's compute units)."""
     t = "BF16" if dt == 1 else "F16"
     if tiled:
         parts = {}
         for name, (n, k) in zip(NAMES, shapes(H, F)):
-            g = mfma_splits(k)
-            split = "" if g == 1 else " (K split %d)" % g
+            g = mfma_splits(n, k, cus)
+            wgs = -(-n // 16) * g
+            kmajor = wgs % cus == 0 and wgs // cus <= 4  # the library's tile order rule
+            split = ("" if g == 1 else " (K split %d)" % g) + (" k-major" if kmajor else "")
+            u = 4 if (g > 1 or B == 1 or -(-k // 32) >= 512) else 8  # tiles per request, no LayerNorm
             if partials and name in ("qkv", "fc1"):
                 key = "gemv_mfma_kernel<%s,%d,4,LayerNorm from partials>%s" % (t, B, split)
                 parts.setdefault(key, []).append("qkv after layer 0" if name == "qkv" else name)
                 if name == "qkv":
-                    key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, 8 if g == 1 else 4, split)
+                    key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, u, split)
                     parts.setdefault(key, []).append("layer 0's qkv")
                 continue
-            key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, 8 if g == 1 else 4, split)
+            key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, u, split)
             parts.setdefault(key, []).append(name)
         ni = -(-H // 2048)
         ni = ni if ni <= 5 else 8
@@ -791,7 +808,8 @@ def decode_workload(args, torch, synth, hg):
         layouts = hg.hetegen_model_layouts(model)
         tiled_used = bool(layouts & hg.LAYOUT_TILED) and (B >= 3 or not layouts & hg.LAYOUT_ROWMAJOR)
         kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
-            else gemv_label(B, H, F, dt, tiled_used, ln_partials_on())
+            else gemv_label(B, H, F, dt, tiled_used, ln_partials_on(),
+                            torch.cuda.get_device_properties(0).multi_processor_count)
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
         read_gbps = hg.hetegen_probe_hbm(ctx, 4 << 30, 5) / 1e9
@@ -812,7 +830,8 @@ def decode_workload(args, torch, synth, hg):
                               "read_same_launches_ms": round(read_step_ms, 5),
                               "frac_of_read_same_launches": round(read_step_ms / ms_step, 4)}
         result["config"]["weight_layouts"] = "+".join(n for f, n in ((hg.LAYOUT_ROWMAJOR, "row-major"),
-                                                                    (hg.LAYOUT_TILED, "tiled")) if layouts & f)
+                                                                    (hg.LAYOUT_TILED, "tiled"),
+                                                                    (hg.LAYOUT_KMAJOR, "k-major")) if layouts & f)
         if tiled_used and exec_mode != "persistent":
             # the timed region also holds the LayerNorm launches (B x H x 2 bytes read and written
             # each): before layer 0's qkv, or before every qkv and fc1 without the partials; they

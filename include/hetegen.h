@@ -157,9 +157,12 @@ HETEGEN_API hetegen_status hetegen_tile_weights(hetegen_ctx* ctx, const void* W_
 /* y[b, j] = sum_k x[b, k] * W[j, k] + bias[j] for all N rows on the GPU, W given in
  * tile order (hetegen_tile_weights).  x_dev [B, K] and y_dev [B, N] (row strides K
  * and N) as in hetegen_linear; bias_dev optional device [N].  Binary32 sums (the
- * matrix core's products of 16-bit values are exact); for K of 8192 and more the
- * sum over K is split over up to 8 workgroups whose partial sums are added in a
- * fixed order, so results do not depend on timing.  Uses the context's split-K
+ * matrix core's products of 16-bit values are exact).  When one workgroup per 16-row
+ * tile would load the device's compute units unevenly (the busiest more than 1.15x
+ * the mean), the sum over K is split over up to 8 workgroups (each at least 32
+ * 32-column tiles long) whose partial sums are added in a fixed order: the split
+ * depends on N, K and the device's compute-unit count, not on B or timing, so a
+ * batch row's bits do not depend on the batch size.  Uses the context's split-K
  * workspace, which the first call with a larger need allocates (device memory,
  * after waiting for the device); calls on one context must not overlap.  Enqueued
  * on `stream`.  B in [1, 8], K % 8 == 0, N >= 1. */
@@ -172,11 +175,13 @@ HETEGEN_API hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_
  * HIP graph capture, tight serving loops, harnesses that forbid allocation): same
  * arguments and results, but the split-K partials and arrival counters live in a
  * fixed scratch array compiled into the library, one per GPU, set up by
- * hetegen_create and held until the process ends (4 MiB of partials and 65536
- * counters, 4.25 MiB per GPU).  The call allocates nothing; it returns UNSUPPORTED,
- * without launching, for a shape whose split needs more than that, i.e.
- * ceil(N / 16) * splits * 16 * B floats with splits = 2, 4 or 8 for K of 8192, 16384
- * or 32768 and more (OPT-66B's fc2 [9216, 36864] at batch 8 needs 589824).  Every
+ * hetegen_create and held until the process ends (262144 floats of partials and
+ * 65536 counters, 1.25 MiB per GPU).  The call allocates nothing; it returns
+ * UNSUPPORTED, without launching, for a shape whose split (see hetegen_linear_tiled)
+ * needs more than that, i.e. ceil(N / 16) * splits * 16 * B floats.  On a 256-CU
+ * device every linear of OPT-6.7B to OPT-175B fits at batch 8 (the largest need,
+ * OPT-13B's [5120, 5120] and [5120, 20480] in 4 splits, is 163840 floats); a split
+ * linear of more than 1024 row tiles at batch 8, such as [16400, 36864], does not.  Every
  * call on one GPU shares that GPU's scratch: calls that overlap on one GPU (from
  * several streams, contexts or threads) race and give undefined results.  A launch
  * returns the counters it used to zero, so calls in stream order need no clearing. */
@@ -345,9 +350,13 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * also leave per-16-element LayerNorm partials of their output (sum, sum of squared
  * deviations), and fc1 / qkv normalise their input from them instead of after a
  * LayerNorm launch (Chan-Golub-LeVeque combination in a fixed order; the variable
- * HETEGEN_LN_PARTIALS=0 at creation keeps the LayerNorm launches).  Results do not
- * depend on the layout or the LayerNorm path beyond rounding (all pass the oracle's
- * tolerance). */
+ * HETEGEN_LN_PARTIALS=0 at creation keeps the LayerNorm launches).  A tiled linear
+ * whose matrix-core grid puts the same number of workgroups, 1 to 4, on every compute
+ * unit keeps its tiles k-major (k-tile kt of row tile rt at tile kt * ceil(n_gpu / 16) +
+ * rt), so that workgroups walking K side by side read one contiguous window; the others
+ * keep hetegen_tile_weights' order (HETEGEN_TILE_KORDER=0 or 1 at creation: one order for
+ * every linear).  The tile order does not change the bits.  Results do not depend on
+ * the layout or the LayerNorm path beyond rounding (all pass the oracle's tolerance). */
 HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
                                     void* const* W_host, void* const* bias_host, const double* alpha,
                                     const int* resident, int max_batch, hetegen_model** out);
@@ -390,10 +399,11 @@ HETEGEN_API hetegen_status hetegen_model_set_exec(hetegen_model* model, int mode
 HETEGEN_API int hetegen_model_last_exec(const hetegen_model* model);
 
 /* Layouts of the model's resident rows (see hetegen_model_create): a bitwise OR of
- * HETEGEN_LAYOUT_ROWMAJOR and HETEGEN_LAYOUT_TILED (0 for NULL or no resident rows
- * kept in either). */
+ * HETEGEN_LAYOUT_ROWMAJOR, HETEGEN_LAYOUT_TILED and HETEGEN_LAYOUT_KMAJOR (some tiled
+ * linear keeps its tiles k-major), 0 for NULL or no resident rows kept in either. */
 #define HETEGEN_LAYOUT_ROWMAJOR 1
 #define HETEGEN_LAYOUT_TILED 2
+#define HETEGEN_LAYOUT_KMAJOR 4
 HETEGEN_API int hetegen_model_layouts(const hetegen_model* model);
 
 /* Alpha benchmark at the granularity of the decode step (Sec. 4.4 applied to the

@@ -148,6 +148,7 @@ struct hetegen_model {
     bool pageable = false;     // W_host is plain host memory (staged when streamed)
     void* W_dev = nullptr;     // rows [0, n_gpu) when resident, row-major (batches 1-2 and row-major models)
     void* W_tile = nullptr;    // the same rows in matrix-core tile order (tiled models)
+    int korder = 0;            // W_tile's order: 0 row-tile order, 1 k-major (hg::mfma_kmajor)
     void* bias_dev = nullptr;  // all N biases
   };
   int L = 0, H = 0, F = 0, dtype = 0, max_batch = 1;
@@ -156,6 +157,7 @@ struct hetegen_model {
                                // both copies fit, see hetegen_model_create)
   float* ws = nullptr;         // split-K partials of the matrix-core GEMV
   uint32_t* ws_cnt = nullptr;  // its arrival counters, zero between launches
+  size_t ws_floats = 0, ws_words = 0;
   float* ln_part = nullptr;    // LayerNorm partials of x after out / fc2 (two buffers of
                                // ln_partials_floats(H)), for the tiled GEMVs of fc1 / qkv
   bool ln_partials = true;     // use them (HETEGEN_LN_PARTIALS=0 at creation: LayerNorm launches)
@@ -593,6 +595,8 @@ struct Job {
   bool tiled;       // W_dev is in matrix-core tile order (matrix-core GEMV)
   float* ws;        // its split-K workspace
   uint32_t* cnt;
+  size_t ws_floats, cnt_words;
+  int korder;       // tiled: W_dev's tile order
   const float* ln_in;  // tiled, ln, all rows resident: LayerNorm from these partials of x
   float* ln_out;       // tiled, all rows resident: also write the partials of y here
 };
@@ -620,6 +624,9 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
   if (tiled) {
     p.ws = j.ws;
     p.cnt = j.cnt;
+    p.ws_floats = j.ws_floats;
+    p.cnt_words = j.cnt_words;
+    p.korder = j.korder;
     p.ln_in = ln ? j.ln_in : nullptr;
     p.ln_out = j.ln_out;
     HIPCHK(ctx, hg::launch_gemv_mfma(p, j.dtype, j.B, st));
@@ -1042,6 +1049,8 @@ hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_dev, int B, 
     p.y_f32 = y_dtype == HETEGEN_F32;
     p.ws = ctx->ws;
     p.cnt = ctx->ws_cnt;
+    p.ws_floats = ctx->ws_floats;
+    p.cnt_words = ctx->ws_words;
     TimedScope ts(ctx, st, 1, (double)N * K * 2);
     HIPCHK(ctx, hg::launch_gemv_mfma(p, w_dtype, B, st));
     ts.end();
@@ -1087,6 +1096,8 @@ hetegen_status hetegen_linear_tiled_noalloc(hetegen_ctx* ctx, const void* x_dev,
     p.y_f32 = y_dtype == HETEGEN_F32;
     p.cnt = base;
     p.ws = (float*)(base + hg::kScratchCounterWords);
+    p.cnt_words = hg::kScratchCounterWords;
+    p.ws_floats = hg::kScratchFloats;
     HIPCHK(ctx, hg::launch_gemv_mfma(p, w_dtype, B, (hipStream_t)stream));
     return HETEGEN_OK;
   });
@@ -1777,6 +1788,9 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
       j.tiled = use_tile;
       j.ws = m->ws;
       j.cnt = m->ws_cnt;
+      j.ws_floats = m->ws_floats;
+      j.cnt_words = m->ws_words;
+      j.korder = use_tile ? lin.korder : 0;
       j.ln_buf = m->lnbuf;
       const int i = 4 * l + which;
       if (which == 0 && l > 0 && all_tiled(i - 1) && all_tiled(i)) j.ln_in = m->ln_part;
@@ -1981,6 +1995,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     if (m->tiled) {
       const char* lp = getenv("HETEGEN_LN_PARTIALS");
       m->ln_partials = !(lp && strcmp(lp, "0") == 0);
+
     }
     // A tiled model also keeps the row-major copy, for batches 1-2 on the vector GEMV, when
     // both copies take at most half of the device memory free now (HETEGEN_DUAL_LAYOUT=0 at
@@ -2025,7 +2040,13 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
         model_free(m);
         return fail(ctx, HETEGEN_ERR_HIP, "split-K counter initialisation failed");
       }
+      m->ws_floats = ws_floats;
+      m->ws_words = ws_words;
     }
+    // tile order per linear (HETEGEN_TILE_KORDER=0 / 1 at creation: row-tile order / k-major
+    // for every linear)
+    const char* ko = getenv("HETEGEN_TILE_KORDER");
+    const int korder_env = ko && (strcmp(ko, "0") == 0 || strcmp(ko, "1") == 0) ? atoi(ko) : -1;
     char* p = (char*)m->arena;
     for (auto& l : m->lin) {
       if (l.resident) {
@@ -2042,10 +2063,11 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
         }
         if (m->tiled) {
           l.W_tile = p;
+          l.korder = korder_env >= 0 ? korder_env : hg::mfma_kmajor(l.n_gpu, l.K);
           p += align256(hg::tiled_bytes(l.n_gpu, l.K));
           if (ok && l.n_gpu > 0)
             ok = (m->rowmajor || hipMemcpy(stage, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess) &&
-                 hg::launch_tile(src, l.K, l.n_gpu, l.K, l.W_tile, nullptr) == hipSuccess &&
+                 hg::launch_tile(src, l.K, l.n_gpu, l.K, l.W_tile, nullptr, l.korder) == hipSuccess &&
                  hipDeviceSynchronize() == hipSuccess;
         }
         if (!ok) {
@@ -2127,7 +2149,11 @@ hetegen_status hetegen_model_set_exec(hetegen_model* m, int mode, uint32_t barri
 int hetegen_model_last_exec(const hetegen_model* m) { return m ? m->last_exec : -1; }
 
 int hetegen_model_layouts(const hetegen_model* m) {
-  return m ? (m->rowmajor ? HETEGEN_LAYOUT_ROWMAJOR : 0) | (m->tiled ? HETEGEN_LAYOUT_TILED : 0) : 0;
+  if (!m) return 0;
+  int kmajor = 0;
+  for (const auto& l : m->lin) kmajor |= l.W_tile && l.korder == 1;
+  return (m->rowmajor ? HETEGEN_LAYOUT_ROWMAJOR : 0) | (m->tiled ? HETEGEN_LAYOUT_TILED : 0) |
+         (kmajor ? HETEGEN_LAYOUT_KMAJOR : 0);
 }
 
 hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {

@@ -28,8 +28,11 @@ struct GemvParams {
   int ktile;           // set by the launcher: K elements staged in LDS per pass (tiled kernel)
   int rpw;             // set by the launcher: rows per workgroup (contiguous block)
   // matrix-core GEMV on tile-ordered weights (launch_gemv_mfma) only:
-  float* ws;           // split-K partials: mfma_ws_floats(rows, K, B) floats
-  uint32_t* cnt;       // split-K arrival counters: mfma_cnt_words(rows, K) words, zero between launches
+  float* ws;           // split-K partials: at least mfma_ws_floats(rows, K, B) floats
+  uint32_t* cnt;       // split-K arrival counters: at least mfma_cnt_words(rows, K) words, zero between launches
+  size_t ws_floats;    // floats at ws and words at cnt (checked by the launcher)
+  size_t cnt_words;
+  int korder;          // W's tile order (launch_tile's korder: 0 row-tile order, 1 k-major)
   const float* ln_in;  // ln != 0: LayerNorm partials of x (ln_partials_floats(K)), written by the
                        // launch that produced x through ln_out
   float* ln_out;       // or nullptr: LayerNorm partials of y (y in the activation type)
@@ -115,11 +118,16 @@ hipError_t launch_import_rows(const float* src_host_f32, int B, int n, int dtype
 size_t tiled_bytes(int rows, int K);
 
 // dst = tile order of W [rows, K] (row stride ldw elements, 16-byte aligned rows).
-hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream);
+// korder 1: k-major tile order instead, k-tile kt of row tile rt at tile kt * ceil(rows / 16) + rt.
+hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream, int korder = 0);
 
-// K-splits of the matrix-core GEMV for reduction length K (1 = no split), and the
-// workspace a launch of `rows` rows at batch B needs (0 when not split).
-int mfma_splits(int K);
+// K-splits of the matrix-core GEMV for `rows` rows and reduction length K on the current
+// device (1 = no split; it depends on the device's compute-unit count, not on the batch),
+// and the workspace a launch at batch B needs (0 when not split).
+int mfma_splits(int rows, int K);
+// Tile order for a model's copy of W [rows, K] on the current device: 1 k-major, 0 row-tile
+// order (1 when the launch grid puts the same number of workgroups, at most 4, on every CU).
+int mfma_kmajor(int rows, int K);
 size_t mfma_ws_floats(int rows, int K, int B);
 size_t mfma_cnt_words(int rows, int K);
 
@@ -132,13 +140,14 @@ size_t ln_partials_floats(int n);
 // y = epi(xn W^T + bias) with W in tile order (p.W), every row on the GPU, where xn is x,
 // or, when p.ln != 0, LayerNorm(x) from the partials p.ln_in (h_out, if set, receives xn
 // from workgroup 0).  With p.ln_out set the launch also writes the partials of y (p.y_f32
-// must be 0).  Split launches need p.ws and p.cnt.
+// must be 0).  Split launches need p.ws and p.cnt with their sizes in p.ws_floats and
+// p.cnt_words (hipErrorInvalidValue if too small).
 hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream);
 
 // Fixed split-K scratch of the matrix-core GEMV, one per GPU, for callers that cannot
 // allocate: kScratchCounterWords counters, then kScratchFloats floats of partials.
 constexpr size_t kScratchCounterWords = 65536;
-constexpr size_t kScratchFloats = (size_t)1 << 20;
+constexpr size_t kScratchFloats = (size_t)1 << 18;
 // Takes the scratch's address on `device` (which must be current) and zeroes its counters,
 // once per device; later calls return at once.
 hipError_t scratch_init(int device);

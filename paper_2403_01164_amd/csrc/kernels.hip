@@ -32,6 +32,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 
 #include "kernels.h"
 
@@ -734,6 +735,11 @@ __device__ __forceinline__ uint4 normalize8_fma(const uint4& v, float a, float c
 }
 
 constexpr int kTileRows = 16, kTileK = 32;
+// K-split choice of the matrix-core GEMV (mfma_splits)
+constexpr double kMaxUneven = 1.15;  // busiest CU's workgroups over the mean, tolerated unsplit
+constexpr int kMaxSplits = 8, kMinSplitTiles = 32;
+constexpr int kMaxDevices = 64, kDefaultCus = 256;
+constexpr int kMaxKmajorPerCu = 4;  // mfma_kmajor
 constexpr int kLnGroup = 16;    // elements per LayerNorm partial
 constexpr int kLnSlots = 8;     // batch rows per partial group (the largest batch)
 constexpr int kLnMaxGroups = kMaxLnK / kLnGroup;
@@ -824,7 +830,10 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
   const int pw = (ke - kb + kWaves - 1) / kWaves;
   const int k0 = min(ke, kb + wave * pw), k1 = min(ke, k0 + pw);
   const int nst = (k1 - k0 + U - 1) / U;
-  const uint4* wp = (const uint4*)p.W + (size_t)rt * KT * 64 + lane;
+  // k-tile kt of row tile rt: tile rt * KT + kt (row-tile order) or kt * RT + rt (k-major)
+  const size_t RT = (size_t)((p.rows + kTileRows - 1) / kTileRows);
+  const uint4* wp = (const uint4*)p.W + (p.korder ? (size_t)rt : (size_t)rt * KT) * 64 + lane;
+  const size_t kstride = p.korder ? RT * 64 : 64;
   const int b = min(lane & 15, B - 1), grp = lane >> 4;
   const uint16_t* xr = (const uint16_t*)p.x + (long long)b * p.ldx;
   struct Buf {
@@ -834,7 +843,7 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kt = min(k0 + st * U + u, k1 - 1);
-      f.w[u] = load_stream(wp + (size_t)kt * 64);
+      f.w[u] = load_stream(wp + (size_t)kt * kstride);
       const int kx = kt * kTileK + 8 * grp;  // K % 8 == 0: a group is wholly inside or past K
       f.x[u] = load_g16((const uint4*)(xr + min(kx, K - 8)));
       // columns past K, and (as a second guard) the repeated tile of a step past k1,
@@ -953,14 +962,15 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
 
 // Tile order of W [rows, K]: one 16-byte group per thread (see tiled_bytes in kernels.h).
 __global__ __launch_bounds__(kThreads) void tile_kernel(const uint16_t* __restrict__ W, long long ldw, int rows,
-                                                        int K, uint4* __restrict__ dst, long long groups) {
+                                                        int K, uint4* __restrict__ dst, long long groups, int korder) {
   const int KT = (K + kTileK - 1) / kTileK;
+  const long long RT = (rows + kTileRows - 1) / kTileRows;
   for (long long q = (long long)blockIdx.x * kThreads + threadIdx.x; q < groups;
        q += (long long)gridDim.x * kThreads) {
     const int l = (int)(q & 63);
     const long long tile = q >> 6;
-    const int kt = (int)(tile % KT);
-    const long long rt = tile / KT;
+    const int kt = korder ? (int)(tile / RT) : (int)(tile % KT);
+    const long long rt = korder ? tile % RT : tile / KT;
     const long long row = rt * kTileRows + (l & 15);
     const int k = kt * kTileK + 8 * (l >> 4);
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
@@ -1483,63 +1493,116 @@ size_t tiled_bytes(int rows, int K) {
   return (size_t)((rows + kTileRows - 1) / kTileRows) * (size_t)((K + kTileK - 1) / kTileK) * 1024;
 }
 
-hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream) {
+hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream, int korder) {
   const long long groups = (long long)(tiled_bytes(rows, K) / 16);
   if (groups == 0) return hipSuccess;
   long long g = (groups + kThreads - 1) / kThreads;
   if (g > 4096) g = 4096;
   hipLaunchKernelGGL(tile_kernel, dim3((unsigned)g), dim3(kThreads), 0, stream, (const uint16_t*)W, ldw, rows, K,
-                     (uint4*)dst, groups);
+                     (uint4*)dst, groups, korder);
   return hipGetLastError();
 }
 
-// Split K when one workgroup would walk more than 256 k-tiles (256 KiB of a row tile):
-// the short-N linears with long K (fc2) otherwise leave too few workgroups per CU
-// (OPT-6.7B fc2 [4096, 16384]: 256 workgroups; with 4 splits 25.0 -> 23.1 us at B = 1).
-// Splitting shorter K costs more in the merge than it gains.
-int mfma_splits(int K) {
-  const int KT = (K + kTileK - 1) / kTileK;
-  int g = 1;
-  while (g < 8 && KT / (2 * g) >= 128) g *= 2;
-  return g;
+// Compute units of the current device (read once per device).
+static int device_cus() {
+  static std::atomic<int> cus[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return kDefaultCus;
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c < 1) c = kDefaultCus;
+    cus[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+
+// How unevenly `wgs` equal workgroups load `cus` compute units: the busiest unit's
+// workgroups over the mean (1 when wgs is a multiple of cus).
+static double uneven(long long wgs, int cus) {
+  const long long per = (wgs + cus - 1) / cus;
+  return (double)(per * cus) / (double)wgs;
+}
+
+// One row tile per workgroup unless that loads the CUs unevenly (more than 1.15x the
+// mean on the busiest); then the fewest splits that do not, each at least 32 k-tiles
+// long, or else the most even split.  Splitting a balanced grid only adds the merge:
+// OPT-6.7B fc2 [4096, 16384] (256 row tiles) at B = 8 takes 23.9 us unsplit against
+// 26.2 us in 4 splits; OPT-13B fc2 [5120, 20480] (320 row tiles) 49.4 unsplit against
+// 39.1 us in 4 splits.  Measured over the 16 linear shapes of OPT-6.7B/13B/30B/66B at
+// B = 1, 2, 3 and 8, the rule picks the fastest split count or one within 1.5 % of it.
+// The choice does not depend on B, so a batch row's bits do not either.
+int mfma_splits(int rows, int K) {
+  if (rows <= 0 || K <= 0) return 1;
+  const int KT = (K + kTileK - 1) / kTileK, RT = (rows + kTileRows - 1) / kTileRows, cus = device_cus();
+  double best_u = uneven(RT, cus);
+  if (best_u <= kMaxUneven) return 1;
+  int best = 1;
+  for (int g = 2; g <= kMaxSplits && KT / g >= kMinSplitTiles; g *= 2) {
+    const double u = uneven((long long)RT * g, cus);
+    if (u <= kMaxUneven) return g;
+    if (u < best_u) {
+      best = g;
+      best_u = u;
+    }
+  }
+  return best;
+}
+
+// k-major tiles when the grid puts the same number of workgroups, 1 to 4, on every CU: all
+// of them then start together and walk K side by side, and in row-tile order their loads
+// would fall on the same offsets of blocks a fixed multiple of 16 rows apart, crowding a few
+// memory channels (OPT-6.7B fc2 [4096, 16384] at B = 8: 23.9 against 25.5 us in a decode
+// step, and the whole step 2.42 against 2.49 ms); k-major, the walk reads one contiguous
+// window.  With more workgroups per CU, or uneven ones, they drift apart and k-major
+// scatters the loads instead (OPT-30B fc1 [28672, 7168], 7 per CU: 72.8 against 70.5 us).
+int mfma_kmajor(int rows, int K) {
+  if (rows <= 0 || K <= 0) return 0;
+  const long long wgs = (long long)((rows + kTileRows - 1) / kTileRows) * mfma_splits(rows, K);
+  const int cus = device_cus();
+  return wgs % cus == 0 && wgs / cus <= kMaxKmajorPerCu ? 1 : 0;
 }
 
 size_t mfma_ws_floats(int rows, int K, int B) {
-  const int G = mfma_splits(K);
+  const int G = mfma_splits(rows, K);
   if (G == 1 || rows <= 0) return 0;
   return (size_t)((rows + kTileRows - 1) / kTileRows) * G * kTileRows * B;
 }
 
 size_t mfma_cnt_words(int rows, int K) {
-  if (mfma_splits(K) == 1 || rows <= 0) return 0;
+  if (mfma_splits(rows, K) == 1 || rows <= 0) return 0;
   return (size_t)((rows + kTileRows - 1) / kTileRows);
 }
 
+// Tiles per request: 4 with the LayerNorm prologue (fewer registers: the grid fits the
+// device at once), in split launches, at B = 1 and for long rows (K >= 16384); 8 for
+// the rest of the unsplit launches (OPT-6.7B out [4096, 4096] at B = 3: 8.5 against
+// 8.9 us; fc2 [4096, 16384] at B = 8: 24.6 against 23.9 us; out at B = 1: 9.4 against
+// 8.7 us).  Each wavefront sums its k-tiles in order either way: the bits are the same.
 template <class T, int B, bool LN>
-hipError_t launch_mfma_ln(const GemvParams& p, hipStream_t s) {
-  const int G = mfma_splits(p.K);
+hipError_t launch_mfma_ln(const GemvParams& p, int G, hipStream_t s) {
   const int grid = ((p.rows + kTileRows - 1) / kTileRows) * G;
-  if (G == 1) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, LN ? 4 : 8, LN>), dim3(grid), dim3(kThreads), 0, s, p, 1);
-  else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4, LN>), dim3(grid), dim3(kThreads), 0, s, p, G);
+  const bool u4 = LN || G > 1 || B == 1 || (p.K + kTileK - 1) / kTileK >= 512;
+  if (u4) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4, LN>), dim3(grid), dim3(kThreads), 0, s, p, G);
+  else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 8, false>), dim3(grid), dim3(kThreads), 0, s, p, 1);
   return hipGetLastError();
 }
 
 template <class T, int B>
-hipError_t launch_mfma_b(const GemvParams& p, hipStream_t s) {
-  return p.ln ? launch_mfma_ln<T, B, true>(p, s) : launch_mfma_ln<T, B, false>(p, s);
+hipError_t launch_mfma_b(const GemvParams& p, int G, hipStream_t s) {
+  return p.ln ? launch_mfma_ln<T, B, true>(p, G, s) : launch_mfma_ln<T, B, false>(p, G, s);
 }
 
 template <class T>
-hipError_t launch_mfma_t(const GemvParams& p, int B, hipStream_t s) {
+hipError_t launch_mfma_t(const GemvParams& p, int B, int G, hipStream_t s) {
   switch (B) {
-    case 1: return launch_mfma_b<T, 1>(p, s);
-    case 2: return launch_mfma_b<T, 2>(p, s);
-    case 3: return launch_mfma_b<T, 3>(p, s);
-    case 4: return launch_mfma_b<T, 4>(p, s);
-    case 5: return launch_mfma_b<T, 5>(p, s);
-    case 6: return launch_mfma_b<T, 6>(p, s);
-    case 7: return launch_mfma_b<T, 7>(p, s);
-    case 8: return launch_mfma_b<T, 8>(p, s);
+    case 1: return launch_mfma_b<T, 1>(p, G, s);
+    case 2: return launch_mfma_b<T, 2>(p, G, s);
+    case 3: return launch_mfma_b<T, 3>(p, G, s);
+    case 4: return launch_mfma_b<T, 4>(p, G, s);
+    case 5: return launch_mfma_b<T, 5>(p, G, s);
+    case 6: return launch_mfma_b<T, 6>(p, G, s);
+    case 7: return launch_mfma_b<T, 7>(p, G, s);
+    case 8: return launch_mfma_b<T, 8>(p, G, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1551,8 +1614,11 @@ hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream) 
   if (p.K < 8 || p.K % 8 || B < 1 || B > kLnSlots) return hipErrorInvalidValue;
   if (p.ln && (!p.ln_in || p.K > kMaxLnK)) return hipErrorInvalidValue;
   if (p.ln_out && p.y_f32) return hipErrorInvalidValue;
-  if (mfma_splits(p.K) > 1 && (!p.ws || !p.cnt)) return hipErrorInvalidValue;
-  return dtype == 1 ? launch_mfma_t<BF16>(p, B, stream) : launch_mfma_t<F16>(p, B, stream);
+  const int G = mfma_splits(p.rows, p.K);
+  if (G > 1 && (!p.ws || !p.cnt || p.ws_floats < mfma_ws_floats(p.rows, p.K, B) ||
+                p.cnt_words < mfma_cnt_words(p.rows, p.K)))
+    return hipErrorInvalidValue;
+  return dtype == 1 ? launch_mfma_t<BF16>(p, B, G, stream) : launch_mfma_t<F16>(p, B, G, stream);
 }
 
 }  // namespace hg

@@ -12,7 +12,7 @@ namespace hg {
 
 // ---- fixed split-K scratch for callers that cannot allocate ----
 // One array per GPU, zero-initialised when the code object loads: kScratchCounterWords
-// arrival counters, then kScratchFloats floats of partials.  Host code must not use the
+// arrival counters, then kScratchFloats floats of partials (1.25 MiB).  Host code must not use the
 // array's name as a device address (it is a host-side stand-in): the address is taken
 // once per device with hipGetSymbolAddress and kept in g_scratch.
 static __device__ __align__(256) uint32_t scratch[kScratchCounterWords + kScratchFloats];

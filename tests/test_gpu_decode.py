@@ -170,7 +170,7 @@ def test_exec_modes_bit_identical(ctx, dtype, B, max_batch, dual):
     L, H, F = 3, 512, 2048
     m = _model_with_env(ctx, {} if dual else {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1,
                         max_batch=max_batch)
-    layouts = hg.hetegen_model_layouts(m.m)
+    layouts = hg.hetegen_model_layouts(m.m) & ~hg.LAYOUT_KMAJOR
     assert layouts == (hg.LAYOUT_ROWMAJOR if max_batch < 3 else
                        hg.LAYOUT_TILED | (hg.LAYOUT_ROWMAJOR if dual else 0))
     try:
@@ -211,8 +211,8 @@ def test_dual_layout_runs_each_batch_on_the_matching_copy(ctx, dtype):
                                 weights=(rm.W, rm.b))
         try:
             assert hg.hetegen_model_layouts(rm.m) == hg.LAYOUT_ROWMAJOR
-            assert hg.hetegen_model_layouts(dual.m) == hg.LAYOUT_ROWMAJOR | hg.LAYOUT_TILED
-            assert hg.hetegen_model_layouts(tiles.m) == hg.LAYOUT_TILED
+            assert hg.hetegen_model_layouts(dual.m) & ~hg.LAYOUT_KMAJOR == hg.LAYOUT_ROWMAJOR | hg.LAYOUT_TILED
+            assert hg.hetegen_model_layouts(tiles.m) & ~hg.LAYOUT_KMAJOR == hg.LAYOUT_TILED
             for B in (1, 2, 3, 8):
                 x = synth.normal((B, H), dtype, 0, synth.act_id(10 + B))
                 want = (rm if B <= 2 else tiles).step(x)
@@ -265,6 +265,42 @@ def test_tiled_layernorm_from_partials(ctx, dtype, H, F):
             k.free()
     finally:
         m.free()
+
+
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+def test_tile_order_does_not_change_bits(ctx, dtype):
+    # tiles k-major (k-tile kt of row tile rt at kt * row tiles + rt) or in row-tile order:
+    # every wavefront adds the same tiles in the same order, so the bits are the same at
+    # every batch, and they pass the teacher-forced check.  On a 256-CU device the library
+    # keeps fc1 [4096, 1024] (256 workgroups) and fc2 [1024, 4096] (64 row tiles in 4 K-splits)
+    # k-major and qkv and out in row-tile order.
+    L, H, F = 2, 1024, 4096
+    env = {"HETEGEN_DUAL_LAYOUT": "0"}
+    rule = _model_with_env(ctx, env, L, H, F, dtype, 0.0, 1, max_batch=8)
+    try:
+        rows = _model_with_env(ctx, dict(env, HETEGEN_TILE_KORDER="0"), L, H, F, dtype, 0.0, 1, max_batch=8,
+                               weights=(rule.W, rule.b))
+        kmaj = _model_with_env(ctx, dict(env, HETEGEN_TILE_KORDER="1"), L, H, F, dtype, 0.0, 1, max_batch=8,
+                               weights=(rule.W, rule.b))
+        try:
+            assert hg.hetegen_model_layouts(rows.m) == hg.LAYOUT_TILED
+            assert hg.hetegen_model_layouts(kmaj.m) == hg.LAYOUT_TILED | hg.LAYOUT_KMAJOR
+            if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+                assert hg.hetegen_model_layouts(rule.m) == hg.LAYOUT_TILED | hg.LAYOUT_KMAJOR
+            for B in (8, 3, 1):
+                x = synth.normal((B, H), dtype, 0, synth.act_id(30 + B))
+                want = rows.step(x)
+                assert np.array_equal(kmaj.step(x), want), B
+                out, tr = rule.step(x, trace=True)
+                assert np.array_equal(out, want), B
+                if B == 8:
+                    last, _ = rule.check_teacher_forced(x, tr)
+                    assert np.array_equal(out, last)
+        finally:
+            kmaj.free()
+            rows.free()
+    finally:
+        rule.free()
 
 
 @pytest.mark.parametrize("B", [3, 8])

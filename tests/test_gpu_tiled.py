@@ -66,7 +66,8 @@ def test_tile_layout_matches_definition(ctx, N, K):
             assert np.array_equal(got, ref), (lane, e)
 
 
-SHAPES = [(37, 72), (256, 1024), (1000, 4104), (130, 8192), (48, 16384), (16, 36864)]  # the last three split K
+# on a 256-CU device the last four split K (into 4, 8, 8 and 8); the first two cannot (K < 2048)
+SHAPES = [(37, 72), (256, 1024), (1000, 4104), (130, 8192), (48, 16384), (16, 36864)]
 
 
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])

@@ -41,10 +41,10 @@ def _call(ctx, c, fn):
 
 
 def test_noalloc_matches_allocating_entry_point_call_after_call(ctx):
-    # a large split call (fc2 of OPT-6.7B at batch 8, 4 splits), then a smaller one (2 splits,
+    # a large split call (fc2 of OPT-13B at batch 8, 4 splits), then a smaller one (8 splits,
     # batch 2), then an unsplit one, then the large one again: each gives the allocating
     # entry point's bits and stays within the tolerance of the oracle
-    cases = [_case(ctx, 4096, 16384, 8, synth.F16, 100), _case(ctx, 130, 8192, 2, synth.BF16, 110),
+    cases = [_case(ctx, 5120, 20480, 8, synth.F16, 100), _case(ctx, 130, 8192, 2, synth.BF16, 110),
              _case(ctx, 300, 1024, 3, synth.F16, 120)]
     for c in cases + cases[:1]:
         ref_lib = _call(ctx, c, hg.hetegen_linear_tiled)
@@ -54,21 +54,34 @@ def test_noalloc_matches_allocating_entry_point_call_after_call(ctx):
         assert rel_err(got, ref) <= TOL
 
 
-def test_noalloc_refuses_shapes_beyond_its_scratch(ctx):
-    # 16400 rows at K = 36864 and batch 8 need 1025 * 8 * 16 * 8 = 1049600 partial floats,
-    # above the 1048576 of the fixed scratch; 16384 rows fit exactly.  The buffers are
-    # full-sized, so the refusal is the entry point's check, not a lucky launch.
-    K, B, dt = 36864, 8, synth.F16
+def _status(ctx, N, K, B, dt=synth.F16):
+    # full-sized zero buffers, so that an accepted call is a valid launch and a refusal is
+    # the entry point's check, not a lucky launch
     x = torch.zeros((B, K), dtype=torch.int16, device="cuda")
-    Wt = torch.zeros((hg.hetegen_tiled_bytes(16400, K) // 2,), dtype=torch.int16, device="cuda")
-    y = torch.zeros((B, 16400), dtype=torch.float32, device="cuda")
-    s = torch.cuda.current_stream().cuda_stream
-    rc = hg.hetegen_linear_tiled_noalloc_status(ctx, x.data_ptr(), B, K, Wt.data_ptr(), 16400, dt, 0, y.data_ptr(),
-                                                hg.F32, s)
-    assert rc == hg.ERR_UNSUPPORTED
-    assert "scratch" in hg.hetegen_last_error(ctx)
-    rc = hg.hetegen_linear_tiled_noalloc_status(ctx, x.data_ptr(), B, K, Wt.data_ptr(), 16384, dt, 0, y.data_ptr(),
-                                                hg.F32, s)
-    assert rc == hg.OK
+    Wt = torch.zeros((hg.hetegen_tiled_bytes(N, K) // 2,), dtype=torch.int16, device="cuda")
+    y = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    rc = hg.hetegen_linear_tiled_noalloc_status(ctx, x.data_ptr(), B, K, Wt.data_ptr(), N, dt, 0, y.data_ptr(),
+                                                hg.F32, torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
-    assert np.all(np_from_dev(y[:, :16384], np.float32) == 0.0)
+    return rc, y
+
+
+def test_noalloc_refuses_shapes_beyond_its_scratch(ctx):
+    # The split over K (one workgroup per 16-row tile unless that loads the compute units
+    # more than 1.15x unevenly) on a 256-CU device: [16400, 36864] is 1025 row tiles in 2
+    # splits, 1025 * 2 * 16 * 8 = 262400 partial floats at batch 8, and [4112, 36864] 257 row
+    # tiles in 8 splits, 263168, both above the 262144 of the fixed scratch; [14240, 36864],
+    # 890 row tiles in 2 splits, needs 227840 and runs.
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("the shapes are chosen for a 256-CU device")
+    for N in (16400, 4112):
+        rc, _ = _status(ctx, N, 36864, 8)
+        assert rc == hg.ERR_UNSUPPORTED, N
+        assert "scratch" in hg.hetegen_last_error(ctx)
+    rc, y = _status(ctx, 14240, 36864, 8)
+    assert rc == hg.OK
+    assert np.all(np_from_dev(y, np.float32) == 0.0)
+    # at batch 4 the 1025-tile shape needs half as much and runs
+    rc, y = _status(ctx, 16400, 36864, 4)
+    assert rc == hg.OK
+    assert np.all(np_from_dev(y, np.float32) == 0.0)
