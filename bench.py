@@ -435,8 +435,8 @@ def main():
                          "below unless --no-streamed)")
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--max-batch", type=int, default=0,
-                    help="largest batch the model is created for (0: --batch); from 3 on its resident weights "
-                         "are kept in matrix-core tile order, also for smaller batches")
+                    help="largest batch the model is created for (0: --batch); from 2 on its resident weights "
+                         "are kept in matrix-core tile order (and row-major too, for batch 1, when both fit)")
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N decoder layers (0: all); reported in config")
     ap.add_argument("--placement", choices=("all", "half", "none", "sched"), default=None,
@@ -806,7 +806,7 @@ def decode_workload(args, torch, synth, hg):
         log("%s: avg %.2f us/launch, %.2f MB/launch -> %.1f GB/s" %
             (exec_mode, avg_us, bytes_per_launch / 1e6, achieved))
         layouts = hg.hetegen_model_layouts(model)
-        tiled_used = bool(layouts & hg.LAYOUT_TILED) and (B >= 3 or not layouts & hg.LAYOUT_ROWMAJOR)
+        tiled_used = bool(layouts & hg.LAYOUT_TILED) and (B >= 2 or not layouts & hg.LAYOUT_ROWMAJOR)
         kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
             else gemv_label(B, H, F, dt, tiled_used, ln_partials_on(),
                             torch.cuda.get_device_properties(0).multi_processor_count)

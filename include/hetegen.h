@@ -338,11 +338,11 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * otherwise they are streamed every step.  max_batch in [1, 8]; H, F multiples
  * of 8, H <= 16384 (UNSUPPORTED above: the LayerNorm keeps a row in registers; the
  * largest OPT hidden size is 12288).  Layout of the resident rows: with max_batch
- * < 3 they are row-major and run on the vector GEMV (fused LayerNorm, the faster
- * kernels at batches 1-2); with max_batch >= 3 they are stored in matrix-core tile
- * order and batches of 3 and more run on the matrix-core GEMV (see
+ * 1 they are row-major and run on the vector GEMV (fused LayerNorm, the faster
+ * kernels at batch 1); with max_batch >= 2 they are stored in matrix-core tile
+ * order and batches of 2 and more run on the matrix-core GEMV (see
  * hetegen_linear_tiled; the model also owns its split-K workspace).  Such a model
- * also keeps the row-major copy, and runs batches 1-2 from it, when both copies
+ * also keeps the row-major copy, and runs batch 1 from it, when both copies
  * take at most half of the device memory free at creation (the environment
  * variable HETEGEN_DUAL_LAYOUT=0 at creation keeps the tile order only);
  * hetegen_model_layouts tells which copies a model holds.  On the matrix-core path,
@@ -388,8 +388,8 @@ HETEGEN_API hetegen_status hetegen_decode_step(hetegen_ctx* ctx, hetegen_model* 
 #define HETEGEN_EXEC_EAGER 3
 
 /* Select the execution mode (UNSUPPORTED when a forced mode cannot run this
- * model; PERSISTENT needs the row-major copy of the resident rows and runs batches
- * 1-2 only).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
+ * model; PERSISTENT needs the row-major copy of the resident rows and runs batch
+ * 1 only).  barrier_spin_limit bounds the polls of one grid-barrier wait in the
  * persistent mode (0: the default, seconds of waiting); a wait that gives up lets
  * the step finish with undefined outputs and makes the next hetegen_decode_step
  * on the model fail with HETEGEN_ERR_HIP.  A small limit exists to test that path. */

@@ -63,12 +63,12 @@ constexpr size_t kCounterBytes = 256;
 constexpr int kDefaultRing = 8;
 constexpr int kMaxBatch = 8;
 // Models created for batches of kTiledMinBatch or more keep their resident rows in the
-// matrix-core tile order and run them on the matrix-core GEMV at every batch size: the
-// vector GEMV's dot products and LDS reads of x grow with the batch (OPT-6.7B-shaped
-// steps: 2.74 / 2.95 / 3.95 ms at batch 3 / 4 / 8 against 2.56 / 2.57 / 2.67 ms on the
-// matrix cores), while at batches 1-2 the vector kernels with their fused LayerNorm are
-// faster (2.19 / 2.45 against 2.57 / 2.55 ms).
-constexpr int kTiledMinBatch = 3;
+// matrix-core tile order and run batches from kTiledMinBatch on on the matrix-core GEMV:
+// the vector GEMV's dot products and reads of x grow with the batch (OPT-6.7B-shaped
+// steps: 2.44 / 2.74 / 3.95 ms at batch 2 / 3 / 8 against 2.32 / 2.33 / 2.42 ms on the
+// matrix cores), while at batch 1 the vector kernels with their fused LayerNorm are
+// faster (2.19 against 2.30 ms); with both copies, batch 1 runs the row-major one.
+constexpr int kTiledMinBatch = 2;
 constexpr int kDefaultPinThreads = 4;
 constexpr int kDefaultPinRing = 4;
 
@@ -146,7 +146,7 @@ struct hetegen_model {
     int resident = 0;
     int n_gpu = 0, n_cpu = 0;
     bool pageable = false;     // W_host is plain host memory (staged when streamed)
-    void* W_dev = nullptr;     // rows [0, n_gpu) when resident, row-major (batches 1-2 and row-major models)
+    void* W_dev = nullptr;     // rows [0, n_gpu) when resident, row-major (batch 1 and row-major models)
     void* W_tile = nullptr;    // the same rows in matrix-core tile order (tiled models)
     int korder = 0;            // W_tile's order: 0 row-tile order, 1 k-major (hg::mfma_kmajor)
     void* bias_dev = nullptr;  // all N biases
@@ -1997,7 +1997,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       m->ln_partials = !(lp && strcmp(lp, "0") == 0);
 
     }
-    // A tiled model also keeps the row-major copy, for batches 1-2 on the vector GEMV, when
+    // A tiled model also keeps the row-major copy, for batch 1 on the vector GEMV, when
     // both copies take at most half of the device memory free now (HETEGEN_DUAL_LAYOUT=0 at
     // creation: tile order only)
     if (m->tiled && rm_bytes) {

@@ -1400,8 +1400,9 @@ hipError_t launch_ln_t(const void* x, long long ldx, int B, int K, void* h, long
   }
 }
 
-// The persistent step runs row-major models, i.e. models created for batches of 1 or 2
-// (larger ones keep their weights in matrix-core tile order).
+// The persistent step runs the row-major copy, which only batch 1 uses (models created for
+// larger batches run batches from 2 on their matrix-core tiles; the batch-2 instance is
+// not launched by the library).
 template <class T>
 const void* step_fn(int B) {
   switch (B) {

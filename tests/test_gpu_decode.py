@@ -165,13 +165,13 @@ def _model_with_env(ctx, env, *args, **kw):
 def test_exec_modes_bit_identical(ctx, dtype, B, max_batch, dual):
     # persistent (one cooperative launch, grid barriers), graph replay and eager
     # per-linear launches compute every output row the same way; the persistent step runs
-    # the row-major copy at batches 1-2 only (models for batches of 3 or more keep it
-    # beside the tile order when memory allows, HETEGEN_DUAL_LAYOUT=0 keeps tiles only)
+    # the row-major copy at batch 1 only (models for batches of 2 or more keep it beside
+    # the tile order when memory allows, HETEGEN_DUAL_LAYOUT=0 keeps tiles only)
     L, H, F = 3, 512, 2048
     m = _model_with_env(ctx, {} if dual else {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1,
                         max_batch=max_batch)
     layouts = hg.hetegen_model_layouts(m.m) & ~hg.LAYOUT_KMAJOR
-    assert layouts == (hg.LAYOUT_ROWMAJOR if max_batch < 3 else
+    assert layouts == (hg.LAYOUT_ROWMAJOR if max_batch < 2 else
                        hg.LAYOUT_TILED | (hg.LAYOUT_ROWMAJOR if dual else 0))
     try:
         xs = [synth.normal((B, H), dtype, 0, synth.act_id(t)) for t in range(3)]
@@ -180,7 +180,7 @@ def test_exec_modes_bit_identical(ctx, dtype, B, max_batch, dual):
             with pytest.raises(hg.HetegenError) as e:
                 hg.hetegen_model_set_exec(m.m, hg.EXEC_PERSISTENT)
             assert e.value.status == hg.ERR_UNSUPPORTED
-        persistent = bool(layouts & hg.LAYOUT_ROWMAJOR) and B <= 2
+        persistent = bool(layouts & hg.LAYOUT_ROWMAJOR) and B == 1
         modes = (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT, hg.EXEC_AUTO) if persistent else \
             (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_AUTO)
         for mode in modes:
@@ -201,10 +201,10 @@ def test_exec_modes_bit_identical(ctx, dtype, B, max_batch, dual):
 
 @pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
 def test_dual_layout_runs_each_batch_on_the_matching_copy(ctx, dtype):
-    # a model for batches up to 8 with both copies gives, at batches 1-2, the bits of a
-    # row-major model and, from batch 3, the bits of a tile-only model (same weights)
+    # a model for batches up to 8 with both copies gives, at batch 1, the bits of a
+    # row-major model and, from batch 2, the bits of a tile-only model (same weights)
     L, H, F = 2, 1024, 8192
-    rm = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=2)
+    rm = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1)
     try:
         dual = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=8, weights=(rm.W, rm.b))
         tiles = _model_with_env(ctx, {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1, max_batch=8,
@@ -215,7 +215,7 @@ def test_dual_layout_runs_each_batch_on_the_matching_copy(ctx, dtype):
             assert hg.hetegen_model_layouts(tiles.m) & ~hg.LAYOUT_KMAJOR == hg.LAYOUT_TILED
             for B in (1, 2, 3, 8):
                 x = synth.normal((B, H), dtype, 0, synth.act_id(10 + B))
-                want = (rm if B <= 2 else tiles).step(x)
+                want = (rm if B == 1 else tiles).step(x)
                 out, tr = dual.step(x, trace=True)
                 assert np.array_equal(out, want), B
                 last, _ = dual.check_teacher_forced(x, tr)
