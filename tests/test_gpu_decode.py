@@ -133,6 +133,36 @@ def test_opt67b_full_model_resident_as_benchmarked(ctx):
         m.free()
 
 
+def test_opt67b_full_model_batched_as_benchmarked(ctx):
+    # the batched workload as benchmarked: all 32 OPT-6.7B-shaped layers resident in a model
+    # created for batch 8 (matrix-core tiles, k-major on a 256-CU device, no K split, LayerNorm
+    # partials between the linears), at batches 8, 3 and 2; every linear checked against the
+    # oracle on 256 sampled output rows of the input it was given, the untraced step gives the
+    # same bits, and a batch row's bits do not depend on the batch size
+    dtype, L, H, F = synth.F16, 32, 4096, 16384
+    m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=8)
+    try:
+        layouts = hg.hetegen_model_layouts(m.m)
+        assert layouts & hg.LAYOUT_TILED
+        if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+            assert layouts & hg.LAYOUT_KMAJOR
+        x = synth.normal((8, H), dtype, 0, synth.act_id(5))
+        out8, tr = m.step(x, trace=True)
+        assert hg.hetegen_model_last_exec(m.m) == 3  # eager per-linear launches
+        last, worst = m.check_teacher_forced(x, tr, sample=256)
+        assert np.array_equal(out8, last)
+        assert np.array_equal(m.step(x), out8)
+        for B in (3, 2):
+            xb = np.ascontiguousarray(x[:B])
+            out, tr = m.step(xb, trace=True)
+            last, _ = m.check_teacher_forced(xb, tr, sample=256)
+            assert np.array_equal(out, last)
+            assert np.array_equal(out, out8[:B]), B
+        print("32 layers at batch 8: worst per-linear relative error %.3g" % worst)
+    finally:
+        m.free()
+
+
 def test_opt13b_shape_one_layer_hetero(ctx):
     dtype, L, H, F = synth.F16, 1, 5120, 20480
     m = Model(ctx, L, H, F, dtype, [0.62, 0.6, 0.63, 0.61], 0, max_batch=1)
