@@ -85,6 +85,32 @@ def test_linear_tiled_parity(ctx, dtype, N, K, B):
     assert rel_err(oracle.decode(y16, dtype), ref) <= TOL + U_ACT[dtype]
 
 
+@pytest.mark.parametrize("N,K,dtype", [
+    (4096, 16384, synth.F16),   # OPT-6.7B fc2: 256 row tiles, unsplit on a 256-CU device
+    (5120, 5120, synth.F16),    # OPT-13B out: 320 row tiles, 4 K-splits
+    (5120, 20480, synth.F16),   # OPT-13B fc2: 4 K-splits
+    (7168, 28672, synth.F16),   # OPT-30B fc2: 448 row tiles, unsplit
+    (9216, 9216, synth.BF16),   # OPT-66B out: 576 row tiles, 2 K-splits
+    (9216, 36864, synth.BF16),  # OPT-66B fc2: 2 K-splits
+    (27648, 9216, synth.BF16),  # OPT-66B qkv: 1728 row tiles, unsplit
+])
+@pytest.mark.parametrize("B", [1, 8])
+def test_linear_tiled_full_size_opt_shapes(ctx, N, K, dtype, B):
+    # the matrix-core GEMV at full OPT out / fc2 / qkv sizes, where the split rule keeps or
+    # drops the split over K: 288 output rows (the first and last 16, 256 more at random)
+    # against the oracle, and the bits do not change from call to call
+    W = synth.normal((N, K), dtype, 0, 71, 0, 0.02)
+    b = synth.normal((N,), dtype, 0, 72, 0, 0.02)
+    x = synth.normal((B, K), dtype, 0, 73)
+    Wt = _tiled(ctx, W)
+    y = _run(ctx, x, Wt, N, dtype, b)
+    rows = np.unique(np.concatenate([np.arange(16), np.arange(N - 16, N),
+                                     np.random.default_rng(N + K).choice(N, 256, replace=False)]))
+    ref = oracle.linear(x, np.ascontiguousarray(W[rows]), np.ascontiguousarray(b[rows]), dtype).astype(np.float64)
+    assert rel_err(y[:, rows], ref) <= TOL
+    assert np.array_equal(_run(ctx, x, Wt, N, dtype, b).view(np.uint32), y.view(np.uint32))
+
+
 @pytest.mark.parametrize("dtype,N,K", [(synth.F16, 100, 2040), (synth.BF16, 40, 248), (synth.F16, 64, 16384),
                                        (synth.BF16, 33, 36864)])
 @pytest.mark.parametrize("B", [1, 8])
