@@ -384,10 +384,12 @@ def mfma_splits(rows, K, cus):
     return best
 
 
-def ln_partials_on():
-    """Whether tiled models normalise the inputs of qkv (after layer 0) and fc1 from the
-    LayerNorm partials of the out / fc2 before them (the library default)."""
-    return os.environ.get("HETEGEN_LN_PARTIALS") != "0"
+def ln_partials_on(H):
+    """Whether tiled models of hidden size H normalise the inputs of qkv (after layer 0) and
+    fc1 from the LayerNorm partials of the out / fc2 before them (the library's rule: H <= 6144
+    unless HETEGEN_LN_PARTIALS forces it)."""
+    env = os.environ.get("HETEGEN_LN_PARTIALS")
+    return {"0": False, "1": True}.get(env, H <= 6144)
 
 
 def gemv_label(B, H, F, dt, tiled, partials=True, cus=256):
@@ -808,7 +810,7 @@ def decode_workload(args, torch, synth, hg):
         layouts = hg.hetegen_model_layouts(model)
         tiled_used = bool(layouts & hg.LAYOUT_TILED) and (B >= 2 or not layouts & hg.LAYOUT_ROWMAJOR)
         kernel_label = "step_kernel<%s,%d,...>" % ("BF16" if dt == 1 else "F16", B) if exec_mode == "persistent" \
-            else gemv_label(B, H, F, dt, tiled_used, ln_partials_on(),
+            else gemv_label(B, H, F, dt, tiled_used, ln_partials_on(H),
                             torch.cuda.get_device_properties(0).multi_processor_count)
         result["frac_of_hbm_peak"] = round(gbps / HBM_PEAK_GBPS, 4)
         # achievable read bandwidth of this device (streaming read of 4 GiB), for information
@@ -837,7 +839,7 @@ def decode_workload(args, torch, synth, hg):
             # each): before layer 0's qkv, or before every qkv and fc1 without the partials; they
             # are not in launches_per_step or bytes_per_launch, so `achieved` understates the
             # GEMV's own rate by their share of the step
-            n_ln = 1 if ln_partials_on() else 2 * L
+            n_ln = 1 if ln_partials_on(H) else 2 * L
             result["roofline"]["region_also_holds"] = "%d layernorm_regs_kernel launch%s per step (%d bytes each)" % (
                 n_ln, "" if n_ln == 1 else "es", B * H * 4)
     elif streamed:

@@ -349,8 +349,9 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * when out (fc2) and the fc1 (next qkv) after it run every row on the GPU, out / fc2
  * also leave per-16-element LayerNorm partials of their output (sum, sum of squared
  * deviations), and fc1 / qkv normalise their input from them instead of after a
- * LayerNorm launch (Chan-Golub-LeVeque combination in a fixed order; the variable
- * HETEGEN_LN_PARTIALS=0 at creation keeps the LayerNorm launches).  A tiled linear
+ * LayerNorm launch (Chan-Golub-LeVeque combination in a fixed order), when H <= 6144:
+ * for larger hidden sizes combining the H / 16 partials costs more than the launch (the
+ * variable HETEGEN_LN_PARTIALS=0 or 1 at creation forces the launches or the partials).  A tiled linear
  * whose matrix-core grid puts the same number of workgroups, 1 to 4, on every compute
  * unit keeps its tiles k-major (k-tile kt of row tile rt at tile kt * ceil(n_gpu / 16) +
  * rt), so that workgroups walking K side by side read one contiguous window; the others

@@ -69,6 +69,14 @@ constexpr int kMaxBatch = 8;
 // matrix cores), while at batch 1 the vector kernels with their fused LayerNorm are
 // faster (2.19 against 2.30 ms); with both copies, batch 1 runs the row-major one.
 constexpr int kTiledMinBatch = 2;
+// Largest hidden size at which the matrix-core qkv and fc1 normalise their input from the
+// LayerNorm partials of the linear before them: their prologue combines H / 16 partials per
+// batch row before the first product, and above this a LayerNorm launch is cheaper (16-layer
+// steps at batch 8 / 3: OPT-13B, H = 5120, 1.961 / 1.763 ms with partials against 2.029 /
+// 1.820 with launches; OPT-30B, 7168, 3.557 / 3.137 against 3.529 / 3.174; OPT-66B, 9216,
+// 5.727 / 5.113 against 5.584 / 5.115).  The choice depends on H alone, so that a batch row's
+// bits do not depend on the batch size.
+constexpr int kMaxPartialsH = 6144;
 constexpr int kDefaultPinThreads = 4;
 constexpr int kDefaultPinRing = 4;
 
@@ -160,7 +168,7 @@ struct hetegen_model {
   size_t ws_floats = 0, ws_words = 0;
   float* ln_part = nullptr;    // LayerNorm partials of x after out / fc2 (two buffers of
                                // ln_partials_floats(H)), for the tiled GEMVs of fc1 / qkv
-  bool ln_partials = true;     // use them (HETEGEN_LN_PARTIALS=0 at creation: LayerNorm launches)
+  bool ln_partials = true;     // use them (H <= kMaxPartialsH; HETEGEN_LN_PARTIALS=0 / 1 at creation forces)
   std::vector<Lin> lin;
   std::vector<double> lin_ms;  // host time of each linear in the last eager step
   void* arena = nullptr;  // device memory for resident weights and biases
@@ -1994,7 +2002,7 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     }
     if (m->tiled) {
       const char* lp = getenv("HETEGEN_LN_PARTIALS");
-      m->ln_partials = !(lp && strcmp(lp, "0") == 0);
+      m->ln_partials = lp && strcmp(lp, "0") == 0 ? false : lp && strcmp(lp, "1") == 0 ? true : H <= kMaxPartialsH;
 
     }
     // A tiled model also keeps the row-major copy, for batch 1 on the vector GEMV, when

@@ -127,6 +127,44 @@ def test_opt66b_layer_bf16_teacher_forced(ctx, B):
         m.free()
 
 
+@pytest.mark.parametrize("H,dtype", [(7168, synth.F16), (9216, synth.BF16)])
+@pytest.mark.parametrize("partials", ["default", "1"])
+def test_large_hidden_layernorm_partials_choice(ctx, H, dtype, partials):
+    # two resident layers (F = H) in tile order at batch 8: above H = 6144 the library
+    # normalises qkv and fc1 after LayerNorm launches; HETEGEN_LN_PARTIALS=1 makes it combine
+    # the partials of out / fc2 (H / 16 of them per batch row) instead.  Both pass the
+    # teacher-forced check, and agree within the tolerance per layer.
+    import os
+    from common import TOL, U_ACT, rel_err
+    import oracle
+    L, F, B = 2, H, 8
+    old = os.environ.get("HETEGEN_LN_PARTIALS")
+    if partials != "default":
+        os.environ["HETEGEN_LN_PARTIALS"] = partials
+    try:
+        m = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=8)
+    finally:
+        if old is None:
+            os.environ.pop("HETEGEN_LN_PARTIALS", None)
+        else:
+            os.environ["HETEGEN_LN_PARTIALS"] = old
+    try:
+        x = synth.normal((B, H), dtype, 0, synth.act_id(7))
+        out, tr = m.step(x, trace=True)
+        last, _ = m.check_teacher_forced(x, tr, sample=256)
+        assert np.array_equal(out, last)
+        for b in (3, 2):
+            assert np.array_equal(m.step(np.ascontiguousarray(x[:b])), out[:b]), b
+        ref = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1, weights=(m.W, m.b))
+        try:
+            want = ref.step(x[:1])
+        finally:
+            ref.free()
+        assert rel_err(oracle.decode(out[:1], dtype), oracle.decode(want, dtype), floor=1.0) <= L * (TOL + U_ACT[dtype])
+    finally:
+        m.free()
+
+
 def test_hidden_size_above_limit_rejected(ctx):
     W = [0] * 4
     with pytest.raises(hg.HetegenError) as e:
