@@ -1529,9 +1529,11 @@ static double uneven(long long wgs, int cus) {
 // long, or else the most even split.  Splitting a balanced grid only adds the merge:
 // OPT-6.7B fc2 [4096, 16384] (256 row tiles) at B = 8 takes 23.9 us unsplit against
 // 26.2 us in 4 splits; OPT-13B fc2 [5120, 20480] (320 row tiles) 49.4 unsplit against
-// 39.1 us in 4 splits.  Measured over the 16 linear shapes of OPT-6.7B/13B/30B/66B at
-// B = 1, 2, 3 and 8, the rule picks the fastest split count or one within 1.5 % of it.
-// The choice does not depend on B, so a batch row's bits do not either.
+// 39.1 us in 4 splits.  Over the 16 linear shapes of OPT-6.7B/13B/30B/66B at B = 1, 2, 3
+// and 8 the rule picks the fastest split count but at B = 8 for OPT-13B out [5120, 5120]
+// (4 splits: 15.5 against 14.8 us with 2) and OPT-66B fc2 [9216, 36864] (2 splits: 117.3
+// against 114.0 us with 4).  The choice does not depend on B, so a batch row's bits do not
+// either.
 int mfma_splits(int rows, int K) {
   if (rows <= 0 || K <= 0) return 1;
   const int KT = (K + kTileK - 1) / kTileK, RT = (rows + kTileRows - 1) / kTileRows, cus = device_cus();
