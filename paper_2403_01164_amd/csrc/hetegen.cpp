@@ -63,7 +63,7 @@ constexpr size_t kCounterBytes = 256;
 constexpr int kDefaultRing = 8;
 constexpr int kMaxBatch = 8;
 // Models created for batches of kTiledMinBatch or more keep their resident rows in the
-// matrix-core tile order and run batches from kTiledMinBatch on on the matrix-core GEMV:
+// matrix-core tile order and run every batch of kTiledMinBatch or more on the matrix-core GEMV:
 // the vector GEMV's dot products and reads of x grow with the batch (OPT-6.7B-shaped
 // steps: 2.44 / 2.74 / 3.95 ms at batch 2 / 3 / 8 against 2.32 / 2.33 / 2.42 ms on the
 // matrix cores), while at batch 1 the vector kernels with their fused LayerNorm are
@@ -2003,7 +2003,6 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     if (m->tiled) {
       const char* lp = getenv("HETEGEN_LN_PARTIALS");
       m->ln_partials = lp && strcmp(lp, "0") == 0 ? false : lp && strcmp(lp, "1") == 0 ? true : H <= kMaxPartialsH;
-
     }
     // A tiled model also keeps the row-major copy, for batch 1 on the vector GEMV, when
     // both copies take at most half of the device memory free now (HETEGEN_DUAL_LAYOUT=0 at

@@ -1578,9 +1578,10 @@ size_t mfma_cnt_words(int rows, int K) {
 
 // Tiles per request: 4 with the LayerNorm prologue (fewer registers: the grid fits the
 // device at once), in split launches, at B = 1 and for long rows (K >= 16384); 8 for
-// the rest of the unsplit launches (OPT-6.7B out [4096, 4096] at B = 3: 8.5 against
-// 8.9 us; fc2 [4096, 16384] at B = 8: 24.6 against 23.9 us; out at B = 1: 9.4 against
-// 8.7 us).  Each wavefront sums its k-tiles in order either way: the bits are the same.
+// the rest of the unsplit launches.  8 against 4 tiles per request, OPT-6.7B shapes:
+// out [4096, 4096] at B = 3 8.5 against 8.9 us, fc2 [4096, 16384] at B = 8 24.6 against
+// 23.9 us, out at B = 1 9.4 against 8.7 us.  Each wavefront sums its k-tiles in order
+// either way: the bits are the same.
 template <class T, int B, bool LN>
 hipError_t launch_mfma_ln(const GemvParams& p, int G, hipStream_t s) {
   const int grid = ((p.rows + kTileRows - 1) / kTileRows) * G;
