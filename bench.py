@@ -18,8 +18,10 @@ under --hbm-budget; --pageable keeps the weights in plain pageable memory, strea
 through the hybrid pin || transfer path (Sec. 4.2-4.3).
 
 The default run (no --model) measures the all-resident OPT-6.7B line above and then,
-after freeing it, the streamed half of the metric in the same process (`streamed` in the
-same JSON line; --no-streamed skips it): OPT-30B shapes, 48 layers, every linear in
+after freeing it, the same stack at batch 8 in a model created for batch 8 (matrix-core
+tiles; `batched` in the same JSON line, 32 steps; --no-batched skips it), and the streamed
+half of the metric in the same process (`streamed` in the same JSON line; --no-streamed
+skips it): OPT-30B shapes, 48 layers, every linear in
 pinned host memory, the planner's CPU fractions refined by the step-level alpha
 benchmark, batch 1, 32 steps; the same model with every GPU row streamed (CPU
 fraction 0, 2 steps); both against the idle link, one 1 GiB pinned host-to-device copy,
@@ -486,6 +488,10 @@ def main():
                     help="default run only: skip the streamed leg (OPT-30B shapes, every linear in pinned host "
                          "memory, planner alpha refined by the step-level benchmark, batch 1)")
     ap.add_argument("--streamed-steps", type=int, default=32, help="timed steps of the streamed leg")
+    ap.add_argument("--no-batched", action="store_true",
+                    help="default run only: skip the batched leg (the OPT-6.7B stack at batch 8 on the "
+                         "matrix-core GEMV, in a model created for batch 8)")
+    ap.add_argument("--batched-steps", type=int, default=32, help="timed steps of the batched leg")
     ap.add_argument("--all-streamed-steps", type=int, default=None,
                     help="streamed workloads: also time this many steps with every GPU row streamed (CPU "
                          "fraction 0), against the idle link (default: 2 in the streamed leg, 0 otherwise)")
@@ -514,9 +520,28 @@ def main():
     if args.model is None:
         args.model = "opt-6.7b"
     result = decode_workload(args, torch, synth, hg)
+    if default_run and not args.no_batched:
+        result["batched"] = batched_leg(args, torch, synth, hg)
     if default_run and not args.no_streamed:
         result["streamed"] = streamed_leg(args, torch, synth, hg)
     print(json.dumps(result), flush=True)
+
+
+def batched_leg(args, torch, synth, hg):
+    """The matrix-core half of the resident path, after the headline line has freed its
+    memory: the same OPT-6.7B-shaped stack (32 layers, fp16, every linear resident) in a model
+    created for batch 8, stepped at batch 8; tokens per second count all 8 rows."""
+    import copy
+    a = copy.copy(args)
+    a.model, a.batch, a.max_batch, a.layers, a.placement, a.hbm_budget = "opt-6.7b", 8, 8, 0, "all", None
+    a.alpha, a.alpha_sweep, a.pageable, a.context, a.exec = None, None, False, 0, "auto"
+    a.steps, a.warmup, a.no_cpu_baseline, a.copy_calibration = args.batched_steps, 3, True, False
+    log("batched leg: OPT-6.7B shapes, all linears resident, batch 8, %d steps" % a.steps)
+    r = decode_workload(a, torch, synth, hg)
+    return {"workload": r["config"]["workload"], "batch": 8, "steps": r["steps"], "warmup": r["warmup"],
+            "ms_per_step": r["ms_per_step"], "tokens_per_s": round(8 * 1e3 / r["ms_per_step"], 1),
+            "step_ms_p10_p50_p90": r.get("step_ms_p10_p50_p90"), "weight_GBps": r["value"],
+            "weight_layouts": r["config"].get("weight_layouts"), "roofline": r["roofline"]}
 
 
 def streamed_leg(args, torch, synth, hg):
