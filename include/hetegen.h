@@ -351,13 +351,17 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * deviations), and fc1 / qkv normalise their input from them instead of after a
  * LayerNorm launch (Chan-Golub-LeVeque combination in a fixed order), when H <= 6144:
  * for larger hidden sizes combining the H / 16 partials costs more than the launch (the
- * variable HETEGEN_LN_PARTIALS=0 or 1 at creation forces the launches or the partials).  A tiled linear
- * whose matrix-core grid puts the same number of workgroups, 1 to 4, on every compute
- * unit keeps its tiles k-major (k-tile kt of row tile rt at tile kt * ceil(n_gpu / 16) +
- * rt), so that workgroups walking K side by side read one contiguous window; the others
- * keep hetegen_tile_weights' order (HETEGEN_TILE_KORDER=0 or 1 at creation: one order for
- * every linear).  The tile order does not change the bits.  Results do not depend on
- * the layout or the LayerNorm path beyond rounding (all pass the oracle's tolerance). */
+ * variable HETEGEN_LN_PARTIALS=0 or 1 at creation forces the launches or the partials).
+ * A tiled linear whose matrix-core grid puts the same number of workgroups, 1 to 4, on
+ * every compute unit keeps its tiles k-major (k-tile kt of row tile rt at tile kt *
+ * ceil(n_gpu / 16) + rt), so that workgroups walking K side by side read one contiguous
+ * window; the others keep hetegen_tile_weights' order (HETEGEN_TILE_KORDER=0 or 1 at
+ * creation: one order for every linear).  The row-major copy of a GPU-only linear with
+ * K >= 8192 and K a multiple of 2048 is stored segment-major (2048-element segment s of
+ * row r at (s * n_gpu + r) * 2048 elements), which batch-1 wavefronts walking rows side
+ * by side read as one window (HETEGEN_SEGMAJOR=0 at creation: plain row-major).  Neither
+ * order changes the bits.  Results do not depend on the layout or the LayerNorm path
+ * beyond rounding (all pass the oracle's tolerance). */
 HETEGEN_API hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, hetegen_dtype dtype,
                                     void* const* W_host, void* const* bias_host, const double* alpha,
                                     const int* resident, int max_batch, hetegen_model** out);
@@ -400,11 +404,13 @@ HETEGEN_API hetegen_status hetegen_model_set_exec(hetegen_model* model, int mode
 HETEGEN_API int hetegen_model_last_exec(const hetegen_model* model);
 
 /* Layouts of the model's resident rows (see hetegen_model_create): a bitwise OR of
- * HETEGEN_LAYOUT_ROWMAJOR, HETEGEN_LAYOUT_TILED and HETEGEN_LAYOUT_KMAJOR (some tiled
- * linear keeps its tiles k-major), 0 for NULL or no resident rows kept in either. */
+ * HETEGEN_LAYOUT_ROWMAJOR, HETEGEN_LAYOUT_TILED, HETEGEN_LAYOUT_KMAJOR (some tiled linear
+ * keeps its tiles k-major) and HETEGEN_LAYOUT_SEGMAJOR (some row-major copy is stored
+ * segment-major), 0 for NULL or no resident rows kept in either. */
 #define HETEGEN_LAYOUT_ROWMAJOR 1
 #define HETEGEN_LAYOUT_TILED 2
 #define HETEGEN_LAYOUT_KMAJOR 4
+#define HETEGEN_LAYOUT_SEGMAJOR 8
 HETEGEN_API int hetegen_model_layouts(const hetegen_model* model);
 
 /* Alpha benchmark at the granularity of the decode step (Sec. 4.4 applied to the

@@ -335,7 +335,7 @@ def hetegen_model_last_exec(model):
     return _lib.hetegen_model_last_exec(model)
 
 
-LAYOUT_ROWMAJOR, LAYOUT_TILED, LAYOUT_KMAJOR = 1, 2, 4
+LAYOUT_ROWMAJOR, LAYOUT_TILED, LAYOUT_KMAJOR, LAYOUT_SEGMAJOR = 1, 2, 4, 8
 
 
 def hetegen_model_layouts(model):

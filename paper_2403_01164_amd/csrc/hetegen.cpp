@@ -77,6 +77,14 @@ constexpr int kTiledMinBatch = 2;
 // 5.727 / 5.113 against 5.584 / 5.115).  The choice depends on H alone, so that a batch row's
 // bits do not depend on the batch size.
 constexpr int kMaxPartialsH = 6144;
+// Resident row-major copies (batch 1) of GPU-only linears with K >= kMinSegmajorK (and K a
+// multiple of hg::kSegElems) are stored segment-major: the batch-1 GEMV walks each row in
+// 2048-element segments, every wavefront its own row, so in row-major order the wavefronts'
+// loads fall on the same offsets of rows K * 2 bytes apart; segment-major, they read one
+// contiguous window.  OPT-6.7B fc2 [4096, 16384]: 21.7 us against 22.1-22.8 us over weight
+// placements (probe), the whole batch-1 step 2.168 against 2.203 ms (three runs each,
+// alternating); out [4096, 4096] (two segments per row) gained nothing.
+constexpr int kMinSegmajorK = 8192;
 constexpr int kDefaultPinThreads = 4;
 constexpr int kDefaultPinRing = 4;
 
@@ -157,6 +165,7 @@ struct hetegen_model {
     void* W_dev = nullptr;     // rows [0, n_gpu) when resident, row-major (batch 1 and row-major models)
     void* W_tile = nullptr;    // the same rows in matrix-core tile order (tiled models)
     int korder = 0;            // W_tile's order: 0 row-tile order, 1 k-major (hg::mfma_kmajor)
+    int segmajor = 0;          // W_dev segment-major (hg::launch_segmajor; see kMinSegmajorK)
     void* bias_dev = nullptr;  // all N biases
   };
   int L = 0, H = 0, F = 0, dtype = 0, max_batch = 1;
@@ -605,6 +614,7 @@ struct Job {
   uint32_t* cnt;
   size_t ws_floats, cnt_words;
   int korder;       // tiled: W_dev's tile order
+  int segmajor;     // W_dev segment-major (resident row-major copy, batch 1)
   const float* ln_in;  // tiled, ln, all rows resident: LayerNorm from these partials of x
   float* ln_out;       // tiled, all rows resident: also write the partials of y here
 };
@@ -628,6 +638,7 @@ hetegen_status run_gemv(hetegen_ctx* ctx, const Job& j, const void* x, long long
   p.epi = j.epi;
   p.y_f32 = j.y_f32;
   p.ln = ln;
+  p.segmajor = resident && !tiled ? j.segmajor : 0;
   TimedScope ts(ctx, st, resident ? 2 : 1, (double)rows * j.K * 2);
   if (tiled) {
     p.ws = j.ws;
@@ -1799,6 +1810,7 @@ hetegen_status enqueue_step(hetegen_ctx* ctx, hetegen_model* m, const void* x_de
       j.ws_floats = m->ws_floats;
       j.cnt_words = m->ws_words;
       j.korder = use_tile ? lin.korder : 0;
+      j.segmajor = use_tile ? 0 : lin.segmajor;  // the row-major copy runs batch 1 only
       j.ln_buf = m->lnbuf;
       const int i = 4 * l + which;
       if (which == 0 && l > 0 && all_tiled(i - 1) && all_tiled(i)) j.ln_in = m->ln_part;
@@ -1878,6 +1890,7 @@ hetegen_status build_plan(hetegen_ctx* ctx, hetegen_model* m, int B) {
         d.rows = lin.n_gpu;
         d.K = lin.K;
         d.rpw = rpw[i];
+        d.segmajor = lin.segmajor;
         switch (which) {
           case 0:
             d.x = m->xbuf; d.x_in = l == 0; d.ldx = H; d.ln = 1;
@@ -2054,6 +2067,9 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
     // for every linear)
     const char* ko = getenv("HETEGEN_TILE_KORDER");
     const int korder_env = ko && (strcmp(ko, "0") == 0 || strcmp(ko, "1") == 0) ? atoi(ko) : -1;
+    // segment-major row-major copies (HETEGEN_SEGMAJOR=0 at creation: plain row-major)
+    const char* sm = getenv("HETEGEN_SEGMAJOR");
+    const bool seg_on = !(sm && strcmp(sm, "0") == 0);
     char* p = (char*)m->arena;
     for (auto& l : m->lin) {
       if (l.resident) {
@@ -2062,11 +2078,26 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
         const size_t rb = (size_t)l.n_gpu * l.K * 2;
         bool ok = true;
         void* src = stage;
+        void* rm_stage = nullptr;  // row-major rows of a segment-major copy (also the tiling's source)
         if (m->rowmajor) {
           l.W_dev = p;
           src = p;
           p += align256(rb);
-          if (l.n_gpu > 0) ok = hipMemcpy(l.W_dev, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess;
+          if (seg_on && l.n_gpu > 0 && l.n_cpu == 0 && l.K % hg::kSegElems == 0 && l.K >= kMinSegmajorK) {
+            if (hipMalloc(&rm_stage, rb) == hipSuccess) {
+              l.segmajor = 1;
+            } else {  // no room for the staging copy: this linear stays row-major
+              (void)hipGetLastError();
+              rm_stage = nullptr;
+            }
+          }
+          if (l.segmajor) {
+            ok = hipMemcpy(rm_stage, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess &&
+                 hg::launch_segmajor(rm_stage, l.n_gpu, l.K, l.W_dev, nullptr) == hipSuccess;
+            src = rm_stage;
+          } else if (l.n_gpu > 0) {
+            ok = hipMemcpy(l.W_dev, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess;
+          }
         }
         if (m->tiled) {
           l.W_tile = p;
@@ -2076,6 +2107,10 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
             ok = (m->rowmajor || hipMemcpy(stage, l.W_host, rb, hipMemcpyHostToDevice) == hipSuccess) &&
                  hg::launch_tile(src, l.K, l.n_gpu, l.K, l.W_tile, nullptr, l.korder) == hipSuccess &&
                  hipDeviceSynchronize() == hipSuccess;
+        }
+        if (rm_stage) {
+          ok = hipDeviceSynchronize() == hipSuccess && ok;
+          (void)hipFree(rm_stage);
         }
         if (!ok) {
           (void)hipGetLastError();
@@ -2157,10 +2192,13 @@ int hetegen_model_last_exec(const hetegen_model* m) { return m ? m->last_exec : 
 
 int hetegen_model_layouts(const hetegen_model* m) {
   if (!m) return 0;
-  int kmajor = 0;
-  for (const auto& l : m->lin) kmajor |= l.W_tile && l.korder == 1;
+  int kmajor = 0, segmajor = 0;
+  for (const auto& l : m->lin) {
+    kmajor |= l.W_tile && l.korder == 1;
+    segmajor |= l.W_dev && l.segmajor;
+  }
   return (m->rowmajor ? HETEGEN_LAYOUT_ROWMAJOR : 0) | (m->tiled ? HETEGEN_LAYOUT_TILED : 0) |
-         (kmajor ? HETEGEN_LAYOUT_KMAJOR : 0);
+         (kmajor ? HETEGEN_LAYOUT_KMAJOR : 0) | (segmajor ? HETEGEN_LAYOUT_SEGMAJOR : 0);
 }
 
 hetegen_status hetegen_model_set_alpha(hetegen_model* m, const double* alpha) {

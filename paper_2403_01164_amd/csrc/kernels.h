@@ -33,6 +33,7 @@ struct GemvParams {
   size_t ws_floats;    // floats at ws and words at cnt (checked by the launcher)
   size_t cnt_words;
   int korder;          // W's tile order (launch_tile's korder: 0 row-tile order, 1 k-major)
+  int segmajor;        // W segment-major (launch_segmajor): gemv_x1_kernel and the persistent step only
   const float* ln_in;  // ln != 0: LayerNorm partials of x (ln_partials_floats(K)), written by the
                        // launch that produced x through ln_out
   float* ln_out;       // or nullptr: LayerNorm partials of y (y in the activation type)
@@ -52,6 +53,7 @@ struct StepLinear {
   long long ldr;
   int rows, K, epi, ln, rpw;
   int x_in, resid_in, y_out;
+  int segmajor;  // W segment-major (launch_segmajor)
 };
 
 struct StepArgs {
@@ -91,6 +93,13 @@ hipError_t launch_step(const StepArgs& a, int dtype, int B, int grid, size_t lds
 // dtype: 0 = fp16, 1 = bf16.  grid_cap bounds the number of workgroups
 // (0 = default).  Returns the launch status.
 hipError_t launch_gemv(GemvParams p, int dtype, int B, hipStream_t stream, int grid_cap);
+
+// Segment-major layout of a row-major weight [rows, K] (K a multiple of kSegElems): the
+// kSegElems-element segment s of row r is stored at (s * rows + r) * kSegElems elements, so
+// that wavefronts walking rows side by side read one contiguous window.
+constexpr int kSegElems = 2048;
+// dst = segment-major copy of row-major W [rows, K] (16-byte aligned, not overlapping).
+hipError_t launch_segmajor(const void* W, int rows, int K, void* dst, hipStream_t stream);
 
 // Largest LayerNorm width (hidden size) the kernels support.
 constexpr int kMaxLnK = 16384;

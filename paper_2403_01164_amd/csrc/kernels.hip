@@ -303,6 +303,12 @@ __device__ __forceinline__ void store_y_c(void* yrow, uint32_t n, uint32_t i, in
   store_y<T>(yrow, i, y_f32, v);
 }
 
+// 16-byte group col of row `row` in the segment-major layout of a [rows, K] weight.
+__device__ __forceinline__ const uint4* seg_addr(const uint4* W, int rows, int row, int col) {
+  constexpr int G = kSegElems / 8;  // 16-byte groups per segment
+  return W + ((long long)(col / G) * rows + row) * G + (col % G);
+}
+
 // ---------------------------------------------------------------------------
 // Main GEMV, one workgroup's block of rows (x fits in LDS).  Dynamic LDS layout:
 //   xs [B][K/8] uint4 | bias [rpw] f32 | resid [B][rpw] f32 | out [B][rpw] f32
@@ -341,7 +347,8 @@ __device__ __forceinline__ void gemv_block(const GemvParams& p, int blk, uint4* 
         // unconditional load (clamped address): no branch, so the compiler can keep
         // later tasks' loads in flight; lanes past the row end reread its last
         // chunk (same cache line, no extra traffic) and skip it in compute()
-        w[u][r] = load_stream(wr + min(c0 + 64 * u, k8 - 1));
+        const int col = min(c0 + 64 * u, k8 - 1);
+        w[u][r] = load_stream(p.segmajor ? seg_addr((const uint4*)W, p.rows, row, col) : wr + col);
       }
     }
   };
@@ -478,6 +485,7 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
   const int row_begin = blockIdx.x * rpw;
   const int nrows = min(rpw, p.rows - row_begin);  // >= 1: the grid covers rows exactly
   constexpr int SEG = 64 * U;
+  static_assert(SEG * 8 == kSegElems, "a request segment is one segment of the segment-major layout");
   const int nseg = (k8 + SEG - 1) / SEG;
   const int my_rg = nrows > wave ? (nrows - wave + kWaves - 1) / kWaves : 0;  // <= kX1MaxRows (launcher)
   const int ntask = my_rg * nseg;
@@ -501,7 +509,9 @@ __global__ __launch_bounds__(kThreads) void gemv_x1_kernel(GemvParams p) {
   auto load = [&](int t, Buf& f) {
     const int j = t / nseg, seg = t - j * nseg;
     const int row = row_begin + wave + j * kWaves;
-    const uint4* wr = (const uint4*)(W + (long long)row * K);
+    // segment-major: segment seg of this row at (seg * rows + row) * SEG 16-byte groups
+    const uint4* wr = p.segmajor ? (const uint4*)W + ((long long)seg * p.rows + row) * SEG - (long long)seg * SEG
+                                 : (const uint4*)(W + (long long)row * K);
     const int c0 = seg * SEG + lane;
 #pragma unroll
     for (int u = 0; u < U; ++u) f.w[u] = load_stream(wr + min(c0 + 64 * u, k8 - 1));
@@ -1046,6 +1056,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
     p.epi = d.epi;
     p.ln = d.ln;
     p.rpw = d.rpw;
+    p.segmajor = d.segmajor;
     const uint32_t n = a.barrier_base + (uint32_t)i;
     gemv_block<T, B, R, U, true, true>(p, blockIdx.x, smem, red, [&] {
       if (i > 0) grid_wait(a, n - 1u);
@@ -1299,6 +1310,9 @@ hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
     // NC = 18 (9216) the row no longer fits the registers well and the LDS kernel is as fast
     const int nc = p.K % 512 == 0 ? p.K / 512 : 0;
     const bool ln_regs = B == 1 && p.ln && (nc == 1 || nc == 2 || nc == 4 || nc == 5 || nc == 8 || nc == 10 || nc == 14);
+    // segment-major weights: gemv_x1_kernel and gemv_block (below) read them, the register
+    // LayerNorm kernel does not
+    if (p.segmajor && ln_regs) return hipErrorInvalidValue;
     if (!p.ln || ln_regs) {
       const long long units = (p.rows + kWaves - 1) / kWaves;
       const long long per = std::min<long long>((units + cap - 1) / cap, kX1MaxRows);
@@ -1347,6 +1361,7 @@ hipError_t launch_gemv_b(GemvParams p, hipStream_t s, int grid_cap) {
     return hipGetLastError();
   }
   if (p.ln) return hipErrorInvalidValue;  // not reached: see gemv_tiled_kernel
+  if (p.segmajor) return hipErrorInvalidValue;  // gemv_tiled_kernel reads row-major weights
   int kt = kTiledLdsBudget / (2 * B);
   kt -= kt % 512;
   p.ktile = kt;
@@ -1458,6 +1473,7 @@ hipError_t launch_step(const StepArgs& a, int dtype, int B, int grid, size_t lds
 
 hipError_t launch_gemv(GemvParams p, int dtype, int B, hipStream_t stream, int grid_cap) {
   if (p.rows <= 0) return hipSuccess;
+  if (p.segmajor && (B != 1 || p.K % kSegElems)) return hipErrorInvalidValue;
   return dtype == 1 ? launch_gemv_t<BF16>(p, B, stream, grid_cap) : launch_gemv_t<F16>(p, B, stream, grid_cap);
 }
 
@@ -1492,6 +1508,25 @@ hipError_t launch_import_rows(const float* src, int B, int n, int dtype, int epi
 size_t tiled_bytes(int rows, int K) {
   if (rows <= 0 || K <= 0) return 0;
   return (size_t)((rows + kTileRows - 1) / kTileRows) * (size_t)((K + kTileK - 1) / kTileK) * 1024;
+}
+
+// Segment-major copy (see launch_segmajor): one 16-byte group per thread.
+__global__ __launch_bounds__(kThreads) void segmajor_kernel(const uint4* __restrict__ W, int rows, int k8,
+                                                            uint4* __restrict__ dst, long long n) {
+  constexpr int SEG = kSegElems / 8;
+  for (long long q = (long long)blockIdx.x * kThreads + threadIdx.x; q < n; q += (long long)gridDim.x * kThreads) {
+    const long long s = q / ((long long)rows * SEG), rem = q - s * rows * SEG, r = rem / SEG, i = rem - r * SEG;
+    dst[q] = W[r * k8 + s * SEG + i];
+  }
+}
+
+hipError_t launch_segmajor(const void* W, int rows, int K, void* dst, hipStream_t stream) {
+  if (rows <= 0 || K <= 0 || K % kSegElems) return hipErrorInvalidValue;
+  const long long n = (long long)rows * (K / 8);
+  long long g = std::min<long long>((n + kThreads - 1) / kThreads, 4096);
+  hipLaunchKernelGGL(segmajor_kernel, dim3((unsigned)g), dim3(kThreads), 0, stream, (const uint4*)W, rows, K / 8,
+                     (uint4*)dst, n);
+  return hipGetLastError();
 }
 
 hipError_t launch_tile(const void* W, long long ldw, int rows, int K, void* dst, hipStream_t stream, int korder) {

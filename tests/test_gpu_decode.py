@@ -200,7 +200,7 @@ def test_exec_modes_bit_identical(ctx, dtype, B, max_batch, dual):
     L, H, F = 3, 512, 2048
     m = _model_with_env(ctx, {} if dual else {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1,
                         max_batch=max_batch)
-    layouts = hg.hetegen_model_layouts(m.m) & ~hg.LAYOUT_KMAJOR
+    layouts = hg.hetegen_model_layouts(m.m) & ~(hg.LAYOUT_KMAJOR | hg.LAYOUT_SEGMAJOR)
     assert layouts == (hg.LAYOUT_ROWMAJOR if max_batch < 2 else
                        hg.LAYOUT_TILED | (hg.LAYOUT_ROWMAJOR if dual else 0))
     try:
@@ -240,9 +240,10 @@ def test_dual_layout_runs_each_batch_on_the_matching_copy(ctx, dtype):
         tiles = _model_with_env(ctx, {"HETEGEN_DUAL_LAYOUT": "0"}, L, H, F, dtype, 0.0, 1, max_batch=8,
                                 weights=(rm.W, rm.b))
         try:
-            assert hg.hetegen_model_layouts(rm.m) == hg.LAYOUT_ROWMAJOR
-            assert hg.hetegen_model_layouts(dual.m) & ~hg.LAYOUT_KMAJOR == hg.LAYOUT_ROWMAJOR | hg.LAYOUT_TILED
-            assert hg.hetegen_model_layouts(tiles.m) & ~hg.LAYOUT_KMAJOR == hg.LAYOUT_TILED
+            order = hg.LAYOUT_KMAJOR | hg.LAYOUT_SEGMAJOR  # tile and row orders
+            assert hg.hetegen_model_layouts(rm.m) & ~order == hg.LAYOUT_ROWMAJOR
+            assert hg.hetegen_model_layouts(dual.m) & ~order == hg.LAYOUT_ROWMAJOR | hg.LAYOUT_TILED
+            assert hg.hetegen_model_layouts(tiles.m) & ~order == hg.LAYOUT_TILED
             for B in (1, 2, 3, 8):
                 x = synth.normal((B, H), dtype, 0, synth.act_id(10 + B))
                 want = (rm if B == 1 else tiles).step(x)
@@ -331,6 +332,44 @@ def test_tile_order_does_not_change_bits(ctx, dtype):
             rows.free()
     finally:
         rule.free()
+
+
+@pytest.mark.parametrize("dtype", [synth.F16, synth.BF16])
+def test_segment_major_rows_keep_bits(ctx, dtype):
+    # fc2 [1024, 8192] (K >= 8192, a multiple of 2048) keeps its row-major copy segment-major
+    # (2048-element segment s of row r at s * N + r); qkv, out and fc1 (K = 1024) stay
+    # row-major.  Eager, graph and persistent steps at batch 1 give the bits of a model with
+    # plain row-major copies, and pass the teacher-forced check; a model created for batch 8
+    # (both copies, tiles made from the row-major staging) does at batches 1 and 8.
+    L, H, F = 2, 1024, 8192
+    plain = _model_with_env(ctx, {"HETEGEN_SEGMAJOR": "0"}, L, H, F, dtype, 0.0, 1, max_batch=1)
+    try:
+        seg = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=1, weights=(plain.W, plain.b))
+        dual = Model(ctx, L, H, F, dtype, 0.0, 1, max_batch=8, weights=(plain.W, plain.b))
+        try:
+            assert hg.hetegen_model_layouts(plain.m) == hg.LAYOUT_ROWMAJOR
+            assert hg.hetegen_model_layouts(seg.m) == hg.LAYOUT_ROWMAJOR | hg.LAYOUT_SEGMAJOR
+            assert hg.hetegen_model_layouts(dual.m) & hg.LAYOUT_SEGMAJOR
+            x = synth.normal((1, H), dtype, 0, synth.act_id(40))
+            want = plain.step(x)
+            for mode in (hg.EXEC_EAGER, hg.EXEC_GRAPH, hg.EXEC_PERSISTENT):
+                hg.hetegen_model_set_exec(seg.m, mode)
+                assert np.array_equal(seg.step(x), want), mode
+                assert hg.hetegen_model_last_exec(seg.m) == mode
+            hg.hetegen_model_set_exec(seg.m, hg.EXEC_AUTO)
+            out, tr = seg.step(x, trace=True)
+            last, _ = seg.check_teacher_forced(x, tr)
+            assert np.array_equal(out, last) and np.array_equal(out, want)
+            assert np.array_equal(dual.step(x), want)
+            x8 = synth.normal((8, H), dtype, 0, synth.act_id(41))
+            out8, tr8 = dual.step(x8, trace=True)
+            last8, _ = dual.check_teacher_forced(x8, tr8)
+            assert np.array_equal(out8, last8)
+        finally:
+            dual.free()
+            seg.free()
+    finally:
+        plain.free()
 
 
 @pytest.mark.parametrize("B", [3, 8])
