@@ -44,3 +44,28 @@ def test_host_record_fields():
     for k in ("cpu", "physical_cores", "logical_cpus", "numa_nodes", "rocm", "hip", "torch"):
         assert k in h
     assert h["logical_cpus"] >= 1 and h["torch"] == torch.__version__
+
+
+def test_kernel_labels_follow_the_measured_rules():
+    # bench.py names the kernels a step runs from the library's dispatch rules; on a 256-CU
+    # device the split counts of the OPT linears are the ones the library's sweep picked
+    # (unsplit where one workgroup per 16-row tile loads the CUs evenly), and the LayerNorm
+    # partials are used up to a hidden size of 6144
+    splits = {(12288, 4096): 1, (4096, 4096): 1, (16384, 4096): 1, (4096, 16384): 1,      # OPT-6.7B
+              (15360, 5120): 1, (5120, 5120): 4, (20480, 5120): 1, (5120, 20480): 4,      # OPT-13B
+              (21504, 7168): 1, (7168, 7168): 1, (28672, 7168): 1, (7168, 28672): 1,      # OPT-30B
+              (27648, 9216): 1, (9216, 9216): 2, (36864, 9216): 1, (9216, 36864): 2,      # OPT-66B
+              (16400, 36864): 2, (4112, 36864): 8, (256, 1024): 1, (37, 72): 1}
+    for (n, k), g in splits.items():
+        assert bench.mfma_splits(n, k, 256) == g, (n, k)
+    env = os.environ.pop("HETEGEN_LN_PARTIALS", None)
+    try:
+        assert bench.ln_partials_on(4096) and bench.ln_partials_on(5120)
+        assert not bench.ln_partials_on(7168) and not bench.ln_partials_on(9216)
+    finally:
+        if env is not None:
+            os.environ["HETEGEN_LN_PARTIALS"] = env
+    label = bench.gemv_label(8, 4096, 16384, 0, True, True, 256)
+    assert "k-major" in label and "K split" not in label
+    label = bench.gemv_label(8, 9216, 36864, 1, True, False, 256)
+    assert "K split 2" in label and "k-major" not in label and "LayerNorm from partials" not in label
