@@ -19,7 +19,9 @@ through the hybrid pin || transfer path (Sec. 4.2-4.3).
 
 The default run (no --model) measures the all-resident OPT-6.7B line above and then,
 after freeing it, the same stack at batch 8 in a model created for batch 8 (matrix-core
-tiles; `batched` in the same JSON line, 32 steps; --no-batched skips it), and the streamed
+tiles; `batched` in the same JSON line, 32 steps; --no-batched skips it), the full decode step
+at batch 1 with attention over a 512-position KV cache (`kv_step`, 32 steps; --no-kv skips it),
+and the streamed
 half of the metric in the same process (`streamed` in the same JSON line; --no-streamed
 skips it): OPT-30B shapes, 48 layers, every linear in
 pinned host memory, the planner's CPU fractions refined by the step-level alpha
@@ -492,6 +494,10 @@ def main():
                     help="default run only: skip the batched leg (the OPT-6.7B stack at batch 8 on the "
                          "matrix-core GEMV, in a model created for batch 8)")
     ap.add_argument("--batched-steps", type=int, default=32, help="timed steps of the batched leg")
+    ap.add_argument("--no-kv", action="store_true",
+                    help="default run only: skip the kv leg (the OPT-6.7B stack at batch 1 with attention over "
+                         "a 512-position KV cache)")
+    ap.add_argument("--kv-steps", type=int, default=32, help="timed steps of the kv leg")
     ap.add_argument("--all-streamed-steps", type=int, default=None,
                     help="streamed workloads: also time this many steps with every GPU row streamed (CPU "
                          "fraction 0), against the idle link (default: 2 in the streamed leg, 0 otherwise)")
@@ -522,9 +528,27 @@ def main():
     result = decode_workload(args, torch, synth, hg)
     if default_run and not args.no_batched:
         result["batched"] = batched_leg(args, torch, synth, hg)
+    if default_run and not args.no_kv:
+        result["kv_step"] = kv_leg(args, torch, synth, hg)
     if default_run and not args.no_streamed:
         result["streamed"] = streamed_leg(args, torch, synth, hg)
     print(json.dumps(result), flush=True)
+
+
+def kv_leg(args, torch, synth, hg):
+    """The full decode step (Sec. 2.1, Eq. 1): the same OPT-6.7B stack at batch 1 with attention
+    over a KV cache of 512 earlier positions (synthetic keys and values standing in for a
+    prefill), every linear resident."""
+    import copy
+    a = copy.copy(args)
+    a.model, a.batch, a.max_batch, a.layers, a.placement, a.hbm_budget = "opt-6.7b", 1, 0, 0, "all", None
+    a.alpha, a.alpha_sweep, a.pageable, a.context, a.exec = None, None, False, 512, "auto"
+    a.steps, a.warmup, a.no_cpu_baseline, a.copy_calibration = args.kv_steps, 3, True, False
+    log("kv leg: OPT-6.7B shapes, all linears resident, batch 1, 512-position KV cache, %d steps" % a.steps)
+    r = decode_workload(a, torch, synth, hg)
+    return {"workload": r["config"]["workload"], "context": 512, "steps": r["steps"], "warmup": r["warmup"],
+            "ms_per_step": r["ms_per_step"], "step_ms_p10_p50_p90": r.get("step_ms_p10_p50_p90"),
+            "kv": r.get("kv"), "roofline": r["roofline"]}
 
 
 def batched_leg(args, torch, synth, hg):
@@ -763,7 +787,7 @@ def decode_workload(args, torch, synth, hg):
     log("per-step ms p10 / p50 / p90: %s" % step_pct)
 
     if placement == "all":
-        desc = "all linears HBM-resident (alpha=0), GEMV-only"
+        desc = "all linears HBM-resident (alpha=0)" + ("" if P > 0 else ", GEMV-only")
     elif placement == "half":
         desc = "layers 0-%d HBM-resident, %d-%d streamed from pinned host" % (res_layers - 1, res_layers, L - 1)
     elif placement == "sched":
