@@ -141,7 +141,7 @@ HETEGEN_API hetegen_status hetegen_linear(hetegen_ctx* ctx, const void* x_dev, i
  * and columns past K are zero.  One tile is the 16-row operand of one 16x16x32
  * matrix-core product, so the GEMV reads every tile with one coalesced 1 KiB load
  * and runs on the matrix cores at every batch size (decode steps of models created
- * for batches of 3 or more keep their resident rows in this order). */
+ * for batches of 2 or more keep their resident rows in this order). */
 
 /* Bytes of the tile-ordered copy of a [rows, K] weight (0 for rows < 1 or K not a
  * positive multiple of 8). */
@@ -165,7 +165,8 @@ HETEGEN_API hetegen_status hetegen_tile_weights(hetegen_ctx* ctx, const void* W_
  * batch row's bits do not depend on the batch size.  Uses the context's split-K
  * workspace, which the first call with a larger need allocates (device memory,
  * after waiting for the device); calls on one context must not overlap.  Enqueued
- * on `stream`.  B in [1, 8], K % 8 == 0, N >= 1. */
+ * on `stream`.  B in [1, 8], K % 8 == 0, N >= 1, B * K < 2^30 (x is read through
+ * a buffer descriptor, whose offsets are 32-bit). */
 HETEGEN_API hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_dev, int B, int K,
                                                 const void* W_tiled_dev, int N, hetegen_dtype w_dtype,
                                                 const void* bias_dev, void* y_dev, hetegen_dtype y_dtype,

@@ -1029,6 +1029,8 @@ hetegen_status hetegen_linear_tiled(hetegen_ctx* ctx, const void* x_dev, int B, 
     if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
     if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
     if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+    if ((long long)B * K >= (1LL << 30))  // x is read through a buffer descriptor (32-bit offsets)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B * K = %lld: x must hold fewer than 2^30 elements", (long long)B * K);
     if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
       return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
     if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)
@@ -1087,6 +1089,8 @@ hetegen_status hetegen_linear_tiled_noalloc(hetegen_ctx* ctx, const void* x_dev,
     if (N < 1) return fail(ctx, HETEGEN_ERR_INVALID_ARG, "N = %d", N);
     if (B < 1 || B > kMaxBatch) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B = %d outside [1, %d]", B, kMaxBatch);
     if (K < 8 || K % 8) return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "K = %d must be a positive multiple of 8", K);
+    if ((long long)B * K >= (1LL << 30))  // x is read through a buffer descriptor (32-bit offsets)
+      return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "B * K = %lld: x must hold fewer than 2^30 elements", (long long)B * K);
     if (w_dtype != HETEGEN_F16 && w_dtype != HETEGEN_BF16)
       return fail(ctx, HETEGEN_ERR_UNSUPPORTED, "weight dtype %d: fp16 or bf16 only", (int)w_dtype);
     if (y_dtype != w_dtype && y_dtype != HETEGEN_F32)

@@ -267,6 +267,7 @@ __device__ __forceinline__ void store_y(void* y, long long i, int y_f32, float v
 // ---------------------------------------------------------------------------
 constexpr int kBufWord3 = 0x00020000;
 constexpr int kCoherent = 1 | 16;  // sc0 | sc1
+constexpr uint32_t kXPast = 0x80000000u;  // a buffer offset past every descriptor the GEMVs build
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
@@ -845,7 +846,15 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
   const uint4* wp = (const uint4*)p.W + (p.korder ? (size_t)rt : (size_t)rt * KT) * 64 + lane;
   const size_t kstride = p.korder ? RT * 64 : 64;
   const int b = min(lane & 15, B - 1), grp = lane >> 4;
-  const uint16_t* xr = (const uint16_t*)p.x + (long long)b * p.ldx;
+  // x fragments through a buffer descriptor over rows [0, B) of x: a lane whose result
+  // column is past B (its products are never read), a group past K and the repeated tile
+  // of a step past k1 get an offset past the descriptor's size, for which the load
+  // returns zeros without a memory access; at B = 8 that halves the x fragments' share of
+  // the load pipeline, and no branch is needed (a branch around the loads makes the
+  // compiler wait for the weights in flight)
+  const auto xrs = rsrc(p.x, (uint32_t)(((long long)(B - 1) * p.ldx + K) * 2));
+  const bool xlane = (lane & 15) < B;
+  const uint32_t xrow = (uint32_t)((long long)b * p.ldx * 2);
   struct Buf {
     uint4 w[U], x[U];
   };
@@ -855,10 +864,9 @@ __global__ __launch_bounds__(kThreads) void gemv_mfma_kernel(GemvParams p, int G
       const int kt = min(k0 + st * U + u, k1 - 1);
       f.w[u] = load_stream(wp + (size_t)kt * kstride);
       const int kx = kt * kTileK + 8 * grp;  // K % 8 == 0: a group is wholly inside or past K
-      f.x[u] = load_g16((const uint4*)(xr + min(kx, K - 8)));
-      // columns past K, and (as a second guard) the repeated tile of a step past k1,
-      // multiply zeros
-      if (!LN && (kx >= K || k0 + st * U + u >= k1)) f.x[u] = make_uint4(0u, 0u, 0u, 0u);
+      const bool in = xlane & (kx < K) & (k0 + st * U + u < k1);  // no short circuit: no branch
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(xrs, in ? xrow + 2u * kx : kXPast, 0, 0);
+      f.x[u] = make_uint4(v.x, v.y, v.z, v.w);
     }
   };
   // LayerNorm of x on the fly: xn = x * ln_a + ln_c for this lane's batch row
@@ -1653,6 +1661,7 @@ hipError_t launch_gemv_mfma(GemvParams p, int dtype, int B, hipStream_t stream) 
   if (p.K < 8 || p.K % 8 || B < 1 || B > kLnSlots) return hipErrorInvalidValue;
   if (p.ln && (!p.ln_in || p.K > kMaxLnK)) return hipErrorInvalidValue;
   if (p.ln_out && p.y_f32) return hipErrorInvalidValue;
+  if (p.ldx < p.K || ((long long)(B - 1) * p.ldx + p.K) * 2 >= (long long)kXPast) return hipErrorInvalidValue;
   const int G = mfma_splits(p.rows, p.K);
   if (G > 1 && (!p.ws || !p.cnt || p.ws_floats < mfma_ws_floats(p.rows, p.K, B) ||
                 p.cnt_words < mfma_cnt_words(p.rows, p.K)))

@@ -186,6 +186,10 @@ def test_linear_tiled_argument_errors(ctx):
     assert call(x.data_ptr(), 1, K, Wt.data_ptr(), N, hg.F32, 0, y.data_ptr(), hg.F32, s) == hg.ERR_UNSUPPORTED
     assert call(x.data_ptr(), 1, K, Wt.data_ptr(), N, dtype, 0, y.data_ptr(), hg.BF16, s) == hg.ERR_UNSUPPORTED
     assert call(x.data_ptr() + 2, 1, K, Wt.data_ptr(), N, dtype, 0, y.data_ptr(), hg.F32, s) == hg.ERR_UNSUPPORTED
+    # x of 2^30 elements or more: refused before anything is read (x is read through a
+    # buffer descriptor with 32-bit offsets)
+    for c in (call, lambda *a: hg.hetegen_linear_tiled_noalloc_status(ctx, *a)):
+        assert c(x.data_ptr(), 8, 1 << 27, Wt.data_ptr(), N, dtype, 0, y.data_ptr(), hg.F32, s) == hg.ERR_UNSUPPORTED
     assert hg.hetegen_tiled_bytes(0, K) == 0 and hg.hetegen_tiled_bytes(N, 60) == 0
     with pytest.raises(hg.HetegenError):
         hg.hetegen_tile_weights(ctx, Wt.data_ptr(), N, 60, Wt.data_ptr(), s)
