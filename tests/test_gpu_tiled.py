@@ -113,7 +113,7 @@ def test_linear_tiled_full_size_opt_shapes(ctx, N, K, dtype, B):
 
 @pytest.mark.parametrize("dtype,N,K", [(synth.F16, 100, 2040), (synth.BF16, 40, 248), (synth.F16, 64, 16384),
                                        (synth.BF16, 33, 36864)])
-@pytest.mark.parametrize("B", [1, 8])
+@pytest.mark.parametrize("B", [1, 2, 5, 8])  # lanes of product columns past B read no x
 def test_linear_tiled_integer_inputs_bit_exact(ctx, dtype, N, K, B):
     # x, W in {-1, 0, 1}, bias in {-4..4}: every partial sum is an integer below 2^24, so any
     # summation order (the matrix core's, the split over K) gives the oracle's bits
