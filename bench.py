@@ -20,7 +20,8 @@ through the hybrid pin || transfer path (Sec. 4.2-4.3).
 The default run (no --model) measures the all-resident OPT-6.7B line above and then,
 after freeing it, the same stack at batch 8 in a model created for batch 8 (matrix-core
 tiles; `batched` in the same JSON line, 32 steps; --no-batched skips it), the full decode step
-at batch 1 with attention over a 512-position KV cache (`kv_step`, 32 steps; --no-kv skips it),
+at batch 1 with attention over a 512-position KV cache (`kv_step`, 64 decoded tokens after 3 warmup
+steps, the paper's end-to-end workload of a 512-token prompt and 64 generated tokens; --no-kv skips it),
 and the streamed
 half of the metric in the same process (`streamed` in the same JSON line; --no-streamed
 skips it): OPT-30B shapes, 48 layers, every linear in
@@ -497,7 +498,7 @@ def main():
     ap.add_argument("--no-kv", action="store_true",
                     help="default run only: skip the kv leg (the OPT-6.7B stack at batch 1 with attention over "
                          "a 512-position KV cache)")
-    ap.add_argument("--kv-steps", type=int, default=32, help="timed steps of the kv leg")
+    ap.add_argument("--kv-steps", type=int, default=64, help="timed steps of the kv leg")
     ap.add_argument("--all-streamed-steps", type=int, default=None,
                     help="streamed workloads: also time this many steps with every GPU row streamed (CPU "
                          "fraction 0), against the idle link (default: 2 in the streamed leg, 0 otherwise)")
