@@ -1620,15 +1620,16 @@ size_t mfma_cnt_words(int rows, int K) {
 }
 
 // Tiles per request: 4 with the LayerNorm prologue (fewer registers: the grid fits the
-// device at once), in split launches, at B = 1 and for long rows (K >= 16384); 8 for
-// the rest of the unsplit launches.  8 against 4 tiles per request, OPT-6.7B shapes:
-// out [4096, 4096] at B = 3 8.5 against 8.9 us, fc2 [4096, 16384] at B = 8 24.6 against
-// 23.9 us, out at B = 1 9.4 against 8.7 us.  Each wavefront sums its k-tiles in order
-// either way: the bits are the same.
+// device at once), in split launches and at B = 1; 8 for the rest of the unsplit launches.
+// 8 against 4 tiles per request, OPT-6.7B shapes: out [4096, 4096] at B = 3 8.5 against
+// 8.9 us, out at B = 1 9.4 against 8.7 us; fc2 [4096, 16384] took 4 while every lane of the
+// product loaded x (24.6 against 23.9 us at B = 8), and 8 since lanes of columns past B load
+// none (whole steps 2.354-2.357 against 2.383-2.385 ms at B = 8; OPT-30B fc2 [7168, 28672]
+// unchanged).  Each wavefront sums its k-tiles in order either way: the bits are the same.
 template <class T, int B, bool LN>
 hipError_t launch_mfma_ln(const GemvParams& p, int G, hipStream_t s) {
   const int grid = ((p.rows + kTileRows - 1) / kTileRows) * G;
-  const bool u4 = LN || G > 1 || B == 1 || (p.K + kTileK - 1) / kTileK >= 512;
+  const bool u4 = LN || G > 1 || B == 1;
   if (u4) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4, LN>), dim3(grid), dim3(kThreads), 0, s, p, G);
   else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 8, false>), dim3(grid), dim3(kThreads), 0, s, p, 1);
   return hipGetLastError();

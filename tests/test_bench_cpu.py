@@ -67,5 +67,7 @@ def test_kernel_labels_follow_the_measured_rules():
             os.environ["HETEGEN_LN_PARTIALS"] = env
     label = bench.gemv_label(8, 4096, 16384, 0, True, True, 256)
     assert "k-major" in label and "K split" not in label
+    # unsplit linears without the LayerNorm take 8 tiles per request at B >= 2, whatever K
+    assert "gemv_mfma_kernel<F16,8,8> k-major: layer 0's qkv, out, fc2" in label
     label = bench.gemv_label(8, 9216, 36864, 1, True, False, 256)
     assert "K split 2" in label and "k-major" not in label and "LayerNorm from partials" not in label
