@@ -409,9 +409,10 @@ def gemv_label(B, H, F, dt, tiled, partials=True, cus=256):
             wgs = -(-n // 16) * g
             kmajor = wgs % cus == 0 and wgs // cus <= 4  # the library's tile order rule
             split = ("" if g == 1 else " (K split %d)" % g) + (" k-major" if kmajor else "")
-            u = 4 if (g > 1 or B == 1) else 8  # tiles per request, no LayerNorm
+            u = 4 if g > 1 else 8  # tiles per request, no LayerNorm
             if partials and name in ("qkv", "fc1"):
-                key = "gemv_mfma_kernel<%s,%d,4,LayerNorm from partials>%s" % (t, B, split)
+                uln = 8 if (g == 1 and B == 1 and -(-wgs // cus) <= 3) else 4  # with the LayerNorm prologue
+                key = "gemv_mfma_kernel<%s,%d,%d,LayerNorm from partials>%s" % (t, B, uln, split)
                 parts.setdefault(key, []).append("qkv after layer 0" if name == "qkv" else name)
                 if name == "qkv":
                     key = "gemv_mfma_kernel<%s,%d,%d>%s" % (t, B, u, split)

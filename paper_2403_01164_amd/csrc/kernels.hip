@@ -1619,18 +1619,23 @@ size_t mfma_cnt_words(int rows, int K) {
   return (size_t)((rows + kTileRows - 1) / kTileRows);
 }
 
-// Tiles per request: 4 with the LayerNorm prologue (fewer registers: the grid fits the
-// device at once), in split launches and at B = 1; 8 for the rest of the unsplit launches.
-// 8 against 4 tiles per request, OPT-6.7B shapes: out [4096, 4096] at B = 3 8.5 against
-// 8.9 us, out at B = 1 9.4 against 8.7 us; fc2 [4096, 16384] took 4 while every lane of the
-// product loaded x (24.6 against 23.9 us at B = 8), and 8 since lanes of columns past B load
-// none (whole steps 2.354-2.357 against 2.383-2.385 ms at B = 8; OPT-30B fc2 [7168, 28672]
-// unchanged).  Each wavefront sums its k-tiles in order either way: the bits are the same.
+// Tiles per request: 4 in split launches and with the LayerNorm prologue (fewer registers)
+// from B = 2 on or when the grid puts more than 3 workgroups on a CU (142-146 VGPRs with 8
+// allow 3 wavefronts per SIMD); 8 otherwise.  Measured on OPT-6.7B shapes: fc2 [4096,
+// 16384] took 4 while every lane of the product loaded x (24.6 against 23.9 us at B = 8),
+// and 8 since lanes of columns past B load none (whole steps 2.354-2.357 against
+// 2.383-2.385 ms at B = 8; OPT-30B fc2 [7168, 28672] unchanged); qkv with the prologue at
+// B = 8 with 8: 2.370-2.374 against 2.356-2.357 ms per step; at B = 1 on tiles (a model
+// without the row-major copy), 8 for every unsplit linear but fc1 (4 workgroups per CU):
+// 2.260-2.265 against 2.279-2.282 ms.  Each wavefront sums its k-tiles in order either way:
+// the bits are the same.
 template <class T, int B, bool LN>
 hipError_t launch_mfma_ln(const GemvParams& p, int G, hipStream_t s) {
   const int grid = ((p.rows + kTileRows - 1) / kTileRows) * G;
-  const bool u4 = LN || G > 1 || B == 1;
+  const int cus = device_cus();
+  const bool u4 = G > 1 || (LN && (B > 1 || (grid + cus - 1) / cus > 3));
   if (u4) hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 4, LN>), dim3(grid), dim3(kThreads), 0, s, p, G);
+  else if (LN) hipLaunchKernelGGL((gemv_mfma_kernel<T, 1, 8, true>), dim3(grid), dim3(kThreads), 0, s, p, 1);
   else hipLaunchKernelGGL((gemv_mfma_kernel<T, B, 8, false>), dim3(grid), dim3(kThreads), 0, s, p, 1);
   return hipGetLastError();
 }
