@@ -9,8 +9,11 @@
 // is bound by HBM bandwidth (2 * (pos + 1) * D * 2 bytes per (b, h)), not by
 // arithmetic; no matrix cores.
 //
-// Split over positions: workgroup (c, h, b) takes the 64 positions of chunk c,
-// 4 wavefronts x 64 / (D / 8) positions per round (D / 8 lanes hold one 16-byte
+// Split over positions: workgroup (c, h, b) takes the 64 positions of chunk c (128
+// from 2048 cached positions on: fewer partials to merge, 13-35 % faster at 2048 and
+// 4096 positions, slower below at batch 8; the size depends on the position alone, so a
+// batch row's bits do not depend on the batch size), 4 wavefronts x 64 / (D / 8) positions
+// per round (D / 8 lanes hold one 16-byte
 // slice each of a key or value row, so a load instruction reads whole 256-byte
 // rows, coalesced).  It keeps (max score, sum of exponentials, weighted sum of V)
 // of its chunk; the last workgroup of (b, h) to finish (an arrival counter, no
@@ -28,7 +31,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kChunk = 64;       // positions per workgroup
+constexpr int kChunk = 64;       // positions per workgroup, short caches
+constexpr int kLongChunk = 128;  // positions per workgroup from kLongFrom positions on
+constexpr int kLongFrom = 2048;
 constexpr int kMaxChunks = 256;  // chunks the merge holds in LDS (positions <= 16384)
 constexpr int kMergeRegs = 16;   // chunks whose partial outputs the merge requests at once
 
@@ -85,13 +90,14 @@ __device__ __forceinline__ float wave_add(float v) {
   return v;
 }
 
-template <class T, int D>
+template <class T, int D, int CH>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams a) {
   constexpr int LP = D / 8;          // lanes per key/value row
   constexpr int PPW = 64 / LP;       // rows per wavefront per round
   constexpr int PPR = PPW * kWaves;  // rows per workgroup per round
-  constexpr int ROUNDS = kChunk / PPR;
-  __shared__ float sp[kChunk];
+  constexpr int ROUNDS = CH / PPR;
+  constexpr int SPL = CH / 64;       // scores per lane of the softmax wavefront
+  __shared__ float sp[CH];
   __shared__ float sacc[kWaves][D];
   __shared__ float sml[2];
   __shared__ float s_m[kMaxChunks], s_l[kMaxChunks];
@@ -107,7 +113,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams a) {
   const size_t head = ((size_t)b * a.heads + h) * a.max_seq;
   uint16_t* Kc = (uint16_t*)a.kc + head * D;
   uint16_t* Vc = (uint16_t*)a.vc + head * D;
-  const int j0 = c * kChunk;
+  const int j0 = c * CH;
 
   // every key and value row of the chunk is requested at once (positions past pos
   // reread the new token's row and are masked below); position pos comes from qkv
@@ -144,12 +150,22 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams a) {
     if (sub == 0) sp[jl] = j0 + jl <= a.pos ? s : -INFINITY;
   }
   __syncthreads();
-  if (wave == 0) {  // kChunk == 64: one score per lane
-    const float s = sp[lane];
-    const float m = wave_max(s);
-    const float p = s == -INFINITY ? 0.f : expf(s - m);
-    const float l = wave_add(p);
-    sp[lane] = p;
+  if (wave == 0) {  // scores lane + 64 i of the chunk
+    float sv[SPL], mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      sv[i] = sp[lane + 64 * i];
+      mx = fmaxf(mx, sv[i]);
+    }
+    const float m = wave_max(mx);
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      const float p = sv[i] == -INFINITY ? 0.f : expf(sv[i] - m);
+      sp[lane + 64 * i] = p;
+      ps += p;
+    }
+    const float l = wave_add(ps);
     if (lane == 0) {
       sml[0] = m;
       sml[1] = l;
@@ -208,8 +224,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams a) {
   }
   __syncthreads();
   if (!s_last) return;
-  // merge, in chunk order: every partial is requested at once (one memory round trip
-  // for up to kMergeRegs chunks), m and l through LDS
+  // merge, in chunk order: the partials are requested kMergeRegs chunks at a time (one
+  // memory round trip per kMergeRegs chunks), m and l through LDS
   auto ld = [&](int i) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, i * 4, 0, kCoherent));
   };
@@ -227,28 +243,29 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams a) {
     float M = -INFINITY;
     for (int k = 0; k < a.nchunk; ++k) M = fmaxf(M, s_m[k]);
     float L = 0.f, O = 0.f;
+    for (int k0 = 0; k0 < a.nchunk; k0 += kMergeRegs) {
+      if (k0 > 0) {
 #pragma unroll
-    for (int u = 0; u < kMergeRegs; ++u) {
-      if (u < a.nchunk) {
-        const float w = expf(s_m[u] - M);
-        L = fmaf(s_l[u], w, L);
-        O = fmaf(ov[u], w, O);
+        for (int u = 0; u < kMergeRegs; ++u) ov[u] = k0 + u < a.nchunk ? ld((k0 + u) * (D + 2) + 2 + t) : 0.f;
       }
-    }
-    for (int k = kMergeRegs; k < a.nchunk; ++k) {
-      const float w = expf(s_m[k] - M);
-      L = fmaf(s_l[k], w, L);
-      O = fmaf(ld(k * (D + 2) + 2 + t), w, O);
+#pragma unroll
+      for (int u = 0; u < kMergeRegs; ++u) {
+        if (k0 + u < a.nchunk) {
+          const float w = expf(s_m[k0 + u] - M);
+          L = fmaf(s_l[k0 + u], w, L);
+          O = fmaf(ov[u], w, O);
+        }
+      }
     }
     out[t] = T::from_f32(O / L);
   }
 }
 
-template <class T>
+template <class T, int CH>
 hipError_t launch_t(const AttnParams& a, int B, hipStream_t s) {
   const dim3 grid(a.nchunk, a.heads, B);
-  if (a.head_dim == 128) hipLaunchKernelGGL((attn_kernel<T, 128>), grid, dim3(kThreads), 0, s, a);
-  else hipLaunchKernelGGL((attn_kernel<T, 64>), grid, dim3(kThreads), 0, s, a);
+  if (a.head_dim == 128) hipLaunchKernelGGL((attn_kernel<T, 128, CH>), grid, dim3(kThreads), 0, s, a);
+  else hipLaunchKernelGGL((attn_kernel<T, 64, CH>), grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -261,10 +278,13 @@ int attn_max_positions() { return kChunk * kMaxChunks; }
 hipError_t launch_attention(AttnParams a, int dtype, int B, hipStream_t stream) {
   if (B < 1 || a.pos < 0 || a.pos >= a.max_seq || (a.head_dim != 64 && a.head_dim != 128) || a.heads < 1)
     return hipErrorInvalidValue;
-  a.nchunk = (a.pos + kChunk) / kChunk;  // chunks covering positions [0, pos]
+  const bool lng = a.pos + 1 >= kLongFrom;
+  const int ch = lng ? kLongChunk : kChunk;
+  a.nchunk = (a.pos + ch) / ch;  // chunks covering positions [0, pos]
   if (a.nchunk > a.max_chunks || a.nchunk > kMaxChunks) return hipErrorInvalidValue;
   a.scale = 1.0f / sqrtf((float)a.head_dim);
-  return dtype == 1 ? launch_t<BF16>(a, B, stream) : launch_t<F16>(a, B, stream);
+  if (lng) return dtype == 1 ? launch_t<BF16, kLongChunk>(a, B, stream) : launch_t<F16, kLongChunk>(a, B, stream);
+  return dtype == 1 ? launch_t<BF16, kChunk>(a, B, stream) : launch_t<F16, kChunk>(a, B, stream);
 }
 
 }  // namespace hg

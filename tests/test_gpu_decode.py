@@ -687,13 +687,14 @@ def test_kv_argument_errors(ctx):
         m.free()
 
 
-@pytest.mark.parametrize("P", [1023, 1100])
+@pytest.mark.parametrize("P", [1023, 1100, 2046, 2047, 2175])
 def test_kv_long_context_merge(ctx, P):
-    # more chunks than the merge requests at once (16 x 64 positions)
+    # more chunks than the merge requests at once (16 x 64 positions), and around the
+    # switch to 128-position chunks at 2048 positions (2175: 17 chunks of 128)
     dtype, L, H, F, B, D = synth.BF16, 1, 256, 512, 2, 128
     m = Model(ctx, L, H, F, dtype, 0.0, 1)
     try:
-        hg.hetegen_model_kv_create(ctx, m.m, 1200, D)
+        hg.hetegen_model_kv_create(ctx, m.m, 2200, D)
         kc, vc = _fill_cache(m, B, P)
         x = synth.normal((B, H), dtype, 0, synth.act_id(P))
         out, tr = m.step_kv(x, P, trace=True)
