@@ -28,7 +28,9 @@ struct AttnParams {
   float scale;  // set by the launcher: 1 / sqrt(head_dim)
 };
 
-// Positions per workgroup of the attention kernel.
+// Positions per workgroup of the attention kernel for short caches (the smallest chunk:
+// a partial buffer of ceil(max_seq / attn_chunk()) chunks per (batch, head) holds any
+// position's chunks).
 int attn_chunk();
 
 // Largest cache (positions) the attention kernel supports.
