@@ -342,10 +342,12 @@ HETEGEN_API hetegen_status hetegen_module_schedule(const double* t_cpu, const do
  * 1 they are row-major and run on the vector GEMV (fused LayerNorm, the faster
  * kernels at batch 1); with max_batch >= 2 they are stored in matrix-core tile
  * order and batches of 2 and more run on the matrix-core GEMV (see
- * hetegen_linear_tiled; the model also owns its split-K workspace).  Such a model
- * also keeps the row-major copy, and runs batch 1 from it, when both copies
- * take at most half of the device memory free at creation (the environment
- * variable HETEGEN_DUAL_LAYOUT=0 at creation keeps the tile order only);
+ * hetegen_linear_tiled; the model also owns its split-K workspace).  Up to a
+ * hidden size of 6144 such a model also keeps the row-major copy, and runs batch 1
+ * from it, when both copies take at most half of the device memory free at creation;
+ * above 6144 batch 1 runs on the tiles too, which is faster there (the environment
+ * variable HETEGEN_DUAL_LAYOUT=0 / 1 at creation: tile order only / the row-major copy
+ * too at any hidden size, memory allowing);
  * hetegen_model_layouts tells which copies a model holds.  On the matrix-core path,
  * when out (fc2) and the fc1 (next qkv) after it run every row on the GPU, out / fc2
  * also leave per-16-element LayerNorm partials of their output (sum, sum of squared

@@ -77,6 +77,13 @@ constexpr int kTiledMinBatch = 2;
 // 5.727 / 5.113 against 5.584 / 5.115).  The choice depends on H alone, so that a batch row's
 // bits do not depend on the batch size.
 constexpr int kMaxPartialsH = 6144;
+// Largest hidden size at which a model created for batches of 2 or more keeps a row-major
+// copy beside its tiles for batch 1: above it batch 1 is faster on the tiles (all linears
+// resident, created for batch 8, batch 1 per step: OPT-13B, H = 5120, 4.245 / 4.247 ms on
+// the row-major copy against 4.302 / 4.304 on the tiles; OPT-30B, 7168, 9.450 / 9.452 against
+// 9.293 / 9.294; OPT-66B, 9216, whose copies would not both fit, 20.18 ms on the tiles against
+// 20.36-20.44 for a row-major model), and the tiles alone take half the memory.
+constexpr int kMaxDualH = 6144;
 // Resident row-major copies (batch 1) of GPU-only linears with K >= kMinSegmajorK (and K a
 // multiple of hg::kSegElems) are stored segment-major: the batch-1 GEMV walks each row in
 // 2048-element segments, every wavefront its own row, so in row-major order the wavefronts'
@@ -2021,13 +2028,13 @@ hetegen_status hetegen_model_create(hetegen_ctx* ctx, int L, int H, int F, heteg
       const char* lp = getenv("HETEGEN_LN_PARTIALS");
       m->ln_partials = lp && strcmp(lp, "0") == 0 ? false : lp && strcmp(lp, "1") == 0 ? true : H <= kMaxPartialsH;
     }
-    // A tiled model also keeps the row-major copy, for batch 1 on the vector GEMV, when
-    // both copies take at most half of the device memory free now (HETEGEN_DUAL_LAYOUT=0 at
-    // creation: tile order only)
+    // A tiled model with H <= kMaxDualH also keeps the row-major copy, for batch 1 on the
+    // vector GEMV, when both copies take at most half of the device memory free now
+    // (HETEGEN_DUAL_LAYOUT=0 / 1 at creation: tile order only / the row-major copy at any H)
     if (m->tiled && rm_bytes) {
       size_t free_b = 0, total_b = 0;
       const char* de = getenv("HETEGEN_DUAL_LAYOUT");
-      const bool allow = !(de && strcmp(de, "0") == 0);
+      const bool allow = de && strcmp(de, "0") == 0 ? false : de && strcmp(de, "1") == 0 ? true : H <= kMaxDualH;
       if (allow && hipMemGetInfo(&free_b, &total_b) == hipSuccess && rm_bytes + tile_bytes <= free_b / 2)
         m->rowmajor = true;
       (void)hipGetLastError();
